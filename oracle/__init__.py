@@ -1,0 +1,280 @@
+"""fp64 CPU oracle of the SPDP snapshot-parallel Gibbs sweep (ctypes binding).
+
+TEST INFRASTRUCTURE ONLY: imported by the tests, the smoke check and the CPU
+baseline leg of the benchmark, never by the product library.  It shares no code
+with the HIP path.  The arithmetic lives in ``oracle.c``; this module only
+marshals numpy arrays.
+
+Model: Li (2012), arXiv:1510.06549, chapter "Shared Topic Modelling Using
+Shadow Poisson Dirichlet Process" with identity transformation matrices:
+conditionals Eq. SPDP-sampling-w-z-r0 / Eq. SPDP-sampling-w-z-r1, sequential
+semantics Algorithm SPDP-Full-Gibbs, joint from the blocked-Gibbs derivation.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "oracle.c")
+_LIB_PATH = os.path.join(_HERE, "liboracle.so")
+
+PURPOSE_SAMPLE = 0
+PURPOSE_INIT = 1
+
+
+def build(force: bool = True) -> str:
+    """Compile oracle.c into liboracle.so (gcc, -O2, OpenMP)."""
+    if force or not os.path.exists(_LIB_PATH):
+        tmp = _LIB_PATH + ".tmp"
+        subprocess.check_call(
+            ["gcc", "-O2", "-fopenmp", "-fPIC", "-shared", _SRC, "-lm", "-o", tmp]
+        )
+        os.replace(tmp, _LIB_PATH)
+    return _LIB_PATH
+
+
+class _Model(C.Structure):
+    _fields_ = [
+        ("n_tokens", C.c_int64),
+        ("n_docs", C.c_int32),
+        ("vocab", C.c_int32),
+        ("n_groups", C.c_int32),
+        ("K", C.c_int32),
+        ("words", C.c_void_p),
+        ("doc_off", C.c_void_p),
+        ("doc_group", C.c_void_p),
+        ("alpha", C.c_double),
+        ("a", C.c_double),
+        ("b", C.c_double),
+        ("gam", C.c_double),
+        ("ncap", C.c_int32),
+        ("logS", C.c_void_p),
+    ]
+
+
+class _Counts(C.Structure):
+    _fields_ = [
+        ("n", C.c_void_p),
+        ("t", C.c_void_p),
+        ("Ngk", C.c_void_p),
+        ("Tgk", C.c_void_p),
+        ("Bkw", C.c_void_p),
+        ("Bk", C.c_void_p),
+    ]
+
+
+_lib = None
+
+
+def lib():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB_PATH):
+            build(force=True)
+        L = C.CDLL(_LIB_PATH)
+        vp, i32, i64, u32, u64, dbl = C.c_void_p, C.c_int32, C.c_int64, C.c_uint32, C.c_uint64, C.c_double
+        L.or_philox4x32_10.argtypes = [vp, vp, vp]
+        L.or_philox4x32_10.restype = None
+        L.or_philox_word0.argtypes = [u64, i64, u32, u32]
+        L.or_philox_word0.restype = u32
+        L.or_uniform.argtypes = [u64, i64, u32]
+        L.or_uniform.restype = dbl
+        L.or_stirling_log_table.argtypes = [i32, dbl, vp]
+        L.or_stirling_log_table.restype = C.c_int
+        L.or_init.argtypes = [vp, u64, vp, vp]
+        L.or_init.restype = None
+        L.or_rebuild.argtypes = [vp, vp, vp, vp]
+        L.or_rebuild.restype = None
+        L.or_repair.argtypes = [vp, vp, vp, vp]
+        L.or_repair.restype = i64
+        L.or_token_weights.argtypes = [vp, vp, vp, i32, i32, i32, i32, vp]
+        L.or_token_weights.restype = C.c_int
+        L.or_sample_docs.argtypes = [vp, vp, vp, vp, u32, u64, i32, i32, vp, vp, vp, i64, i64]
+        L.or_sample_docs.restype = i64
+        L.or_sweep.argtypes = [vp, vp, vp, vp, u32, u64, C.c_int, vp]
+        L.or_sweep.restype = C.c_int
+        L.or_loglik.argtypes = [vp, vp, vp, vp]
+        L.or_loglik.restype = dbl
+        L.or_max_group_word_count.argtypes = [vp]
+        L.or_max_group_word_count.restype = i32
+        L.or_chain_histogram.argtypes = [vp, vp, vp, vp, u32, i64, u64, C.c_int, vp, i64]
+        L.or_chain_histogram.restype = C.c_int
+        L.or_num_threads.argtypes = []
+        L.or_num_threads.restype = C.c_int
+        _lib = L
+    return _lib
+
+
+def _p(a: np.ndarray):
+    return a.ctypes.data_as(C.c_void_p)
+
+
+# --------------------------------------------------------------------------
+# Philox and Stirling
+# --------------------------------------------------------------------------
+def philox4x32_10(ctr, key) -> np.ndarray:
+    c = np.ascontiguousarray(ctr, dtype=np.uint32)
+    k = np.ascontiguousarray(key, dtype=np.uint32)
+    out = np.zeros(4, dtype=np.uint32)
+    lib().or_philox4x32_10(_p(c), _p(k), _p(out))
+    return out
+
+
+def philox_word0(seed: int, i: int, sweep: int, purpose: int) -> int:
+    return int(lib().or_philox_word0(seed, i, sweep, purpose))
+
+
+def uniform(seed: int, i: int, sweep: int) -> float:
+    return float(lib().or_uniform(seed, i, sweep))
+
+
+def stirling_log_table(nmax: int, a: float) -> np.ndarray:
+    """Triangle of log S^n_{t,a}, 0 <= t <= n <= nmax; row n starts at n(n+1)/2."""
+    out = np.empty((nmax + 1) * (nmax + 2) // 2, dtype=np.float64)
+    if lib().or_stirling_log_table(nmax, a, _p(out)) != 0:
+        raise ValueError("bad Stirling table arguments")
+    return out
+
+
+def tri(n: int, t: int) -> int:
+    return n * (n + 1) // 2 + t
+
+
+# --------------------------------------------------------------------------
+# Model + counts
+# --------------------------------------------------------------------------
+class Model:
+    """A corpus with hyperparameters and the fp64 Stirling table it needs."""
+
+    def __init__(self, words, doc_off, doc_group, n_groups, K, vocab, alpha, a, b, gamma,
+                 ncap: int | None = None):
+        self.words = np.ascontiguousarray(words, dtype=np.int32)
+        self.doc_off = np.ascontiguousarray(doc_off, dtype=np.int64)
+        self.doc_group = np.ascontiguousarray(doc_group, dtype=np.int32)
+        self.N = int(self.words.shape[0])
+        self.D = int(self.doc_group.shape[0])
+        self.G, self.K, self.V = int(n_groups), int(K), int(vocab)
+        self.alpha, self.a, self.b, self.gamma = float(alpha), float(a), float(b), float(gamma)
+        assert self.doc_off.shape[0] == self.D + 1 and self.doc_off[-1] == self.N
+        self._m = _Model()
+        m = self._m
+        m.n_tokens, m.n_docs, m.vocab, m.n_groups, m.K = self.N, self.D, self.V, self.G, self.K
+        m.words, m.doc_off, m.doc_group = (_p(self.words).value, _p(self.doc_off).value,
+                                           _p(self.doc_group).value)
+        m.alpha, m.a, m.b, m.gam = self.alpha, self.a, self.b, self.gamma
+        if ncap is None:
+            ncap = int(lib().or_max_group_word_count(C.byref(m))) if self.N else 0
+        self.ncap = int(ncap)
+        self.logS = stirling_log_table(self.ncap + 1, self.a)
+        m.ncap = self.ncap + 1
+        m.logS = _p(self.logS).value
+
+    @property
+    def ref(self):
+        return C.byref(self._m)
+
+    def new_counts(self) -> "Counts":
+        return Counts(self.G, self.K, self.V)
+
+    # ---- operations ----
+    def init(self, init_seed: int):
+        z = np.empty(self.N, dtype=np.int32)
+        r = np.empty(self.N, dtype=np.uint8)
+        lib().or_init(self.ref, init_seed, _p(z), _p(r))
+        return z, r
+
+    def rebuild(self, z, r, counts: "Counts | None" = None) -> "Counts":
+        c = counts if counts is not None else self.new_counts()
+        lib().or_rebuild(self.ref, _p(z), _p(r), c.ref)
+        return c
+
+    def repair(self, z, r, counts: "Counts") -> int:
+        return int(lib().or_repair(self.ref, _p(z), _p(r), counts.ref))
+
+    def initial_state(self, init_seed: int):
+        """Philox-uniform topics, r = 0, rebuild, repair (one head per non-empty cell)."""
+        z, r = self.init(init_seed)
+        c = self.rebuild(z, r)
+        self.repair(z, r, c)
+        return z, r, c
+
+    def token_weights(self, counts: "Counts", crow, g, w, k0, r0):
+        """2K weights (None if the sole-head point mass applies)."""
+        out = np.zeros(2 * self.K, dtype=np.float64)
+        crow = np.ascontiguousarray(crow, dtype=np.int32)
+        skip = lib().or_token_weights(self.ref, counts.ref, _p(crow), int(g), int(w), int(k0),
+                                      int(r0), _p(out))
+        return None if skip else out
+
+    def sample_docs(self, counts, z, r, sweep, seed, d_begin=0, d_end=None, trace=None):
+        """Sampling step over documents [d_begin, d_end) against `counts` (read only).
+
+        trace = (tok_begin, tok_end) returns (changed, w[T,2K], u[T], skip[T]).
+        """
+        if d_end is None:
+            d_end = self.D
+        if trace is None:
+            ch = lib().or_sample_docs(self.ref, counts.ref, _p(z), _p(r), sweep, seed, d_begin,
+                                      d_end, None, None, None, 0, 0)
+            return int(ch)
+        tb, te = trace
+        T = te - tb
+        tw = np.zeros((T, 2 * self.K), dtype=np.float64)
+        tu = np.full(T, np.nan, dtype=np.float64)
+        ts = np.zeros(T, dtype=np.uint8)
+        ch = lib().or_sample_docs(self.ref, counts.ref, _p(z), _p(r), sweep, seed, d_begin, d_end,
+                                  _p(tw), _p(tu), _p(ts), tb, te)
+        return int(ch), tw, tu, ts
+
+    def sweep(self, counts, z, r, sweep, seed, mode: str = "snapshot"):
+        stats = np.zeros(2, dtype=np.int64)
+        rc = lib().or_sweep(self.ref, counts.ref, _p(z), _p(r), sweep, seed,
+                            0 if mode == "snapshot" else 1, _p(stats))
+        if rc != 0:
+            raise ValueError(mode)
+        return int(stats[0]), int(stats[1])
+
+    def chain_histogram(self, counts, z, r, first_sweep, n_sweeps, seed, mode="sequential"):
+        """Visit counts of encoded states over `n_sweeps` sweeps (tiny corpora only)."""
+        n_bins = (2 * self.K) ** self.N
+        hist = np.zeros(n_bins, dtype=np.int64)
+        rc = lib().or_chain_histogram(self.ref, counts.ref, _p(z), _p(r), first_sweep, n_sweeps,
+                                      seed, 0 if mode == "snapshot" else 1, _p(hist), n_bins)
+        if rc != 0:
+            raise RuntimeError(f"or_chain_histogram failed ({rc})")
+        return hist
+
+    def loglik(self, z, r, counts: "Counts") -> float:
+        return float(lib().or_loglik(self.ref, _p(z), _p(r), counts.ref))
+
+
+class Counts:
+    """Count arrays in the thesis's logical layout: n[g, k, w], t[g, k, w]."""
+
+    def __init__(self, G, K, V):
+        self.n = np.zeros((G, K, V), dtype=np.int32)
+        self.t = np.zeros((G, K, V), dtype=np.int32)
+        self.Ngk = np.zeros((G, K), dtype=np.int32)
+        self.Tgk = np.zeros((G, K), dtype=np.int32)
+        self.Bkw = np.zeros((K, V), dtype=np.int32)
+        self.Bk = np.zeros(K, dtype=np.int32)
+        self._c = _Counts(_p(self.n).value, _p(self.t).value, _p(self.Ngk).value,
+                          _p(self.Tgk).value, _p(self.Bkw).value, _p(self.Bk).value)
+
+    @property
+    def ref(self):
+        return C.byref(self._c)
+
+    def copy(self) -> "Counts":
+        c = Counts(*self.n.shape)
+        for f in ("n", "t", "Ngk", "Tgk", "Bkw", "Bk"):
+            getattr(c, f)[...] = getattr(self, f)
+        return c
+
+
+def num_threads() -> int:
+    return int(lib().or_num_threads())

@@ -1,0 +1,516 @@
+/*
+ * oracle.c -- plain fp64 CPU oracle of the SPDP snapshot-parallel Gibbs sweep.
+ *
+ * TEST INFRASTRUCTURE ONLY.  Nothing in the product path links, loads or calls
+ * this file: only the test suite, the smoke check and the CPU-baseline leg of
+ * the benchmark do.  It shares no code, header, table or constant generator
+ * with the HIP library; its own Philox and Stirling table are written here from
+ * their published definitions.
+ *
+ * Model: Li (2012), "Multi-GPU Distributed Parallel Bayesian Differential Topic
+ * Modelling" (arXiv:1510.06549), chapter "Shared Topic Modelling Using Shadow
+ * Poisson Dirichlet Process", with every transformation matrix P^i = I (the
+ * setting of the thesis's experiments, section "MGPU-DP-SPDP" / identity P).
+ * Then the word-association variables v collapse, q = t, and p_{i,w,v} = 1.
+ *
+ * Notation (thesis -> here):
+ *   m_{ikw}  customers of word w at restaurant (group i, topic k)  -> n[g][k][w]
+ *   t_{ikw}  tables ("multiplicity") of word w at (i,k)            -> t[g][k][w]
+ *   n_{idk}  tokens of document d with topic k                     -> ndk / c[k]
+ *   m_{ik.}, t_{ik.}                                               -> Ngk, Tgk
+ *   sum_i t_{ikw} (shadow-base table counts), sum over w           -> Bkw, Bk
+ *   alpha_{ik} (doc prior), a_k (discount), b_k (concentration),
+ *   gamma_v (base prior)                                           -> alpha, a, b, gam
+ *
+ * Readings of passages the thesis leaves open (each one is listed in the
+ * design notes of the repository):
+ *   - shared counts come from a snapshot taken at sweep start; the document's
+ *     own doc-topic row is live and its tokens run in index order;
+ *   - r is stored per token; removal uses the stored r;
+ *   - removing the only head of a cell that still has other customers has
+ *     joint probability zero for every alternative, so the token keeps its
+ *     state (point mass) and no uniform is consumed;
+ *   - after the sweep, counts are rebuilt from (z, r) and every cell with
+ *     n > 0 and t = 0 gets its smallest-index token promoted to head;
+ *   - outcome j = 2k is (k, r=1), j = 2k+1 is (k, r=0) (even/odd work-item
+ *     convention of the thesis's ParallelSampleWord kernel); the draw takes
+ *     the first j whose inclusive prefix sum exceeds u * total;
+ *   - uniforms come from Philox4x32-10 keyed by the seed, counter =
+ *     (token lo, token hi, sweep, purpose); u = (x0 >> 8) * 2^-24.
+ *
+ * Build:  gcc -O2 -fopenmp -fPIC -shared oracle.c -lm -o liboracle.so
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+#ifdef _OPENMP
+#include <omp.h>
+#endif
+
+#define OR_PURPOSE_SAMPLE 0u
+#define OR_PURPOSE_INIT 1u
+
+/* ------------------------------------------------------------------------ */
+/* Model description.  All arrays are owned by the caller.                   */
+/* ------------------------------------------------------------------------ */
+typedef struct {
+    int64_t n_tokens;
+    int32_t n_docs, vocab, n_groups, K;
+    const int32_t *words;     /* [N]   word id per token                     */
+    const int64_t *doc_off;   /* [D+1] CSR offsets of documents               */
+    const int32_t *doc_group; /* [D]   group of each document                 */
+    double alpha, a, b, gam;  /* doc prior, PYP discount, PYP conc., base prior */
+    int32_t ncap;             /* the Stirling table covers 0 <= t <= n <= ncap */
+    const double *logS;       /* triangle, row n at n(n+1)/2                   */
+} or_model;
+
+/* Counts, logical layout of the thesis: n_{i,k,w} -> n[(g*K + k)*V + w]. */
+typedef struct {
+    int32_t *n, *t;     /* [G][K][V] */
+    int32_t *Ngk, *Tgk; /* [G][K]    */
+    int32_t *Bkw;       /* [K][V]    */
+    int32_t *Bk;        /* [K]       */
+} or_counts;
+
+static inline int64_t tri(int64_t n, int64_t t) { return n * (n + 1) / 2 + t; }
+
+/* ------------------------------------------------------------------------ */
+/* Philox4x32-10 (Salmon, Moraes, Dror, Shaw, "Parallel random numbers: as   */
+/* easy as 1, 2, 3", SC'11): 10 rounds of the 4x32 Philox S-box with the     */
+/* Weyl key schedule.                                                        */
+/* ------------------------------------------------------------------------ */
+void or_philox4x32_10(const uint32_t ctr_in[4], const uint32_t key_in[2], uint32_t out[4])
+{
+    const uint32_t M0 = 0xD2511F53u, M1 = 0xCD9E8D57u;
+    const uint32_t W0 = 0x9E3779B9u, W1 = 0xBB67AE85u;
+    uint32_t c0 = ctr_in[0], c1 = ctr_in[1], c2 = ctr_in[2], c3 = ctr_in[3];
+    uint32_t k0 = key_in[0], k1 = key_in[1];
+    for (int round = 0; round < 10; ++round) {
+        if (round > 0) { k0 += W0; k1 += W1; }
+        uint64_t p0 = (uint64_t)M0 * c0;
+        uint64_t p1 = (uint64_t)M1 * c2;
+        uint32_t hi0 = (uint32_t)(p0 >> 32), lo0 = (uint32_t)p0;
+        uint32_t hi1 = (uint32_t)(p1 >> 32), lo1 = (uint32_t)p1;
+        uint32_t n0 = hi1 ^ c1 ^ k0;
+        uint32_t n2 = hi0 ^ c3 ^ k1;
+        c0 = n0; c1 = lo1; c2 = n2; c3 = lo0;
+    }
+    out[0] = c0; out[1] = c1; out[2] = c2; out[3] = c3;
+}
+
+/* First output word for (seed; token i, sweep, purpose). */
+uint32_t or_philox_word0(uint64_t seed, int64_t i, uint32_t sweep, uint32_t purpose)
+{
+    uint32_t ctr[4] = {(uint32_t)(uint64_t)i, (uint32_t)((uint64_t)i >> 32), sweep, purpose};
+    uint32_t key[2] = {(uint32_t)seed, (uint32_t)(seed >> 32)};
+    uint32_t out[4];
+    or_philox4x32_10(ctr, key, out);
+    return out[0];
+}
+
+/* 24-bit uniform in [0,1): exact in both fp32 and fp64. */
+double or_uniform(uint64_t seed, int64_t i, uint32_t sweep)
+{
+    uint32_t x = or_philox_word0(seed, i, sweep, OR_PURPOSE_SAMPLE);
+    return (double)(x >> 8) * (1.0 / 16777216.0);
+}
+
+/* ------------------------------------------------------------------------ */
+/* Generalised Stirling numbers S^n_{t,a} (thesis, section on the SPDP joint, */
+/* the Corollary 17 passage): S^{n+1}_{t} = S^n_{t-1} + (n - t a) S^n_t,      */
+/* S^n_t = 0 for t > n, S^n_0 = delta_{n,0}.  Tabulated as log S in fp64,     */
+/* -inf where S = 0.  Output: triangle of (nmax+1)(nmax+2)/2 doubles.        */
+/* ------------------------------------------------------------------------ */
+static double log_add(double x, double y)
+{
+    if (x == -INFINITY) return y;
+    if (y == -INFINITY) return x;
+    double m = x > y ? x : y;
+    return m + log1p(exp(-fabs(x - y)));
+}
+
+int or_stirling_log_table(int32_t nmax, double a, double *logS)
+{
+    if (nmax < 0 || !(a >= 0.0 && a < 1.0) || !logS) return -1;
+    logS[0] = 0.0; /* S^0_0 = 1 */
+    for (int64_t n = 0; n < nmax; ++n) {
+        const double *row = logS + tri(n, 0);
+        double *next = logS + tri(n + 1, 0);
+        next[0] = -INFINITY; /* S^{n+1}_0 = 0 */
+        for (int64_t t = 1; t <= n + 1; ++t) {
+            double from_left = row[t - 1];                        /* S^n_{t-1} */
+            double from_same = (t <= n) ? row[t] : -INFINITY;     /* S^n_t     */
+            double term = (from_same == -INFINITY) ? -INFINITY
+                                                   : log((double)n - (double)t * a) + from_same;
+            next[t] = log_add(from_left, term);
+        }
+    }
+    return 0;
+}
+
+static inline double log_stirling(const or_model *m, int64_t n, int64_t t)
+{
+    if (t < 0 || t > n) return -INFINITY;
+    return m->logS[tri(n, t)];
+}
+
+/* ------------------------------------------------------------------------ */
+/* Initialisation: z_i uniform over topics by integer multiply-shift of the  */
+/* first Philox word with purpose INIT; r_i = 0 (repair then makes one head  */
+/* per non-empty cell).                                                      */
+/* ------------------------------------------------------------------------ */
+void or_init(const or_model *m, uint64_t init_seed, int32_t *z, uint8_t *r)
+{
+    for (int64_t i = 0; i < m->n_tokens; ++i) {
+        uint32_t x = or_philox_word0(init_seed, i, 0u, OR_PURPOSE_INIT);
+        z[i] = (int32_t)(((uint64_t)x * (uint64_t)m->K) >> 32);
+        r[i] = 0;
+    }
+}
+
+/* ------------------------------------------------------------------------ */
+/* Counts as pure functions of (z, r): the definitions of the count           */
+/* statistics used by the collapsed joint (thesis, SPDP joint derivation).    */
+/* ------------------------------------------------------------------------ */
+void or_rebuild(const or_model *m, const int32_t *z, const uint8_t *r, or_counts *c)
+{
+    const int64_t G = m->n_groups, K = m->K, V = m->vocab;
+    memset(c->n, 0, sizeof(int32_t) * (size_t)(G * K * V));
+    memset(c->t, 0, sizeof(int32_t) * (size_t)(G * K * V));
+    memset(c->Ngk, 0, sizeof(int32_t) * (size_t)(G * K));
+    memset(c->Tgk, 0, sizeof(int32_t) * (size_t)(G * K));
+    memset(c->Bkw, 0, sizeof(int32_t) * (size_t)(K * V));
+    memset(c->Bk, 0, sizeof(int32_t) * (size_t)K);
+    for (int32_t d = 0; d < m->n_docs; ++d) {
+        const int64_t g = m->doc_group[d];
+        for (int64_t i = m->doc_off[d]; i < m->doc_off[d + 1]; ++i) {
+            const int64_t k = z[i], w = m->words[i];
+            c->n[(g * K + k) * V + w] += 1;
+            c->Ngk[g * K + k] += 1;
+            if (r[i]) {
+                c->t[(g * K + k) * V + w] += 1;
+                c->Tgk[g * K + k] += 1;
+                c->Bkw[k * V + w] += 1;
+                c->Bk[k] += 1;
+            }
+        }
+    }
+}
+
+/* ------------------------------------------------------------------------ */
+/* Repair: scan tokens in increasing index; a token with r = 0 in a cell      */
+/* that has no table becomes that cell's head.  Returns the number promoted. */
+/* ------------------------------------------------------------------------ */
+int64_t or_repair(const or_model *m, const int32_t *z, uint8_t *r, or_counts *c)
+{
+    const int64_t K = m->K, V = m->vocab;
+    int64_t promoted = 0;
+    for (int32_t d = 0; d < m->n_docs; ++d) {
+        const int64_t g = m->doc_group[d];
+        for (int64_t i = m->doc_off[d]; i < m->doc_off[d + 1]; ++i) {
+            const int64_t k = z[i], w = m->words[i];
+            if (r[i] == 0 && c->t[(g * K + k) * V + w] == 0) {
+                r[i] = 1;
+                c->t[(g * K + k) * V + w] += 1;
+                c->Tgk[g * K + k] += 1;
+                c->Bkw[k * V + w] += 1;
+                c->Bk[k] += 1;
+                ++promoted;
+            }
+        }
+    }
+    return promoted;
+}
+
+/* ------------------------------------------------------------------------ */
+/* The 2K unnormalised conditionals of one token (thesis Eq.                  */
+/* SPDP-sampling-w-z-r0 and Eq. SPDP-sampling-w-z-r1, P = I), evaluated on    */
+/* the counts `s` with the token's own contribution removed at its current    */
+/* cell, and on the document row `crow` (which still includes the token).    */
+/*                                                                           */
+/* Returns 1 (and leaves w untouched) when the token is the only head of a    */
+/* cell that still has other customers: every other outcome then has zero    */
+/* joint probability, so the conditional is a point mass on the current      */
+/* state.  Otherwise fills w[2k] = weight of (k, r=1), w[2k+1] = (k, r=0).   */
+/* ------------------------------------------------------------------------ */
+int or_token_weights(const or_model *m, const or_counts *s, const int32_t *crow, int32_t g,
+                     int32_t wd, int32_t k0, int32_t r0, double *w)
+{
+    const int64_t K = m->K, V = m->vocab;
+    const int64_t cell0 = ((int64_t)g * K + k0) * V + wd;
+    if (r0 == 1 && s->t[cell0] == 1 && s->n[cell0] > 1) return 1;
+    const double alpha = m->alpha, a = m->a, b = m->b, gam = m->gam;
+    for (int64_t k = 0; k < K; ++k) {
+        const int del = (k == k0);
+        const int64_t cell = ((int64_t)g * K + k) * V + wd;
+        const int64_t nw = s->n[cell] - del;            /* m_{ikw} without token */
+        const int64_t tw = s->t[cell] - del * r0;       /* t_{ikw} without token */
+        const int64_t Nk = s->Ngk[g * K + k] - del;     /* m_{ik.}               */
+        const int64_t Tk = s->Tgk[g * K + k] - del * r0;/* t_{ik.}               */
+        const int64_t Bw = s->Bkw[k * V + wd] - del * r0;  /* sum_i t_{ikw}        */
+        const int64_t Bt = s->Bk[k] - del * r0;            /* sum_i sum_w t_{ikw}  */
+        const double ck = (double)(crow[k] - del);      /* n_{idk} without token */
+        double q0, q1;
+        if (nw == 0) {
+            /* empty cell: S^1_0 / S^0_0 = 0 and S^1_1 / S^0_0 = 1 */
+            q0 = 0.0;
+            q1 = 1.0;
+        } else {
+            const double ls = log_stirling(m, nw, tw);
+            /* (m - t + 1)/(m + 1) * S^{m+1}_t / S^m_t */
+            q0 = (double)(nw - tw + 1) / (double)(nw + 1) * exp(log_stirling(m, nw + 1, tw) - ls);
+            /* (t + 1)/(m + 1) * S^{m+1}_{t+1} / S^m_t */
+            q1 = (double)(tw + 1) / (double)(nw + 1) * exp(log_stirling(m, nw + 1, tw + 1) - ls);
+        }
+        const double doc = alpha + ck;
+        w[2 * k + 1] = doc / (b + (double)Nk) * q0;
+        w[2 * k] = doc * (b + a * (double)Tk) / (b + (double)Nk) * (gam + (double)Bw) /
+                   ((double)m->vocab * gam + (double)Bt) * q1;
+    }
+    return 0;
+}
+
+/* First outcome whose inclusive prefix sum exceeds u * total. */
+static int draw_outcome(const double *w, int64_t nout, double u)
+{
+    double total = 0.0;
+    for (int64_t j = 0; j < nout; ++j) total += w[j];
+    const double target = u * total;
+    double acc = 0.0;
+    for (int64_t j = 0; j < nout; ++j) {
+        acc += w[j];
+        if (acc > target) return (int)j;
+    }
+    return -1; /* unreachable: u < 1 and total > 0 */
+}
+
+/* ------------------------------------------------------------------------ */
+/* Sampling step of one sweep over documents [d_begin, d_end), against the   */
+/* snapshot `s` (read only).  z, r are updated in place; each document only  */
+/* touches its own tokens, so documents may run in any order or in parallel. */
+/* Optional trace: for tokens i in [tr_begin, tr_end) the weights (2K each),  */
+/* the uniform and a skip flag are written.                                   */
+/* Returns the number of tokens whose (z, r) changed.                        */
+/* ------------------------------------------------------------------------ */
+int64_t or_sample_docs(const or_model *m, const or_counts *s, int32_t *z, uint8_t *r,
+                       uint32_t sweep, uint64_t seed, int32_t d_begin, int32_t d_end,
+                       double *tr_w, double *tr_u, uint8_t *tr_skip, int64_t tr_begin,
+                       int64_t tr_end)
+{
+    const int64_t K = m->K;
+    int64_t changed = 0;
+#pragma omp parallel reduction(+ : changed)
+    {
+        int32_t *crow = (int32_t *)malloc(sizeof(int32_t) * (size_t)K);
+        double *w = (double *)malloc(sizeof(double) * (size_t)(2 * K));
+#pragma omp for schedule(dynamic, 16)
+        for (int32_t d = d_begin; d < d_end; ++d) {
+            const int32_t g = m->doc_group[d];
+            memset(crow, 0, sizeof(int32_t) * (size_t)K);
+            for (int64_t i = m->doc_off[d]; i < m->doc_off[d + 1]; ++i) crow[z[i]] += 1;
+            for (int64_t i = m->doc_off[d]; i < m->doc_off[d + 1]; ++i) {
+                const int32_t k0 = z[i], r0 = r[i];
+                const int skip = or_token_weights(m, s, crow, g, m->words[i], k0, r0, w);
+                const int tr = (tr_w != NULL && i >= tr_begin && i < tr_end);
+                if (tr) tr_skip[i - tr_begin] = (uint8_t)skip;
+                if (skip) continue;
+                const double u = or_uniform(seed, i, sweep);
+                if (tr) {
+                    memcpy(tr_w + (i - tr_begin) * 2 * K, w, sizeof(double) * (size_t)(2 * K));
+                    tr_u[i - tr_begin] = u;
+                }
+                const int j = draw_outcome(w, 2 * K, u);
+                const int32_t k1 = j / 2, r1 = 1 - (j % 2);
+                crow[k0] -= 1;
+                crow[k1] += 1;
+                if (k1 != k0 || r1 != r0) ++changed;
+                z[i] = k1;
+                r[i] = (uint8_t)r1;
+            }
+        }
+        free(crow);
+        free(w);
+    }
+    return changed;
+}
+
+/* ------------------------------------------------------------------------ */
+/* One full sweep.  mode 0: snapshot-parallel (sampling step against the      */
+/* sweep-start counts, then exact rebuild and repair).  mode 1: sequential    */
+/* collapsed Gibbs (Algorithm SPDP-Full-Gibbs with stored r): live counts,    */
+/* updated after every token; the state stays valid so repair never fires.   */
+/* out_stats[0] = tokens changed, out_stats[1] = heads promoted by repair.    */
+/* ------------------------------------------------------------------------ */
+static void apply_token(const or_model *m, or_counts *c, int32_t g, int32_t wd, int32_t k,
+                        int32_t rr, int sgn)
+{
+    const int64_t K = m->K, V = m->vocab;
+    const int64_t cell = ((int64_t)g * K + k) * V + wd;
+    c->n[cell] += sgn;
+    c->Ngk[(int64_t)g * K + k] += sgn;
+    if (rr) {
+        c->t[cell] += sgn;
+        c->Tgk[(int64_t)g * K + k] += sgn;
+        c->Bkw[(int64_t)k * V + wd] += sgn;
+        c->Bk[k] += sgn;
+    }
+}
+
+int or_sweep(const or_model *m, or_counts *c, int32_t *z, uint8_t *r, uint32_t sweep,
+             uint64_t seed, int mode, int64_t *out_stats)
+{
+    int64_t changed = 0, promoted = 0;
+    if (mode == 0) {
+        changed = or_sample_docs(m, c, z, r, sweep, seed, 0, m->n_docs, NULL, NULL, NULL, 0, 0);
+        or_rebuild(m, z, r, c);
+        promoted = or_repair(m, z, r, c);
+    } else if (mode == 1) {
+        const int64_t K = m->K;
+        int32_t *crow = (int32_t *)malloc(sizeof(int32_t) * (size_t)K);
+        double *w = (double *)malloc(sizeof(double) * (size_t)(2 * K));
+        for (int32_t d = 0; d < m->n_docs; ++d) {
+            const int32_t g = m->doc_group[d];
+            memset(crow, 0, sizeof(int32_t) * (size_t)K);
+            for (int64_t i = m->doc_off[d]; i < m->doc_off[d + 1]; ++i) crow[z[i]] += 1;
+            for (int64_t i = m->doc_off[d]; i < m->doc_off[d + 1]; ++i) {
+                const int32_t k0 = z[i], r0 = r[i], wd = m->words[i];
+                if (or_token_weights(m, c, crow, g, wd, k0, r0, w)) continue;
+                const int j = draw_outcome(w, 2 * K, or_uniform(seed, i, sweep));
+                const int32_t k1 = j / 2, r1 = 1 - (j % 2);
+                apply_token(m, c, g, wd, k0, r0, -1);
+                apply_token(m, c, g, wd, k1, r1, +1);
+                crow[k0] -= 1;
+                crow[k1] += 1;
+                if (k1 != k0 || r1 != r0) ++changed;
+                z[i] = k1;
+                r[i] = (uint8_t)r1;
+            }
+        }
+        free(crow);
+        free(w);
+    } else {
+        return -1;
+    }
+    if (out_stats) { out_stats[0] = changed; out_stats[1] = promoted; }
+    return 0;
+}
+
+/* ------------------------------------------------------------------------ */
+/* Joint log p(W, Z, R | alpha, a, b, gamma) with P = I: the collapsed joint  */
+/* of the thesis's blocked-Gibbs derivation (Eq. SPDP-Blocked-Gibbs-Joint-    */
+/* Prob and the final product), read as                                      */
+/*   doc terms      prod_d Beta_K(alpha + n_d) / Beta_K(alpha)                */
+/*   PYP normaliser prod_{g,k} (b|a)_{T_gk} / (b)_{N_gk}                      */
+/*   cells          prod_{g,k,w} S^{n}_{t,a} / C(n, t)                        */
+/*   shadow base    prod_k Beta_V(gamma + B_k.) / Beta_V(gamma)               */
+/* Returns -inf for a state with zero probability (some t > n, or t = 0 < n). */
+/* ------------------------------------------------------------------------ */
+static double log_pochhammer_step(double x, double y, int64_t T)
+{
+    /* log (x|y)_T = sum_{j<T} log(x + j y) */
+    if (T <= 0) return 0.0;
+    if (y == 0.0) return (double)T * log(x);
+    return (double)T * log(y) + lgamma(x / y + (double)T) - lgamma(x / y);
+}
+
+double or_loglik(const or_model *m, const int32_t *z, const uint8_t *r, const or_counts *c)
+{
+    (void)r;
+    const int64_t G = m->n_groups, K = m->K, V = m->vocab;
+    const double alpha = m->alpha, a = m->a, b = m->b, gam = m->gam;
+    double ll_doc = 0.0, ll_pyp = 0.0, ll_cell = 0.0, ll_base = 0.0;
+    int bad = 0;
+
+    /* documents */
+    int32_t *crow = (int32_t *)calloc((size_t)K, sizeof(int32_t));
+    for (int32_t d = 0; d < m->n_docs; ++d) {
+        memset(crow, 0, sizeof(int32_t) * (size_t)K);
+        const int64_t L = m->doc_off[d + 1] - m->doc_off[d];
+        for (int64_t i = m->doc_off[d]; i < m->doc_off[d + 1]; ++i) crow[z[i]] += 1;
+        double s = lgamma((double)K * alpha) - lgamma((double)K * alpha + (double)L);
+        for (int64_t k = 0; k < K; ++k) s += lgamma(alpha + crow[k]) - lgamma(alpha);
+        ll_doc += s;
+    }
+    free(crow);
+
+    /* restaurants (g, k) */
+    for (int64_t g = 0; g < G; ++g)
+        for (int64_t k = 0; k < K; ++k) {
+            const int64_t N = c->Ngk[g * K + k], T = c->Tgk[g * K + k];
+            ll_pyp += log_pochhammer_step(b, a, T) - log_pochhammer_step(b, 1.0, N);
+        }
+
+    /* cells */
+    for (int64_t g = 0; g < G; ++g)
+        for (int64_t k = 0; k < K; ++k)
+            for (int64_t w = 0; w < V; ++w) {
+                const int64_t n = c->n[(g * K + k) * V + w], t = c->t[(g * K + k) * V + w];
+                if (n == 0 && t == 0) continue;
+                if (n > m->ncap) return NAN; /* Stirling table too small */
+                if (t > n || t <= 0) { bad = 1; continue; }
+                ll_cell += log_stirling(m, n, t) -
+                           (lgamma((double)n + 1.0) - lgamma((double)t + 1.0) -
+                            lgamma((double)(n - t) + 1.0));
+            }
+
+    /* shadow base */
+    for (int64_t k = 0; k < K; ++k) {
+        double s = lgamma((double)V * gam) - lgamma((double)V * gam + (double)c->Bk[k]);
+        for (int64_t w = 0; w < V; ++w) s += lgamma(gam + (double)c->Bkw[k * V + w]) - lgamma(gam);
+        ll_base += s;
+    }
+    if (bad) return -INFINITY;
+    return ll_doc + ll_pyp + ll_cell + ll_base;
+}
+
+/* Largest per-(group, word) token count: every n[g][k][w] is bounded by it, */
+/* so it fixes how many Stirling rows any state of this corpus can need.     */
+int32_t or_max_group_word_count(const or_model *m)
+{
+    const int64_t G = m->n_groups, V = m->vocab;
+    int32_t *cnt = (int32_t *)calloc((size_t)(G * V), sizeof(int32_t));
+    int32_t best = 0;
+    for (int32_t d = 0; d < m->n_docs; ++d) {
+        const int64_t g = m->doc_group[d];
+        for (int64_t i = m->doc_off[d]; i < m->doc_off[d + 1]; ++i) {
+            int32_t v = ++cnt[g * V + m->words[i]];
+            if (v > best) best = v;
+        }
+    }
+    free(cnt);
+    return best;
+}
+
+int or_num_threads(void)
+{
+#ifdef _OPENMP
+    return omp_get_max_threads();
+#else
+    return 1;
+#endif
+}
+
+/* ------------------------------------------------------------------------ */
+/* Test helper: run `n_sweeps` sweeps (mode as in or_sweep, sweep index =    */
+/* first_sweep + s) and histogram the visited states.  A state is encoded in  */
+/* base 2K with digit (2 z_i + 1 - r_i) for token i (least significant first), */
+/* so the histogram needs (2K)^N bins; only for tiny corpora.                 */
+/* ------------------------------------------------------------------------ */
+int or_chain_histogram(const or_model *m, or_counts *c, int32_t *z, uint8_t *r,
+                       uint32_t first_sweep, int64_t n_sweeps, uint64_t seed, int mode,
+                       int64_t *hist, int64_t n_bins)
+{
+    const int64_t base = 2 * (int64_t)m->K;
+    for (int64_t s = 0; s < n_sweeps; ++s) {
+        if (or_sweep(m, c, z, r, first_sweep + (uint32_t)s, seed, mode, NULL) != 0) return -1;
+        int64_t code = 0, mul = 1;
+        for (int64_t i = 0; i < m->n_tokens; ++i) {
+            code += (2 * (int64_t)z[i] + 1 - r[i]) * mul;
+            mul *= base;
+        }
+        if (code < 0 || code >= n_bins) return -2;
+        hist[code] += 1;
+    }
+    return 0;
+}
