@@ -1,0 +1,192 @@
+/*
+ * spdp.h -- C ABI of the MI355X (gfx950) SPDP Gibbs-sweep library.
+ *
+ * The library runs the data-parallel hot path of the Shadow Poisson Dirichlet
+ * Process (SPDP) differential topic model of Li (2012), "Multi-GPU Distributed
+ * Parallel Bayesian Differential Topic Modelling" (arXiv:1510.06549): the
+ * collapsed-Gibbs resampling of every token's (topic z, table indicator r)
+ * against Pitman-Yor customer counts n[g,k,w] and table counts t[g,k,w] whose
+ * tables share a per-topic shadow base (chapter "Shared Topic Modelling Using
+ * Shadow Poisson Dirichlet Process", Eq. SPDP-sampling-w-z-r0 and
+ * Eq. SPDP-sampling-w-z-r1, with identity transformation matrices P^i).
+ * Documents are resampled in parallel against a snapshot of the shared counts
+ * taken at the start of the sweep, the document-parallel approximation of the
+ * thesis's Improved-GPU-SPDP (section "Parallelism With Improved Accuracy: Word
+ * Order Rearrangement"), each document's own doc-topic row staying live and its
+ * tokens running in order; the counts are then rebuilt exactly.
+ *
+ * Conventions shared by every entry point:
+ *   - Return value: SPDP_OK (0) or a negative SPDP_E_* code; the text of the
+ *     last error of the calling thread is returned by spdp_last_error().  No
+ *     C++ exception crosses this boundary.
+ *   - Ownership: host inputs are deep-copied before the call returns.  Outputs
+ *     go to caller-allocated buffers of the documented size; `where` = 0 means
+ *     a host pointer, 1 a device pointer on the state's GPU.  The state owns
+ *     all its device memory until spdp_destroy().
+ *   - Streams: all device work of a state runs in order on the HIP stream given
+ *     at creation (NULL = the null stream).  spdp_sweep() only enqueues; calls
+ *     that return data to the host synchronise that stream.
+ *   - Threading: a state may be used by one host thread at a time.
+ *   - Determinism: results are a pure function of (corpus, groups, K,
+ *     hyperparameters, init seed, sequence of (sweep, seed)), independent of
+ *     launch configuration and scheduling.
+ *
+ * Layouts: topics of one (group, word) row are contiguous.  n and t are
+ * exported as [g][w][k] (group-major, then word, then topic); the shadow-base
+ * table counts B as [w][k]; per-restaurant totals as [g][k].
+ * The (z, r) state is per token in corpus order.
+ */
+#ifndef SPDP_H
+#define SPDP_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define SPDP_OK 0
+#define SPDP_E_ARG (-1)   /* invalid argument (null pointer, value out of range) */
+#define SPDP_E_NOMEM (-2) /* device or host allocation failed                   */
+#define SPDP_E_HIP (-3)   /* a HIP runtime call failed                          */
+#define SPDP_E_RANGE (-4) /* the Stirling cache would exceed its memory budget   */
+#define SPDP_E_STATE (-5) /* an invariant of the count state is violated         */
+
+#define SPDP_MAX_K 1024
+
+typedef struct spdp_state spdp_state; /* opaque */
+
+/* A corpus: N tokens in D documents, stored document after document. */
+typedef struct {
+    int64_t n_tokens;           /* N, 0 <= N < 2^31                                */
+    int32_t n_docs;             /* D >= 1                                          */
+    int32_t vocab;              /* V >= 1                                          */
+    const int32_t *words;       /* host [N], 0 <= words[i] < V                     */
+    const int64_t *doc_offsets; /* host [D+1], [0] = 0, nondecreasing, [D] = N     */
+    uint64_t init_seed;         /* key of the Philox stream that draws the initial z */
+    void *hip_stream;           /* hipStream_t for all work of the state, or NULL   */
+} spdp_corpus;
+
+/* The groups ("collections" of the differential model, index i of the thesis). */
+typedef struct {
+    int32_t n_groups;           /* G >= 1, G * V < 2^31                             */
+    const int32_t *doc_group;   /* host [D], 0 <= doc_group[d] < G                  */
+} spdp_groups;
+
+/*
+ * Create a sampler state: validate, upload the corpus, tabulate the
+ * generalised Stirling numbers S^n_{t,a} (recurrence of the PYP joint,
+ * Corollary 17 passage) in fp64 log space for every n the corpus can reach,
+ * draw the initial topics (z uniform from Philox, r = 0), rebuild the counts
+ * and promote the smallest-index token of every non-empty cell to table head.
+ *   K      number of topics, 1 <= K <= SPDP_MAX_K
+ *   alpha  symmetric Dirichlet prior of document-topic proportions, > 0
+ *   a      Pitman-Yor discount, 0 <= a < 1
+ *   b      Pitman-Yor concentration, > 0
+ *   gamma  symmetric Dirichlet prior of the shadow base phi0_k, > 0
+ * Errors: E_ARG, E_NOMEM, E_HIP, E_RANGE (Stirling cache beyond 4 GiB).
+ * On success *out holds the new state; on error *out is NULL.
+ */
+int spdp_create(const spdp_corpus *corpus, const spdp_groups *groups, int32_t K, double alpha,
+                double a, double b, double gamma, spdp_state **out);
+
+/*
+ * One Gibbs sweep (asynchronous on the state's stream): every token's (z, r)
+ * is resampled from the 2K outcomes of Eq. SPDP-sampling-w-z-r0/-r1, with the
+ * shared counts of the sweep start and the live row of its own document;
+ * outcome j = 2k is (k, r = 1), j = 2k + 1 is (k, r = 0); the uniform of token
+ * i is Philox4x32-10 keyed by `seed` at counter (i lo, i hi, sweep, 0), and the
+ * draw is the first j whose prefix sum exceeds u * total.  A token that is the
+ * only head of a cell with other customers keeps its state.  Counts are then
+ * updated exactly and every cell left with customers but no table gets its
+ * smallest-index token as head.  Errors: E_ARG, E_HIP.
+ */
+int spdp_sweep(spdp_state *s, uint32_t sweep, uint64_t seed);
+
+/*
+ * Export customer counts n and table counts t of groups [g_begin, g_end) as
+ * [g_end - g_begin][V][K] int32 each (either pointer may be NULL to skip it).
+ * Synchronises.  Errors: E_ARG, E_HIP.
+ */
+int spdp_counts(const spdp_state *s, int32_t g_begin, int32_t g_end, int32_t *n_gwk,
+                int32_t *t_gwk, int where);
+
+/*
+ * Export the totals: customers N[g][k] = sum_w n, tables T[g][k] = sum_w t,
+ * shadow-base table counts B[w][k] = sum_g t and B[k] = sum_w B[w][k].
+ * Any pointer may be NULL.  Synchronises.  Errors: E_ARG, E_HIP.
+ */
+int spdp_totals(const spdp_state *s, int32_t *N_gk, int32_t *T_gk, int32_t *B_wk, int32_t *B_k,
+                int where);
+
+/*
+ * Joint log p(W, Z, R | alpha, a, b, gamma) of the current state in fp64 (the
+ * collapsed joint of the thesis's blocked-Gibbs derivation with P = I):
+ * document Dirichlet-multinomial terms, per-restaurant (b|a)_T / (b)_N,
+ * per-cell S^n_{t,a} / C(n, t), and the shadow-base Dirichlet-multinomial of
+ * each topic.  Deterministic reduction order.  Synchronises.
+ * Errors: E_ARG, E_HIP, E_STATE (a cell with t > n or t = 0 < n).
+ */
+int spdp_loglik(spdp_state *s, double *out);
+
+/* Free all resources of the state (NULL is ignored). */
+void spdp_destroy(spdp_state *s);
+
+/*
+ * Checkpoint: export z [N] int32 and r [N] uint8 (either may be NULL).
+ * Synchronises.  Errors: E_ARG, E_HIP.
+ */
+int spdp_get_assignments(const spdp_state *s, int32_t *z, uint8_t *r, int where);
+
+/*
+ * Resume: replace the state by (z, r) (z in [0, K), r in {0, 1}), rebuild the
+ * counts and promote the smallest-index token of every cell with customers but
+ * no table.  Synchronises.  Errors: E_ARG (value out of range), E_HIP.
+ */
+int spdp_set_assignments(spdp_state *s, const int32_t *z, const uint8_t *r, int where);
+
+/*
+ * Test hook: run the sampling step of sweep (sweep, seed) on the current state
+ * WITHOUT committing it, and export, for tokens i in [tok_begin, tok_end), the
+ * fp32 unnormalised weights of all 2K outcomes (w_out, [(tok_end - tok_begin)
+ * * 2K], outcome order as in spdp_sweep), the uniform (u_out, -1 for a token
+ * kept by the sole-head rule) and the sampled packed outcome (zr_out, value
+ * 2 z + r, may be NULL).  Uses the same kernel as spdp_sweep.  Synchronises.
+ * Errors: E_ARG, E_NOMEM, E_HIP.
+ */
+int spdp_debug_conditionals(spdp_state *s, uint32_t sweep, uint64_t seed, int64_t tok_begin,
+                            int64_t tok_end, float *w_out, float *u_out, int32_t *zr_out,
+                            int where);
+
+/*
+ * Statistics of the last sweep: tokens whose (z, r) changed and table heads
+ * promoted by the repair step.  Synchronises.  Errors: E_ARG, E_HIP.
+ */
+int spdp_stats(const spdp_state *s, int64_t *changed, int64_t *repaired);
+
+/*
+ * Per-kernel timing with HIP events on the state's stream.  enable = 1 starts
+ * recording (and clears the accumulators), 0 stops.  spdp_kernel_times writes
+ * the accumulated milliseconds and launch counts of the SPDP_NKERNELS kernel
+ * classes (order: sample, update, repair, totals).  Synchronises.
+ */
+#define SPDP_NKERNELS 4
+int spdp_kernel_timing(spdp_state *s, int enable);
+int spdp_kernel_times(spdp_state *s, double *ms, int64_t *launches);
+
+/*
+ * Shape of the state: out[0] = N, [1] = D, [2] = V, [3] = G, [4] = K,
+ * [5] = row stride of the count arrays (topics, >= K), [6] = largest
+ * per-(group, word) token count (the Stirling rows needed), [7] = device bytes
+ * held.  Errors: E_ARG.
+ */
+int spdp_info(const spdp_state *s, int64_t *out8);
+
+/* Text of the calling thread's last error ("" if none). */
+const char *spdp_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SPDP_H */

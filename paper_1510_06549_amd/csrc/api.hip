@@ -1,0 +1,551 @@
+// api.hip -- the extern "C" boundary (declared in include/spdp.h): argument
+// validation, device memory, error mapping and the order of kernel launches.
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "spdp_internal.hpp"
+
+using namespace spdp;
+
+namespace {
+
+thread_local std::string g_last_error;
+
+int fail(int code, const char *fmt, ...)
+{
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof buf, fmt, ap);
+    va_end(ap);
+    g_last_error = buf;
+    return code;
+}
+
+#define HIP_TRY(expr)                                                                      \
+    do {                                                                                   \
+        hipError_t e_ = (expr);                                                            \
+        if (e_ != hipSuccess)                                                              \
+            return fail(SPDP_E_HIP, "%s failed: %s", #expr, hipGetErrorString(e_));        \
+    } while (0)
+
+constexpr int64_t kStirlingBudget = 4ll << 30;  // bytes for log S + ratio pairs
+
+struct EventPair {
+    hipEvent_t a, b;
+};
+
+}  // namespace
+
+struct spdp_state {
+    Model m{};
+    DeviceBuffers b{};
+    hipStream_t st = nullptr;
+    int device = 0;
+    int cur = 0;
+    int64_t bytes = 0;
+    bool timing = false;
+    std::vector<EventPair> events[SPDP_NKERNELS];
+    std::vector<void *> allocs;
+};
+
+namespace {
+
+template <typename T>
+int dev_alloc(spdp_state *s, T **p, int64_t count, const char *what)
+{
+    *p = nullptr;
+    if (count <= 0) count = 1;
+    const size_t bytes = (size_t)count * sizeof(T);
+    void *q = nullptr;
+    hipError_t e = hipMalloc(&q, bytes);
+    if (e != hipSuccess) {
+        (void)hipGetLastError();
+        return fail(SPDP_E_NOMEM, "hipMalloc of %zu bytes for %s failed: %s", bytes, what,
+                    hipGetErrorString(e));
+    }
+    s->allocs.push_back(q);
+    s->bytes += (int64_t)bytes;
+    *p = static_cast<T *>(q);
+    return SPDP_OK;
+}
+
+void free_state(spdp_state *s)
+{
+    if (!s) return;
+    hipSetDevice(s->device);
+    if (s->st) hipStreamSynchronize(s->st);
+    else hipDeviceSynchronize();
+    for (void *p : s->allocs) hipFree(p);
+    for (auto &v : s->events)
+        for (auto &ev : v) {
+            hipEventDestroy(ev.a);
+            hipEventDestroy(ev.b);
+        }
+    delete s;
+}
+
+int sync(const spdp_state *s)
+{
+    HIP_TRY(hipStreamSynchronize(s->st));
+    return SPDP_OK;
+}
+
+// Run `launch` with optional event timing of kernel class `cls`.
+template <typename F>
+int timed(spdp_state *s, int cls, F launch)
+{
+    EventPair ev{};
+    if (s->timing) {
+        HIP_TRY(hipEventCreate(&ev.a));
+        HIP_TRY(hipEventCreate(&ev.b));
+        HIP_TRY(hipEventRecord(ev.a, s->st));
+    }
+    HIP_TRY(launch());
+    if (s->timing) {
+        HIP_TRY(hipEventRecord(ev.b, s->st));
+        s->events[cls].push_back(ev);
+    }
+    return SPDP_OK;
+}
+
+// Counts, repair of every cell and totals for the packed state in zr[cur].
+int rebuild_state(spdp_state *s)
+{
+    const Model &m = s->m;
+    DeviceBuffers &b = s->b;
+    int32_t *zr = b.zr[s->cur];
+    HIP_TRY(launch_rebuild(m, b, zr, s->st));
+    // every row is a repair candidate
+    HIP_TRY(launch_fill_u32(b.flags, ((int64_t)m.G * m.V + 31) / 32, 0xFFFFFFFFu, s->st));
+    HIP_TRY(launch_fill_u64(b.ctr, 4, 0ull, s->st));
+    HIP_TRY(launch_fill_u64(b.ctr + 2, 1, 1ull, s->st));
+    HIP_TRY(launch_repair(m, b, zr, s->st));
+    HIP_TRY(launch_totals(m, b, zr, s->st));
+    return SPDP_OK;
+}
+
+int check_device_flags(spdp_state *s, int32_t *host_err)
+{
+    HIP_TRY(hipMemcpyAsync(host_err, s->b.err, 2 * sizeof(int32_t), hipMemcpyDeviceToHost, s->st));
+    return sync(s);
+}
+
+}  // namespace
+
+extern "C" {
+
+const char *spdp_last_error(void) { return g_last_error.c_str(); }
+
+int spdp_create(const spdp_corpus *corpus, const spdp_groups *groups, int32_t K, double alpha,
+                double a, double b, double gamma, spdp_state **out)
+{
+    g_last_error.clear();
+    if (!out) return fail(SPDP_E_ARG, "out is NULL");
+    *out = nullptr;
+    if (!corpus || !groups) return fail(SPDP_E_ARG, "corpus or groups is NULL");
+    const int64_t N = corpus->n_tokens;
+    const int32_t D = corpus->n_docs, V = corpus->vocab, G = groups->n_groups;
+    if (N < 0 || N >= (1ll << 31)) return fail(SPDP_E_ARG, "n_tokens %lld out of [0, 2^31)", (long long)N);
+    if (D < 1) return fail(SPDP_E_ARG, "n_docs must be >= 1");
+    if (V < 1) return fail(SPDP_E_ARG, "vocab must be >= 1");
+    if (G < 1) return fail(SPDP_E_ARG, "n_groups must be >= 1");
+    if ((int64_t)G * V >= (1ll << 31)) return fail(SPDP_E_ARG, "n_groups * vocab must be < 2^31");
+    if (K < 1 || K > SPDP_MAX_K) return fail(SPDP_E_ARG, "K must be in [1, %d]", SPDP_MAX_K);
+    if (!(alpha > 0.0) || !std::isfinite(alpha)) return fail(SPDP_E_ARG, "alpha must be > 0");
+    if (!(gamma > 0.0) || !std::isfinite(gamma)) return fail(SPDP_E_ARG, "gamma must be > 0");
+    if (!(a >= 0.0 && a < 1.0)) return fail(SPDP_E_ARG, "discount a must be in [0, 1)");
+    if (!(b > 0.0) || !std::isfinite(b)) return fail(SPDP_E_ARG, "concentration b must be > 0");
+    if (!corpus->doc_offsets || !groups->doc_group || (N > 0 && !corpus->words))
+        return fail(SPDP_E_ARG, "null corpus array");
+    const int64_t *off = corpus->doc_offsets;
+    if (off[0] != 0 || off[D] != N) return fail(SPDP_E_ARG, "doc_offsets must start at 0 and end at N");
+    for (int32_t d = 0; d < D; ++d)
+        if (off[d + 1] < off[d]) return fail(SPDP_E_ARG, "doc_offsets not nondecreasing at %d", d);
+
+    spdp_state *s = new (std::nothrow) spdp_state();
+    if (!s) return fail(SPDP_E_NOMEM, "host allocation failed");
+    int rc = SPDP_OK;
+#define TRY(x)                          \
+    do {                                \
+        if ((rc = (x)) != SPDP_OK) {    \
+            std::string msg_ = g_last_error; \
+            free_state(s);              \
+            g_last_error = msg_;        \
+            return rc;                  \
+        }                               \
+    } while (0)
+#define TRY_HIP(x)                                                                         \
+    do {                                                                                   \
+        hipError_t e_ = (x);                                                               \
+        if (e_ != hipSuccess) {                                                            \
+            fail(SPDP_E_HIP, "%s failed: %s", #x, hipGetErrorString(e_));                  \
+            std::string msg_ = g_last_error;                                               \
+            free_state(s);                                                                 \
+            g_last_error = msg_;                                                           \
+            return SPDP_E_HIP;                                                             \
+        }                                                                                  \
+    } while (0)
+
+    TRY_HIP(hipGetDevice(&s->device));
+    s->st = (hipStream_t)corpus->hip_stream;
+    Model &m = s->m;
+    m.N = N;
+    m.D = D;
+    m.V = V;
+    m.G = G;
+    m.K = K;
+    m.Kp = padded_K(K);
+    m.alpha = alpha;
+    m.a = a;
+    m.b = b;
+    m.gamma = gamma;
+    m.alpha_f = (float)alpha;
+    m.a_f = (float)a;
+    m.b_f = (float)b;
+    m.gamma_f = (float)gamma;
+    m.Vgamma_f = (float)((double)V * gamma);
+    m.divV = make_fastdiv((uint32_t)V);
+    DeviceBuffers &B = s->b;
+    const int64_t rows = (int64_t)G * V;
+
+    // corpus
+    int32_t *words_d = nullptr, *gw_count = nullptr;
+    TRY(dev_alloc(s, &B.gw, N, "token rows"));
+    TRY(dev_alloc(s, &B.doc_off, (int64_t)D + 1, "doc offsets"));
+    TRY(dev_alloc(s, &B.doc_group, D, "doc groups"));
+    TRY(dev_alloc(s, &B.err, 2, "error flags"));
+    TRY(dev_alloc(s, &B.ctr, 4, "counters"));
+    TRY(dev_alloc(s, &B.scalar, 1, "scalar"));
+    TRY_HIP(launch_fill_i32(B.err, 2, 0, s->st));
+    {
+        void *tmp = nullptr;
+        if (hipMalloc(&tmp, (size_t)(N > 0 ? N : 1) * sizeof(int32_t)) != hipSuccess) {
+            (void)hipGetLastError();
+            TRY(fail(SPDP_E_NOMEM, "staging buffer for words"));
+        }
+        words_d = (int32_t *)tmp;
+        if (hipMalloc(&tmp, (size_t)rows * sizeof(int32_t)) != hipSuccess) {
+            (void)hipGetLastError();
+            hipFree(words_d);
+            TRY(fail(SPDP_E_NOMEM, "staging buffer for word counts"));
+        }
+        gw_count = (int32_t *)tmp;
+    }
+    auto cleanup_staging = [&]() {
+        hipFree(words_d);
+        hipFree(gw_count);
+    };
+    hipError_t e = hipSuccess;
+    if (N > 0)
+        e = hipMemcpyAsync(words_d, corpus->words, (size_t)N * sizeof(int32_t),
+                           hipMemcpyHostToDevice, s->st);
+    if (e == hipSuccess)
+        e = hipMemcpyAsync(B.doc_off, off, (size_t)(D + 1) * sizeof(int64_t), hipMemcpyHostToDevice,
+                           s->st);
+    if (e == hipSuccess)
+        e = hipMemcpyAsync(B.doc_group, groups->doc_group, (size_t)D * sizeof(int32_t),
+                           hipMemcpyHostToDevice, s->st);
+    if (e == hipSuccess) e = launch_fill_i32(gw_count, rows, 0, s->st);
+    if (e == hipSuccess) e = launch_make_gw(m, words_d, B.doc_off, B.doc_group, B.gw, gw_count, B.err, s->st);
+    if (e == hipSuccess) e = launch_max_i32(gw_count, rows, B.err + 1, s->st);
+    int32_t herr[2] = {0, 0};
+    if (e == hipSuccess) e = hipMemcpyAsync(herr, B.err, sizeof herr, hipMemcpyDeviceToHost, s->st);
+    if (e == hipSuccess) e = hipStreamSynchronize(s->st);
+    cleanup_staging();
+    TRY_HIP(e);
+    if (herr[0] & 1) TRY(fail(SPDP_E_ARG, "doc_group out of [0, n_groups)"));
+    if (herr[0] & 2) TRY(fail(SPDP_E_ARG, "word id out of [0, vocab)"));
+    m.ncap = herr[1] < 1 ? 1 : herr[1];
+    TRY_HIP(launch_fill_i32(B.err, 2, 0, s->st));
+
+    // Stirling cache
+    const int64_t n_logS = tri_index(m.ncap + 1, 0);  // rows 0..ncap
+    const int64_t n_Q = tri_index(m.ncap, 0);         // rows 0..ncap-1
+    if (n_logS * 8 + n_Q * 8 > kStirlingBudget || m.ncap >= 65535)
+        TRY(fail(SPDP_E_RANGE, "Stirling cache for %d customers exceeds its budget", m.ncap));
+    TRY(dev_alloc(s, &B.logS, n_logS, "log Stirling table"));
+    TRY(dev_alloc(s, &B.Q, n_Q, "Stirling ratio pairs"));
+    TRY(dev_alloc(s, &B.lfact, (int64_t)m.ncap + 1, "log factorials"));
+    TRY_HIP(launch_stirling(m, B.logS, B.Q, B.lfact, s->st));
+
+    // state and counts
+    TRY(dev_alloc(s, &B.zr[0], N, "zr"));
+    TRY(dev_alloc(s, &B.zr[1], N, "zr"));
+    TRY(dev_alloc(s, &B.n, rows * m.Kp, "customer counts"));
+    TRY(dev_alloc(s, &B.t, rows * m.Kp, "table counts"));
+    TRY(dev_alloc(s, &B.B, (int64_t)V * m.Kp, "shadow-base table counts"));
+    TRY(dev_alloc(s, &B.Ngk, (int64_t)G * m.Kp, "N_gk"));
+    TRY(dev_alloc(s, &B.Tgk, (int64_t)G * m.Kp, "T_gk"));
+    TRY(dev_alloc(s, &B.Bk, m.Kp, "B_k"));
+    TRY(dev_alloc(s, &B.f0, (int64_t)G * m.Kp, "f0"));
+    TRY(dev_alloc(s, &B.f1, (int64_t)G * m.Kp, "f1"));
+    TRY(dev_alloc(s, &B.flags, (rows + 31) / 32, "repair flags"));
+    B.partial_len = loglik_partials_needed();
+    TRY(dev_alloc(s, &B.partial, B.partial_len, "loglik partials"));
+    s->cur = 0;
+    TRY_HIP(launch_init_z(m, corpus->init_seed, B.zr[0], s->st));
+    TRY(rebuild_state(s));
+    TRY(sync(s));
+#undef TRY
+#undef TRY_HIP
+    *out = s;
+    return SPDP_OK;
+}
+
+void spdp_destroy(spdp_state *s) { free_state(s); }
+
+int spdp_sweep(spdp_state *s, uint32_t sweep, uint64_t seed)
+{
+    if (!s) return fail(SPDP_E_ARG, "state is NULL");
+    HIP_TRY(hipSetDevice(s->device));
+    const Model &m = s->m;
+    DeviceBuffers &b = s->b;
+    int32_t *zr_old = b.zr[s->cur], *zr_new = b.zr[1 - s->cur];
+    int rc;
+    if ((rc = timed(s, 3, [&] { return launch_factors(m, b, s->st); })) != SPDP_OK) return rc;
+    if ((rc = timed(s, 0, [&] {
+             return launch_sample(m, b, zr_old, zr_new, sweep, seed, nullptr, nullptr, 0, 0, s->st);
+         })) != SPDP_OK)
+        return rc;
+    if ((rc = timed(s, 1, [&] { return launch_update(m, b, zr_old, zr_new, s->st); })) != SPDP_OK)
+        return rc;
+    if ((rc = timed(s, 2, [&] { return launch_repair(m, b, zr_new, s->st); })) != SPDP_OK) return rc;
+    if ((rc = timed(s, 3, [&] { return launch_totals(m, b, zr_new, s->st); })) != SPDP_OK) return rc;
+    s->cur = 1 - s->cur;
+    return SPDP_OK;
+}
+
+int spdp_counts(const spdp_state *s, int32_t g_begin, int32_t g_end, int32_t *n_gwk,
+                int32_t *t_gwk, int where)
+{
+    if (!s) return fail(SPDP_E_ARG, "state is NULL");
+    const Model &m = s->m;
+    if (g_begin < 0 || g_end > m.G || g_begin > g_end) return fail(SPDP_E_ARG, "bad group range");
+    if (where != 0 && where != 1) return fail(SPDP_E_ARG, "where must be 0 or 1");
+    HIP_TRY(hipSetDevice(s->device));
+    const hipMemcpyKind kind = where ? hipMemcpyDeviceToDevice : hipMemcpyDeviceToHost;
+    const size_t rows = (size_t)(g_end - g_begin) * m.V;
+    const size_t off = (size_t)g_begin * m.V * m.Kp;
+    if (rows > 0) {
+        if (n_gwk)
+            HIP_TRY(hipMemcpy2DAsync(n_gwk, (size_t)m.K * 4, s->b.n + off, (size_t)m.Kp * 4,
+                                     (size_t)m.K * 4, rows, kind, s->st));
+        if (t_gwk)
+            HIP_TRY(hipMemcpy2DAsync(t_gwk, (size_t)m.K * 4, s->b.t + off, (size_t)m.Kp * 4,
+                                     (size_t)m.K * 4, rows, kind, s->st));
+    }
+    return sync(s);
+}
+
+int spdp_totals(const spdp_state *s, int32_t *N_gk, int32_t *T_gk, int32_t *B_wk, int32_t *B_k,
+                int where)
+{
+    if (!s) return fail(SPDP_E_ARG, "state is NULL");
+    if (where != 0 && where != 1) return fail(SPDP_E_ARG, "where must be 0 or 1");
+    HIP_TRY(hipSetDevice(s->device));
+    const Model &m = s->m;
+    const hipMemcpyKind kind = where ? hipMemcpyDeviceToDevice : hipMemcpyDeviceToHost;
+    const size_t w = (size_t)m.K * 4, p = (size_t)m.Kp * 4;
+    if (N_gk) HIP_TRY(hipMemcpy2DAsync(N_gk, w, s->b.Ngk, p, w, (size_t)m.G, kind, s->st));
+    if (T_gk) HIP_TRY(hipMemcpy2DAsync(T_gk, w, s->b.Tgk, p, w, (size_t)m.G, kind, s->st));
+    if (B_wk) HIP_TRY(hipMemcpy2DAsync(B_wk, w, s->b.B, p, w, (size_t)m.V, kind, s->st));
+    if (B_k) HIP_TRY(hipMemcpyAsync(B_k, s->b.Bk, w, kind, s->st));
+    return sync(s);
+}
+
+int spdp_loglik(spdp_state *s, double *out)
+{
+    if (!s || !out) return fail(SPDP_E_ARG, "null argument");
+    HIP_TRY(hipSetDevice(s->device));
+    HIP_TRY(launch_fill_i32(s->b.err, 2, 0, s->st));
+    HIP_TRY(launch_loglik(s->m, s->b, s->b.zr[s->cur], s->st));
+    double v = 0.0;
+    HIP_TRY(hipMemcpyAsync(&v, s->b.scalar, sizeof v, hipMemcpyDeviceToHost, s->st));
+    int32_t herr[2];
+    int rc = check_device_flags(s, herr);
+    if (rc != SPDP_OK) return rc;
+    if (herr[0]) return fail(SPDP_E_STATE, "count state has a cell with t > n or t = 0 < n");
+    *out = v;
+    return SPDP_OK;
+}
+
+int spdp_get_assignments(const spdp_state *s, int32_t *z, uint8_t *r, int where)
+{
+    if (!s) return fail(SPDP_E_ARG, "state is NULL");
+    if (where != 0 && where != 1) return fail(SPDP_E_ARG, "where must be 0 or 1");
+    HIP_TRY(hipSetDevice(s->device));
+    const Model &m = s->m;
+    if (m.N == 0 || (!z && !r)) return SPDP_OK;
+    if (where == 1) {
+        HIP_TRY(launch_unpack_zr(m, s->b.zr[s->cur], z, r, s->st));
+        return sync(s);
+    }
+    int32_t *zd = nullptr;
+    uint8_t *rd = nullptr;
+    HIP_TRY(hipMalloc(&zd, (size_t)m.N * sizeof(int32_t)));
+    hipError_t e = hipMalloc(&rd, (size_t)m.N);
+    if (e == hipSuccess) e = launch_unpack_zr(m, s->b.zr[s->cur], zd, rd, s->st);
+    if (e == hipSuccess && z) e = hipMemcpyAsync(z, zd, (size_t)m.N * 4, hipMemcpyDeviceToHost, s->st);
+    if (e == hipSuccess && r) e = hipMemcpyAsync(r, rd, (size_t)m.N, hipMemcpyDeviceToHost, s->st);
+    if (e == hipSuccess) e = hipStreamSynchronize(s->st);
+    hipFree(zd);
+    if (rd) hipFree(rd);
+    HIP_TRY(e);
+    return SPDP_OK;
+}
+
+int spdp_set_assignments(spdp_state *s, const int32_t *z, const uint8_t *r, int where)
+{
+    if (!s || !z || !r) return fail(SPDP_E_ARG, "null argument");
+    if (where != 0 && where != 1) return fail(SPDP_E_ARG, "where must be 0 or 1");
+    HIP_TRY(hipSetDevice(s->device));
+    const Model &m = s->m;
+    if (m.N > 0) {
+        const int32_t *zd = z;
+        const uint8_t *rd = r;
+        int32_t *zt = nullptr;
+        uint8_t *rt = nullptr;
+        if (where == 0) {
+            HIP_TRY(hipMalloc(&zt, (size_t)m.N * sizeof(int32_t)));
+            hipError_t e = hipMalloc(&rt, (size_t)m.N);
+            if (e == hipSuccess)
+                e = hipMemcpyAsync(zt, z, (size_t)m.N * 4, hipMemcpyHostToDevice, s->st);
+            if (e == hipSuccess) e = hipMemcpyAsync(rt, r, (size_t)m.N, hipMemcpyHostToDevice, s->st);
+            if (e != hipSuccess) {
+                hipFree(zt);
+                if (rt) hipFree(rt);
+                HIP_TRY(e);
+            }
+            zd = zt;
+            rd = rt;
+        }
+        HIP_TRY(launch_fill_i32(s->b.err, 2, 0, s->st));
+        hipError_t e = launch_pack_zr(m, zd, rd, s->b.zr[s->cur], s->b.err, s->st);
+        int32_t herr[2] = {0, 0};
+        if (e == hipSuccess) e = hipMemcpyAsync(herr, s->b.err, sizeof herr, hipMemcpyDeviceToHost, s->st);
+        if (e == hipSuccess) e = hipStreamSynchronize(s->st);
+        if (zt) hipFree(zt);
+        if (rt) hipFree(rt);
+        HIP_TRY(e);
+        if (herr[0] & 4) return fail(SPDP_E_ARG, "z out of [0, K) or r not in {0, 1}");
+    }
+    int rc = rebuild_state(s);
+    if (rc != SPDP_OK) return rc;
+    return sync(s);
+}
+
+int spdp_debug_conditionals(spdp_state *s, uint32_t sweep, uint64_t seed, int64_t tok_begin,
+                            int64_t tok_end, float *w_out, float *u_out, int32_t *zr_out,
+                            int where)
+{
+    if (!s) return fail(SPDP_E_ARG, "state is NULL");
+    const Model &m = s->m;
+    if (tok_begin < 0 || tok_end > m.N || tok_begin > tok_end)
+        return fail(SPDP_E_ARG, "bad token range");
+    if (where != 0 && where != 1) return fail(SPDP_E_ARG, "where must be 0 or 1");
+    HIP_TRY(hipSetDevice(s->device));
+    DeviceBuffers &b = s->b;
+    const int64_t T = tok_end - tok_begin;
+    if (T == 0) return SPDP_OK;
+    if (T > b.tr_cap) {
+        if (b.tr_w) hipFree(b.tr_w);
+        if (b.tr_u) hipFree(b.tr_u);
+        b.tr_w = nullptr;
+        b.tr_u = nullptr;
+        b.tr_cap = 0;
+        void *p = nullptr;
+        if (hipMalloc(&p, (size_t)T * 2 * m.K * sizeof(float)) != hipSuccess) {
+            (void)hipGetLastError();
+            return fail(SPDP_E_NOMEM, "trace buffer");
+        }
+        b.tr_w = (float *)p;
+        if (hipMalloc(&p, (size_t)T * sizeof(float)) != hipSuccess) {
+            (void)hipGetLastError();
+            return fail(SPDP_E_NOMEM, "trace buffer");
+        }
+        b.tr_u = (float *)p;
+        b.tr_cap = T;
+    }
+    HIP_TRY(launch_fill_i32((int32_t *)b.tr_w, T * 2 * m.K, 0, s->st));
+    HIP_TRY(launch_fill_i32((int32_t *)b.tr_u, T, 0, s->st));
+    int32_t *zr_old = b.zr[s->cur], *zr_tmp = b.zr[1 - s->cur];
+    HIP_TRY(launch_factors(m, b, s->st));
+    HIP_TRY(launch_sample(m, b, zr_old, zr_tmp, sweep, seed, b.tr_w, b.tr_u, tok_begin, tok_end,
+                          s->st));
+    const hipMemcpyKind kind = where ? hipMemcpyDeviceToDevice : hipMemcpyDeviceToHost;
+    if (w_out) HIP_TRY(hipMemcpyAsync(w_out, b.tr_w, (size_t)T * 2 * m.K * 4, kind, s->st));
+    if (u_out) HIP_TRY(hipMemcpyAsync(u_out, b.tr_u, (size_t)T * 4, kind, s->st));
+    if (zr_out) HIP_TRY(hipMemcpyAsync(zr_out, zr_tmp + tok_begin, (size_t)T * 4, kind, s->st));
+    return sync(s);
+}
+
+int spdp_stats(const spdp_state *s, int64_t *changed, int64_t *repaired)
+{
+    if (!s) return fail(SPDP_E_ARG, "state is NULL");
+    HIP_TRY(hipSetDevice(s->device));
+    unsigned long long c[4];
+    HIP_TRY(hipMemcpyAsync(c, s->b.ctr, sizeof c, hipMemcpyDeviceToHost, s->st));
+    int rc = sync(s);
+    if (rc != SPDP_OK) return rc;
+    if (changed) *changed = (int64_t)c[0];
+    if (repaired) *repaired = (int64_t)c[1];
+    return SPDP_OK;
+}
+
+int spdp_kernel_timing(spdp_state *s, int enable)
+{
+    if (!s) return fail(SPDP_E_ARG, "state is NULL");
+    HIP_TRY(hipSetDevice(s->device));
+    int rc = sync(s);
+    if (rc != SPDP_OK) return rc;
+    for (auto &v : s->events) {
+        for (auto &ev : v) {
+            hipEventDestroy(ev.a);
+            hipEventDestroy(ev.b);
+        }
+        v.clear();
+    }
+    s->timing = enable != 0;
+    return SPDP_OK;
+}
+
+int spdp_kernel_times(spdp_state *s, double *ms, int64_t *launches)
+{
+    if (!s) return fail(SPDP_E_ARG, "state is NULL");
+    HIP_TRY(hipSetDevice(s->device));
+    int rc = sync(s);
+    if (rc != SPDP_OK) return rc;
+    for (int c = 0; c < SPDP_NKERNELS; ++c) {
+        double acc = 0.0;
+        for (auto &ev : s->events[c]) {
+            float x = 0.0f;
+            HIP_TRY(hipEventElapsedTime(&x, ev.a, ev.b));
+            acc += x;
+        }
+        if (ms) ms[c] = acc;
+        if (launches) launches[c] = (int64_t)s->events[c].size();
+    }
+    return SPDP_OK;
+}
+
+int spdp_info(const spdp_state *s, int64_t *out8)
+{
+    if (!s || !out8) return fail(SPDP_E_ARG, "null argument");
+    const Model &m = s->m;
+    out8[0] = m.N;
+    out8[1] = m.D;
+    out8[2] = m.V;
+    out8[3] = m.G;
+    out8[4] = m.K;
+    out8[5] = m.Kp;
+    out8[6] = m.ncap;
+    out8[7] = s->bytes;
+    return SPDP_OK;
+}
+
+}  // extern "C"

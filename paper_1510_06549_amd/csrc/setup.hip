@@ -1,0 +1,527 @@
+// setup.hip -- state construction and count maintenance kernels (gfx950).
+//
+//   make_gw        token -> count-row index g V + w, per-(g, w) token counts
+//   stirling       log S^n_{t,a} rows (fp64 recurrence of the PYP joint,
+//                  Corollary 17 passage) and the folded ratio pairs used by the
+//                  sampler (Eq. SPDP-sampling-w-z-r0 / -r1 with P = I)
+//   init_z         initial topics from Philox (purpose INIT), r = 0
+//   rebuild        counts n, t, B from (z, r) with integer atomics
+//   update         per-token count deltas after a sweep (integer atomics)
+//   repair         promote the smallest-index token of every cell left with
+//                  customers but no table (atomicMin on an encoded index)
+//   totals         N_gk, T_gk by an LDS-privatised histogram; B_k = sum_g T_gk
+//   factors        per-(g, k) sweep constants of the conditionals
+#include <climits>
+
+#include "spdp_internal.hpp"
+
+namespace spdp {
+
+namespace {
+
+constexpr int kBlock = 256;
+
+inline int64_t blocks_for(int64_t n, int per_block)
+{
+    int64_t b = (n + per_block - 1) / per_block;
+    return b < 1 ? 1 : b;
+}
+
+// ----------------------------------------------------------------- fills
+template <typename T>
+__global__ void k_fill(T *__restrict__ p, int64_t n, T v)
+{
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride) p[i] = v;
+}
+
+template <typename T>
+hipError_t fill(T *p, int64_t n, T v, hipStream_t st)
+{
+    if (n <= 0) return hipSuccess;
+    int64_t nb = blocks_for(n, kBlock);
+    if (nb > 65536) nb = 65536;
+    hipLaunchKernelGGL(k_fill<T>, dim3((unsigned)nb), dim3(kBlock), 0, st, p, n, v);
+    return hipGetLastError();
+}
+
+// ---------------------------------------------------------------- make_gw
+// One block per document: row index per token, validation, per-row counts.
+__global__ void k_make_gw(int32_t D, int32_t V, int32_t G, const int32_t *__restrict__ words,
+                          const int64_t *__restrict__ doc_off, const int32_t *__restrict__ doc_group,
+                          int32_t *__restrict__ gw, int32_t *__restrict__ gw_count,
+                          int32_t *__restrict__ bad)
+{
+    const int32_t d = blockIdx.x;
+    if (d >= D) return;
+    const int32_t g = doc_group[d];
+    const int64_t beg = doc_off[d], end = doc_off[d + 1];
+    if (g < 0 || g >= G) {
+        if (threadIdx.x == 0) atomicOr(bad, 1);
+        return;
+    }
+    for (int64_t i = beg + threadIdx.x; i < end; i += blockDim.x) {
+        const int32_t w = words[i];
+        if (w < 0 || w >= V) {
+            atomicOr(bad, 2);
+            gw[i] = 0;
+            continue;
+        }
+        const int32_t q = g * V + w;
+        gw[i] = q;
+        atomicAdd(gw_count + q, 1);
+    }
+}
+
+// --------------------------------------------------------------- max int32
+__global__ void k_max_i32(const int32_t *__restrict__ x, int64_t n, int32_t *__restrict__ out)
+{
+    int32_t m = 0;
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride)
+        m = max(m, x[i]);
+    for (int o = 32; o > 0; o >>= 1) m = max(m, __shfl_xor(m, o));
+    if ((threadIdx.x & 63) == 0) atomicMax(out, m);
+}
+
+// --------------------------------------------------------------- Stirling
+// One workgroup walks the rows: row n + 1 from row n,
+//   S^{n+1}_t = S^n_{t-1} + (n - t a) S^n_t,  S^n_0 = [n == 0],  S^n_t = 0 (t > n),
+// in log space (log-sum-exp of the two terms).
+__global__ void __launch_bounds__(1024) k_stirling_rows(int32_t nmax, double a,
+                                                        double *__restrict__ logS)
+{
+    if (threadIdx.x == 0) logS[0] = 0.0;
+    __syncthreads();
+    for (int64_t n = 0; n < nmax; ++n) {
+        const double *row = logS + tri_index(n, 0);
+        double *next = logS + tri_index(n + 1, 0);
+        for (int64_t t = threadIdx.x; t <= n + 1; t += blockDim.x) {
+            double v;
+            if (t == 0) {
+                v = -INFINITY;
+            } else {
+                const double left = row[t - 1];
+                const double same = (t <= n) ? row[t] : -INFINITY;
+                const double term = (same == -INFINITY) ? -INFINITY
+                                                        : same + log((double)n - (double)t * a);
+                if (left == -INFINITY) v = term;
+                else if (term == -INFINITY) v = left;
+                else {
+                    const double hi = fmax(left, term), lo = fmin(left, term);
+                    v = hi + log1p(exp(lo - hi));
+                }
+            }
+            next[t] = v;
+        }
+        __threadfence_block();
+        __syncthreads();
+    }
+}
+
+// Folded ratio pairs for 0 <= t <= n < nmax, computed in fp64, rounded once:
+//   Q0(n, t) = (n - t + 1)/(n + 1) * S^{n+1}_t / S^n_t        (outcome r = 0)
+//   Q1(n, t) = (t + 1)/(n + 1) * S^{n+1}_{t+1} / S^n_t        (outcome r = 1)
+// with Q(0, 0) = (0, 1); entries with t = 0 < n (no valid state) are (0, 0).
+__global__ void k_stirling_pairs(int32_t nmax, const double *__restrict__ logS,
+                                 float2 *__restrict__ Q)
+{
+    const int64_t n = blockIdx.y;
+    const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (n >= nmax || t > n) return;
+    float2 q;
+    if (n == 0) {
+        q = make_float2(0.0f, 1.0f);
+    } else if (t == 0) {
+        q = make_float2(0.0f, 0.0f);
+    } else {
+        const double base = logS[tri_index(n, t)];
+        const double r0 = exp(logS[tri_index(n + 1, t)] - base);
+        const double r1 = exp(logS[tri_index(n + 1, t + 1)] - base);
+        const double inv = 1.0 / (double)(n + 1);
+        q = make_float2((float)((double)(n - t + 1) * inv * r0), (float)((double)(t + 1) * inv * r1));
+    }
+    Q[tri_index(n, t)] = q;
+}
+
+__global__ void k_lfact(int32_t nmax, double *__restrict__ lfact)
+{
+    const int64_t n = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (n <= nmax) lfact[n] = lgamma((double)n + 1.0);
+}
+
+// ----------------------------------------------------------------- init z
+__global__ void k_init_z(int64_t N, int32_t K, uint64_t seed, int32_t *__restrict__ zr)
+{
+    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= N) return;
+    const uint32_t x = philox_x0(seed, (uint64_t)i, 0u, kPurposeInit);
+    const int32_t z = (int32_t)(((uint64_t)x * (uint64_t)K) >> 32);
+    zr[i] = zr_pack(z, 0);
+}
+
+__global__ void k_pack_zr(int64_t N, int32_t K, const int32_t *__restrict__ z,
+                          const uint8_t *__restrict__ r, int32_t *__restrict__ zr,
+                          int32_t *__restrict__ bad)
+{
+    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= N) return;
+    int32_t zi = z[i];
+    int32_t ri = r[i];
+    if (zi < 0 || zi >= K || ri > 1) {
+        atomicOr(bad, 4);
+        zi = 0;
+        ri = 0;
+    }
+    zr[i] = zr_pack(zi, ri);
+}
+
+__global__ void k_unpack_zr(int64_t N, const int32_t *__restrict__ zr, int32_t *__restrict__ z,
+                            uint8_t *__restrict__ r)
+{
+    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= N) return;
+    const int32_t v = zr[i];
+    if (z) z[i] = v >> 1;
+    if (r) r[i] = (uint8_t)(v & 1);
+}
+
+// ---------------------------------------------------------------- rebuild
+__global__ void k_rebuild(int64_t N, int32_t V, int32_t Kp, FastDiv divV,
+                          const int32_t *__restrict__ gw, const int32_t *__restrict__ zr,
+                          int32_t *__restrict__ n, int32_t *__restrict__ t, int32_t *__restrict__ B)
+{
+    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= N) return;
+    const int32_t q = gw[i];
+    const int32_t v = zr[i];
+    const int32_t k = v >> 1;
+    atomicAdd(n + (int64_t)q * Kp + k, 1);
+    if (v & 1) {
+        const int32_t g = (int32_t)fastdiv((uint32_t)q, divV);
+        const int32_t w = q - g * V;
+        atomicAdd(t + (int64_t)q * Kp + k, 1);
+        atomicAdd(B + (int64_t)w * Kp + k, 1);
+    }
+}
+
+// ----------------------------------------------------------------- update
+// Apply the change of every token whose (z, r) moved.  A table count that
+// drops to zero flags its row for the repair step.
+__global__ void k_update(int64_t N, int32_t V, int32_t Kp, FastDiv divV,
+                         const int32_t *__restrict__ gw, const int32_t *__restrict__ zr_old,
+                         const int32_t *__restrict__ zr_new, int32_t *__restrict__ n,
+                         int32_t *__restrict__ t, int32_t *__restrict__ B,
+                         uint32_t *__restrict__ flags, unsigned long long *__restrict__ ctr)
+{
+    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    bool moved = false;
+    if (i < N) {
+        const int32_t vo = zr_old[i], vn = zr_new[i];
+        if (vo != vn) {
+            moved = true;
+            const int32_t q = gw[i];
+            const int32_t g = (int32_t)fastdiv((uint32_t)q, divV);
+            const int32_t w = q - g * V;
+            const int32_t k0 = vo >> 1, k1 = vn >> 1;
+            const int64_t row = (int64_t)q * Kp;
+            if (k0 != k1) {
+                atomicSub(n + row + k0, 1);
+                atomicAdd(n + row + k1, 1);
+            }
+            if (vo & 1) {
+                const int32_t old = atomicSub(t + row + k0, 1);
+                atomicSub(B + (int64_t)w * Kp + k0, 1);
+                if (old == 1) {
+                    const uint32_t bit = 1u << (q & 31);
+                    const uint32_t prev = atomicOr(flags + (q >> 5), bit);
+                    if (!(prev & bit)) atomicAdd(ctr + 2, 1ull);
+                }
+            }
+            if (vn & 1) {
+                atomicAdd(t + row + k1, 1);
+                atomicAdd(B + (int64_t)w * Kp + k1, 1);
+            }
+        }
+    }
+    const unsigned long long m = __ballot(moved);
+    if ((threadIdx.x & 63) == 0 && m) atomicAdd(ctr + 0, (unsigned long long)__popcll(m));
+}
+
+// ----------------------------------------------------------------- repair
+// Pass 1: tokens with r = 0 in a flagged row whose cell has no table bid for
+// the head with atomicMin(t, INT_MIN + i) (t <= 0 there, so the minimum
+// encodes the smallest token index).  Pass 2: the winner becomes the head.
+__device__ __forceinline__ bool row_flagged(const uint32_t *flags, int32_t q)
+{
+    return (flags[q >> 5] >> (q & 31)) & 1u;
+}
+
+__global__ void k_repair_bid(int64_t N, int32_t Kp, const int32_t *__restrict__ gw,
+                             const int32_t *__restrict__ zr, int32_t *__restrict__ t,
+                             const uint32_t *__restrict__ flags,
+                             const unsigned long long *__restrict__ ctr)
+{
+    if (ctr[2] == 0) return;
+    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= N) return;
+    const int32_t v = zr[i];
+    if (v & 1) return;
+    const int32_t q = gw[i];
+    if (!row_flagged(flags, q)) return;
+    int32_t *cell = t + (int64_t)q * Kp + (v >> 1);
+    if (__hip_atomic_load(cell, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) <= 0)
+        atomicMin(cell, INT_MIN + (int32_t)i);
+}
+
+__global__ void k_repair_apply(int64_t N, int32_t V, int32_t Kp, FastDiv divV,
+                               const int32_t *__restrict__ gw, int32_t *__restrict__ zr,
+                               int32_t *__restrict__ t, int32_t *__restrict__ B,
+                               const uint32_t *__restrict__ flags,
+                               unsigned long long *__restrict__ ctr)
+{
+    if (ctr[2] == 0) return;
+    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    bool won = false;
+    if (i < N) {
+        const int32_t v = zr[i];
+        if (!(v & 1)) {
+            const int32_t q = gw[i];
+            if (row_flagged(flags, q)) {
+                const int32_t k = v >> 1;
+                int32_t *cell = t + (int64_t)q * Kp + k;
+                if (__hip_atomic_load(cell, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) ==
+                    INT_MIN + (int32_t)i) {
+                    won = true;
+                    zr[i] = v | 1;
+                    __hip_atomic_store(cell, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                    const int32_t g = (int32_t)fastdiv((uint32_t)q, divV);
+                    atomicAdd(B + (int64_t)(q - g * V) * Kp + k, 1);
+                }
+            }
+        }
+    }
+    const unsigned long long m = __ballot(won);
+    if ((threadIdx.x & 63) == 0 && m) atomicAdd(ctr + 1, (unsigned long long)__popcll(m));
+}
+
+// ----------------------------------------------------------------- totals
+// Per block, a chunk of at most 65535 tokens is histogrammed into LDS bins of
+// (g, k), each bin packing customers (low 16 bits) and tables (high 16 bits);
+// non-zero bins are flushed with global atomics.
+constexpr int kTotalsChunk = 32768;
+
+__global__ void __launch_bounds__(1024) k_totals_lds(int64_t N, int32_t Kp, int32_t bins,
+                                                     FastDiv divV, const int32_t *__restrict__ gw,
+                                                     const int32_t *__restrict__ zr,
+                                                     int32_t *__restrict__ Ngk,
+                                                     int32_t *__restrict__ Tgk)
+{
+    extern __shared__ uint32_t h[];
+    for (int j = threadIdx.x; j < bins; j += blockDim.x) h[j] = 0u;
+    __syncthreads();
+    const int64_t beg = (int64_t)blockIdx.x * kTotalsChunk;
+    const int64_t end = min(beg + (int64_t)kTotalsChunk, N);
+    for (int64_t i = beg + threadIdx.x; i < end; i += blockDim.x) {
+        const int32_t v = zr[i];
+        const int32_t g = (int32_t)fastdiv((uint32_t)gw[i], divV);
+        atomicAdd(&h[g * Kp + (v >> 1)], 1u + ((uint32_t)(v & 1) << 16));
+    }
+    __syncthreads();
+    for (int j = threadIdx.x; j < bins; j += blockDim.x) {
+        const uint32_t x = h[j];
+        if (x) {
+            atomicAdd(Ngk + j, (int32_t)(x & 0xFFFFu));
+            if (x >> 16) atomicAdd(Tgk + j, (int32_t)(x >> 16));
+        }
+    }
+}
+
+__global__ void k_totals_global(int64_t N, int32_t Kp, FastDiv divV,
+                                const int32_t *__restrict__ gw, const int32_t *__restrict__ zr,
+                                int32_t *__restrict__ Ngk, int32_t *__restrict__ Tgk)
+{
+    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= N) return;
+    const int32_t v = zr[i];
+    const int32_t g = (int32_t)fastdiv((uint32_t)gw[i], divV);
+    atomicAdd(Ngk + g * Kp + (v >> 1), 1);
+    if (v & 1) atomicAdd(Tgk + g * Kp + (v >> 1), 1);
+}
+
+__global__ void k_topic_tables(int32_t G, int32_t Kp, const int32_t *__restrict__ Tgk,
+                               int32_t *__restrict__ Bk)
+{
+    const int32_t k = blockIdx.x * blockDim.x + threadIdx.x;
+    if (k >= Kp) return;
+    int32_t s = 0;
+    for (int32_t g = 0; g < G; ++g) s += Tgk[(int64_t)g * Kp + k];
+    Bk[k] = s;
+}
+
+// ---------------------------------------------------------------- factors
+// f0[g][k] = 1 / (b + N_gk)
+// f1[g][k] = (b + a T_gk) / (b + N_gk) / (V gamma + B_k)
+// computed in fp64 and rounded once; padding topics (k >= K) get 0, so their
+// outcomes carry zero weight.
+__global__ void k_factors(int32_t G, int32_t K, int32_t Kp, double a, double b, double Vgamma,
+                          const int32_t *__restrict__ Ngk, const int32_t *__restrict__ Tgk,
+                          const int32_t *__restrict__ Bk, float *__restrict__ f0,
+                          float *__restrict__ f1)
+{
+    const int64_t j = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (j >= (int64_t)G * Kp) return;
+    const int32_t k = (int32_t)(j % Kp);
+    if (k >= K) {
+        f0[j] = 0.0f;
+        f1[j] = 0.0f;
+        return;
+    }
+    const double inv = 1.0 / (b + (double)Ngk[j]);
+    f0[j] = (float)inv;
+    f1[j] = (float)((b + a * (double)Tgk[j]) * inv / (Vgamma + (double)Bk[k]));
+}
+
+}  // namespace
+
+// ======================================================================
+// launchers
+// ======================================================================
+hipError_t launch_fill_i32(int32_t *p, int64_t n, int32_t v, hipStream_t st) { return fill(p, n, v, st); }
+hipError_t launch_fill_u32(uint32_t *p, int64_t n, uint32_t v, hipStream_t st) { return fill(p, n, v, st); }
+hipError_t launch_fill_u64(unsigned long long *p, int64_t n, unsigned long long v, hipStream_t st)
+{
+    return fill(p, n, v, st);
+}
+
+hipError_t launch_make_gw(const Model &m, const int32_t *words, const int64_t *doc_off,
+                          const int32_t *doc_group, int32_t *gw, int32_t *gw_count, int32_t *bad,
+                          hipStream_t st)
+{
+    if (m.D <= 0) return hipSuccess;
+    hipLaunchKernelGGL(k_make_gw, dim3(m.D), dim3(kBlock), 0, st, m.D, m.V, m.G, words, doc_off,
+                       doc_group, gw, gw_count, bad);
+    return hipGetLastError();
+}
+
+hipError_t launch_max_i32(const int32_t *x, int64_t n, int32_t *out, hipStream_t st)
+{
+    int64_t nb = blocks_for(n, kBlock);
+    if (nb > 4096) nb = 4096;
+    hipLaunchKernelGGL(k_max_i32, dim3((unsigned)nb), dim3(kBlock), 0, st, x, n, out);
+    return hipGetLastError();
+}
+
+hipError_t launch_stirling(const Model &m, double *logS, float2 *Q, double *lfact, hipStream_t st)
+{
+    const int32_t nmax = m.ncap;  // rows 0..ncap of log S; pairs for n < ncap
+    hipLaunchKernelGGL(k_stirling_rows, dim3(1), dim3(1024), 0, st, nmax, m.a, logS);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    dim3 grid((unsigned)blocks_for(nmax, kBlock), (unsigned)nmax);
+    hipLaunchKernelGGL(k_stirling_pairs, grid, dim3(kBlock), 0, st, nmax, logS, Q);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(k_lfact, dim3((unsigned)blocks_for(nmax + 1, kBlock)), dim3(kBlock), 0, st,
+                       nmax, lfact);
+    return hipGetLastError();
+}
+
+hipError_t launch_init_z(const Model &m, uint64_t seed, int32_t *zr, hipStream_t st)
+{
+    if (m.N <= 0) return hipSuccess;
+    hipLaunchKernelGGL(k_init_z, dim3((unsigned)blocks_for(m.N, kBlock)), dim3(kBlock), 0, st, m.N,
+                       m.K, seed, zr);
+    return hipGetLastError();
+}
+
+hipError_t launch_pack_zr(const Model &m, const int32_t *z, const uint8_t *r, int32_t *zr,
+                          int32_t *bad, hipStream_t st)
+{
+    if (m.N <= 0) return hipSuccess;
+    hipLaunchKernelGGL(k_pack_zr, dim3((unsigned)blocks_for(m.N, kBlock)), dim3(kBlock), 0, st, m.N,
+                       m.K, z, r, zr, bad);
+    return hipGetLastError();
+}
+
+hipError_t launch_unpack_zr(const Model &m, const int32_t *zr, int32_t *z, uint8_t *r,
+                            hipStream_t st)
+{
+    if (m.N <= 0) return hipSuccess;
+    hipLaunchKernelGGL(k_unpack_zr, dim3((unsigned)blocks_for(m.N, kBlock)), dim3(kBlock), 0, st,
+                       m.N, zr, z, r);
+    return hipGetLastError();
+}
+
+hipError_t launch_rebuild(const Model &m, const DeviceBuffers &b, const int32_t *zr, hipStream_t st)
+{
+    hipError_t e;
+    if ((e = fill(b.n, (int64_t)m.G * m.V * m.Kp, 0, st)) != hipSuccess) return e;
+    if ((e = fill(b.t, (int64_t)m.G * m.V * m.Kp, 0, st)) != hipSuccess) return e;
+    if ((e = fill(b.B, (int64_t)m.V * m.Kp, 0, st)) != hipSuccess) return e;
+    if (m.N <= 0) return hipSuccess;
+    hipLaunchKernelGGL(k_rebuild, dim3((unsigned)blocks_for(m.N, kBlock)), dim3(kBlock), 0, st, m.N,
+                       m.V, m.Kp, m.divV, b.gw, zr, b.n, b.t, b.B);
+    return hipGetLastError();
+}
+
+hipError_t launch_update(const Model &m, const DeviceBuffers &b, const int32_t *zr_old,
+                         const int32_t *zr_new, hipStream_t st)
+{
+    hipError_t e;
+    if ((e = fill(b.flags, ((int64_t)m.G * m.V + 31) / 32, 0u, st)) != hipSuccess) return e;
+    if ((e = fill(b.ctr, 4, 0ull, st)) != hipSuccess) return e;
+    if (m.N <= 0) return hipSuccess;
+    hipLaunchKernelGGL(k_update, dim3((unsigned)blocks_for(m.N, kBlock)), dim3(kBlock), 0, st, m.N,
+                       m.V, m.Kp, m.divV, b.gw, zr_old, zr_new, b.n, b.t, b.B, b.flags, b.ctr);
+    return hipGetLastError();
+}
+
+hipError_t launch_repair(const Model &m, const DeviceBuffers &b, int32_t *zr, hipStream_t st)
+{
+    if (m.N <= 0) return hipSuccess;
+    const unsigned nb = (unsigned)blocks_for(m.N, kBlock);
+    hipLaunchKernelGGL(k_repair_bid, dim3(nb), dim3(kBlock), 0, st, m.N, m.Kp, b.gw, zr, b.t,
+                       b.flags, b.ctr);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(k_repair_apply, dim3(nb), dim3(kBlock), 0, st, m.N, m.V, m.Kp, m.divV, b.gw,
+                       zr, b.t, b.B, b.flags, b.ctr);
+    return hipGetLastError();
+}
+
+hipError_t launch_totals(const Model &m, const DeviceBuffers &b, const int32_t *zr, hipStream_t st)
+{
+    hipError_t e;
+    const int64_t bins = (int64_t)m.G * m.Kp;
+    if ((e = fill(b.Ngk, bins, 0, st)) != hipSuccess) return e;
+    if ((e = fill(b.Tgk, bins, 0, st)) != hipSuccess) return e;
+    if (m.N > 0) {
+        int dev = 0, lds_max = 0;
+        hipGetDevice(&dev);
+        hipDeviceGetAttribute(&lds_max, hipDeviceAttributeMaxSharedMemoryPerBlock, dev);
+        const int64_t lds = bins * (int64_t)sizeof(uint32_t);
+        if (lds <= lds_max && lds <= 96 * 1024) {
+            const unsigned nb = (unsigned)blocks_for(m.N, kTotalsChunk);
+            hipLaunchKernelGGL(k_totals_lds, dim3(nb), dim3(1024), (size_t)lds, st, m.N, m.Kp,
+                               (int32_t)bins, m.divV, b.gw, zr, b.Ngk, b.Tgk);
+        } else {
+            hipLaunchKernelGGL(k_totals_global, dim3((unsigned)blocks_for(m.N, kBlock)), dim3(kBlock),
+                               0, st, m.N, m.Kp, m.divV, b.gw, zr, b.Ngk, b.Tgk);
+        }
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+    }
+    hipLaunchKernelGGL(k_topic_tables, dim3((unsigned)blocks_for(m.Kp, kBlock)), dim3(kBlock), 0, st,
+                       m.G, m.Kp, b.Tgk, b.Bk);
+    return hipGetLastError();
+}
+
+hipError_t launch_factors(const Model &m, const DeviceBuffers &b, hipStream_t st)
+{
+    const int64_t n = (int64_t)m.G * m.Kp;
+    hipLaunchKernelGGL(k_factors, dim3((unsigned)blocks_for(n, kBlock)), dim3(kBlock), 0, st, m.G,
+                       m.K, m.Kp, m.a, m.b, (double)m.V * m.gamma, b.Ngk, b.Tgk, b.Bk, b.f0, b.f1);
+    return hipGetLastError();
+}
+
+}  // namespace spdp

@@ -1,0 +1,150 @@
+// spdp_internal.hpp -- device-side data layout, helpers and kernel launchers
+// shared by the translation units of the gfx950 SPDP library.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "../../include/spdp.h"
+
+namespace spdp {
+
+// ---------------------------------------------------------------------------
+// Philox4x32-10 (Salmon, Moraes, Dror, Shaw, SC'11).  Counter (token lo, token
+// hi, sweep, purpose), key = seed.  Only word 0 of each block is used.
+// ---------------------------------------------------------------------------
+enum : uint32_t { kPurposeSample = 0u, kPurposeInit = 1u };
+
+__host__ __device__ __forceinline__ uint32_t philox_x0(uint64_t seed, uint64_t ctr_lo64,
+                                                       uint32_t c2, uint32_t c3)
+{
+    uint32_t x0 = (uint32_t)ctr_lo64, x1 = (uint32_t)(ctr_lo64 >> 32), x2 = c2, x3 = c3;
+    uint32_t k0 = (uint32_t)seed, k1 = (uint32_t)(seed >> 32);
+#pragma unroll
+    for (int r = 0; r < 10; ++r) {
+        const uint64_t p0 = (uint64_t)0xD2511F53u * x0;
+        const uint64_t p1 = (uint64_t)0xCD9E8D57u * x2;
+        const uint32_t y0 = (uint32_t)(p1 >> 32) ^ x1 ^ k0;
+        const uint32_t y1 = (uint32_t)p1;
+        const uint32_t y2 = (uint32_t)(p0 >> 32) ^ x3 ^ k1;
+        const uint32_t y3 = (uint32_t)p0;
+        x0 = y0; x1 = y1; x2 = y2; x3 = y3;
+        k0 += 0x9E3779B9u;
+        k1 += 0xBB67AE85u;
+    }
+    return x0;
+}
+
+// ---------------------------------------------------------------------------
+// Division of a non-negative int32 by a runtime constant d (1 <= d < 2^31) by
+// multiply-shift: q = (n * m) >> s with m = ceil(2^s / d), s = 31 + ceil(log2 d).
+// Exact for 0 <= n < 2^31 because n * (m d - 2^s) < 2^31 * d <= 2^s; m <= 2^32 + 1
+// so the 64-bit product n * m cannot overflow.
+// ---------------------------------------------------------------------------
+struct FastDiv {
+    uint64_t m;
+    uint32_t s;
+};
+
+inline FastDiv make_fastdiv(uint32_t d)
+{
+    uint32_t l = 0;
+    while ((1ull << l) < d) ++l;
+    FastDiv f;
+    f.s = 31 + l;
+    f.m = (uint64_t)((((unsigned __int128)1 << f.s) + d - 1) / d);
+    return f;
+}
+
+__host__ __device__ __forceinline__ uint32_t fastdiv(uint32_t n, FastDiv f)
+{
+    return (uint32_t)(((uint64_t)n * f.m) >> f.s);
+}
+
+// Packed per-token state: zr = 2 z + r.
+__host__ __device__ __forceinline__ int32_t zr_pack(int32_t z, int32_t r) { return 2 * z + r; }
+
+// Index of (n, t) in a lower-triangular table with row n at n (n + 1) / 2.
+__host__ __device__ __forceinline__ int64_t tri_index(int64_t n, int64_t t)
+{
+    return n * (n + 1) / 2 + t;
+}
+
+// ---------------------------------------------------------------------------
+// Device state.  Count rows: row index q = g V + w; row q of n / t holds the
+// Kp topic entries of (g, w) (Kp = K rounded up to the sampler's vector width,
+// padding entries stay zero).  B rows are indexed by w.
+// ---------------------------------------------------------------------------
+struct Model {
+    int64_t N;
+    int32_t D, V, G, K, Kp;
+    float alpha_f, a_f, b_f, gamma_f, Vgamma_f;
+    double alpha, a, b, gamma;
+    int32_t ncap;  // largest per-(g, w) token count: every n' < ncap in a sweep
+    FastDiv divV;  // q -> g
+};
+
+struct DeviceBuffers {
+    int32_t *gw = nullptr;        // [N]  row index g V + w of each token
+    int64_t *doc_off = nullptr;   // [D+1]
+    int32_t *doc_group = nullptr; // [D]
+    int32_t *zr[2] = {nullptr, nullptr}; // [N] current / next packed state
+    int32_t *n = nullptr;         // [G V][Kp]
+    int32_t *t = nullptr;         // [G V][Kp]
+    int32_t *B = nullptr;         // [V][Kp]
+    int32_t *Ngk = nullptr;       // [G][Kp]
+    int32_t *Tgk = nullptr;       // [G][Kp]
+    int32_t *Bk = nullptr;        // [Kp]
+    float *f0 = nullptr;          // [G][Kp] 1 / (b + N_gk)
+    float *f1 = nullptr;          // [G][Kp] (b + a T_gk) / (b + N_gk) / (V gamma + B_k)
+    float2 *Q = nullptr;          // [tri(ncap)] (Q0, Q1) folded Stirling ratios
+    double *logS = nullptr;       // [tri(ncap + 1)] log S^n_{t,a}
+    double *lfact = nullptr;      // [ncap + 1] log n!
+    uint32_t *flags = nullptr;    // [ceil(G V / 32)] rows whose t hit zero
+    unsigned long long *ctr = nullptr; // [4] changed, repaired, flagged rows, spare
+    double *partial = nullptr;    // loglik block partials
+    int64_t partial_len = 0;
+    int32_t *err = nullptr;       // [2] device error flags
+    double *scalar = nullptr;     // [1] reduction result
+    // debug-conditional buffers (allocated on demand)
+    float *tr_w = nullptr;
+    float *tr_u = nullptr;
+    int64_t tr_cap = 0;
+};
+
+// ---------------------------------------------------------------------------
+// Kernel launchers (each returns hipSuccess or the launch error).
+// ---------------------------------------------------------------------------
+hipError_t launch_fill_i32(int32_t *p, int64_t n, int32_t v, hipStream_t st);
+hipError_t launch_fill_u32(uint32_t *p, int64_t n, uint32_t v, hipStream_t st);
+hipError_t launch_fill_u64(unsigned long long *p, int64_t n, unsigned long long v, hipStream_t st);
+hipError_t launch_make_gw(const Model &m, const int32_t *words, const int64_t *doc_off,
+                          const int32_t *doc_group, int32_t *gw, int32_t *gw_count,
+                          int32_t *bad, hipStream_t st);
+hipError_t launch_max_i32(const int32_t *x, int64_t n, int32_t *out, hipStream_t st);
+hipError_t launch_stirling(const Model &m, double *logS, float2 *Q, double *lfact, hipStream_t st);
+hipError_t launch_init_z(const Model &m, uint64_t seed, int32_t *zr, hipStream_t st);
+hipError_t launch_pack_zr(const Model &m, const int32_t *z, const uint8_t *r, int32_t *zr,
+                          int32_t *bad, hipStream_t st);
+hipError_t launch_unpack_zr(const Model &m, const int32_t *zr, int32_t *z, uint8_t *r,
+                            hipStream_t st);
+hipError_t launch_rebuild(const Model &m, const DeviceBuffers &b, const int32_t *zr,
+                          hipStream_t st);
+hipError_t launch_update(const Model &m, const DeviceBuffers &b, const int32_t *zr_old,
+                         const int32_t *zr_new, hipStream_t st);
+hipError_t launch_repair(const Model &m, const DeviceBuffers &b, int32_t *zr, hipStream_t st);
+hipError_t launch_totals(const Model &m, const DeviceBuffers &b, const int32_t *zr,
+                         hipStream_t st);
+hipError_t launch_factors(const Model &m, const DeviceBuffers &b, hipStream_t st);
+hipError_t launch_sample(const Model &m, const DeviceBuffers &b, const int32_t *zr_old,
+                         int32_t *zr_new, uint32_t sweep, uint64_t seed, float *tr_w,
+                         float *tr_u, int64_t tr_begin, int64_t tr_end, hipStream_t st);
+hipError_t launch_loglik(const Model &m, const DeviceBuffers &b, const int32_t *zr,
+                         hipStream_t st);
+int64_t loglik_partials_needed();
+
+// The sampler's per-lane topic count for K topics (4 at most per dwordx4).
+int sampler_kpl(int32_t K);
+int32_t padded_K(int32_t K);
+
+}  // namespace spdp

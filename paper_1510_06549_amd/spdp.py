@@ -1,0 +1,288 @@
+"""ctypes binding of libspdp.so (the C ABI declared in include/spdp.h).
+
+Argument marshalling only: every step of the sweep runs in the library's HIP
+kernels.  Host buffers are numpy arrays (``where = 0``); device buffers are
+torch tensors on the GPU (``where = 1``).  The library is required: importing
+this module raises if ``libspdp.so`` has not been built.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libspdp.so")
+
+SPDP_OK = 0
+SPDP_E_ARG = -1
+SPDP_E_NOMEM = -2
+SPDP_E_HIP = -3
+SPDP_E_RANGE = -4
+SPDP_E_STATE = -5
+SPDP_MAX_K = 1024
+SPDP_NKERNELS = 4
+KERNEL_CLASSES = ("sample", "update", "repair", "totals")
+
+# Every entry point of include/spdp.h, in declaration order.
+EXPORTS = (
+    "spdp_create", "spdp_sweep", "spdp_counts", "spdp_totals", "spdp_loglik", "spdp_destroy",
+    "spdp_get_assignments", "spdp_set_assignments", "spdp_debug_conditionals", "spdp_stats",
+    "spdp_kernel_timing", "spdp_kernel_times", "spdp_info", "spdp_last_error",
+)
+
+
+class SpdpError(RuntimeError):
+    def __init__(self, code: int, msg: str):
+        super().__init__(f"spdp error {code}: {msg}")
+        self.code = code
+
+
+class _Corpus(C.Structure):
+    _fields_ = [
+        ("n_tokens", C.c_int64),
+        ("n_docs", C.c_int32),
+        ("vocab", C.c_int32),
+        ("words", C.c_void_p),
+        ("doc_offsets", C.c_void_p),
+        ("init_seed", C.c_uint64),
+        ("hip_stream", C.c_void_p),
+    ]
+
+
+class _Groups(C.Structure):
+    _fields_ = [("n_groups", C.c_int32), ("doc_group", C.c_void_p)]
+
+
+def load_library() -> C.CDLL:
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(
+            f"{LIB_PATH} is missing: build it with `python -c 'import __graft_entry__ as g; "
+            f"g.build()'` (hipcc, gfx950) -- there is no fallback implementation")
+    L = C.CDLL(LIB_PATH)
+    vp, i32, i64, u32, u64, dbl = C.c_void_p, C.c_int32, C.c_int64, C.c_uint32, C.c_uint64, C.c_double
+    cint = C.c_int
+    L.spdp_create.argtypes = [vp, vp, i32, dbl, dbl, dbl, dbl, C.POINTER(vp)]
+    L.spdp_create.restype = cint
+    L.spdp_sweep.argtypes = [vp, u32, u64]
+    L.spdp_sweep.restype = cint
+    L.spdp_counts.argtypes = [vp, i32, i32, vp, vp, cint]
+    L.spdp_counts.restype = cint
+    L.spdp_totals.argtypes = [vp, vp, vp, vp, vp, cint]
+    L.spdp_totals.restype = cint
+    L.spdp_loglik.argtypes = [vp, C.POINTER(dbl)]
+    L.spdp_loglik.restype = cint
+    L.spdp_destroy.argtypes = [vp]
+    L.spdp_destroy.restype = None
+    L.spdp_get_assignments.argtypes = [vp, vp, vp, cint]
+    L.spdp_get_assignments.restype = cint
+    L.spdp_set_assignments.argtypes = [vp, vp, vp, cint]
+    L.spdp_set_assignments.restype = cint
+    L.spdp_debug_conditionals.argtypes = [vp, u32, u64, i64, i64, vp, vp, vp, cint]
+    L.spdp_debug_conditionals.restype = cint
+    L.spdp_stats.argtypes = [vp, C.POINTER(i64), C.POINTER(i64)]
+    L.spdp_stats.restype = cint
+    L.spdp_kernel_timing.argtypes = [vp, cint]
+    L.spdp_kernel_timing.restype = cint
+    L.spdp_kernel_times.argtypes = [vp, vp, vp]
+    L.spdp_kernel_times.restype = cint
+    L.spdp_info.argtypes = [vp, vp]
+    L.spdp_info.restype = cint
+    L.spdp_last_error.argtypes = []
+    L.spdp_last_error.restype = C.c_char_p
+    return L
+
+
+_lib = None
+
+
+def lib() -> C.CDLL:
+    global _lib
+    if _lib is None:
+        _lib = load_library()
+    return _lib
+
+
+def spdp_last_error() -> str:
+    return lib().spdp_last_error().decode()
+
+
+def _check(rc: int):
+    if rc != SPDP_OK:
+        raise SpdpError(rc, spdp_last_error())
+
+
+def _buf(x):
+    """(pointer, where) of a numpy array (host) or a torch CUDA tensor (device)."""
+    if x is None:
+        return None, 0
+    if isinstance(x, np.ndarray):
+        assert x.flags.c_contiguous
+        return x.ctypes.data, 0
+    # torch tensor
+    assert x.is_contiguous()
+    return x.data_ptr(), (1 if x.is_cuda else 0)
+
+
+def _where(*bufs) -> int:
+    ws = {w for p, w in (_buf(b) for b in bufs) if p is not None}
+    if len(ws) > 1:
+        raise ValueError("mix of host and device buffers in one call")
+    return ws.pop() if ws else 0
+
+
+# ---------------------------------------------------------------------------
+# Entry points (same names as the C ABI)
+# ---------------------------------------------------------------------------
+def spdp_create(words, doc_offsets, doc_group, n_groups, vocab, K, alpha, a, b, gamma,
+                init_seed=0, hip_stream=None):
+    words = np.ascontiguousarray(words, dtype=np.int32)
+    doc_offsets = np.ascontiguousarray(doc_offsets, dtype=np.int64)
+    doc_group = np.ascontiguousarray(doc_group, dtype=np.int32)
+    corpus = _Corpus(int(words.shape[0]), int(doc_group.shape[0]), int(vocab), words.ctypes.data,
+                     doc_offsets.ctypes.data, int(init_seed) & (2**64 - 1),
+                     None if hip_stream is None else int(hip_stream))
+    groups = _Groups(int(n_groups), doc_group.ctypes.data)
+    h = C.c_void_p()
+    _check(lib().spdp_create(C.byref(corpus), C.byref(groups), int(K), float(alpha), float(a),
+                             float(b), float(gamma), C.byref(h)))
+    return h
+
+
+def spdp_sweep(h, sweep: int, seed: int):
+    _check(lib().spdp_sweep(h, int(sweep) & 0xFFFFFFFF, int(seed) & (2**64 - 1)))
+
+
+def spdp_counts(h, g_begin, g_end, n_out=None, t_out=None):
+    where = _where(n_out, t_out)
+    _check(lib().spdp_counts(h, int(g_begin), int(g_end), _buf(n_out)[0], _buf(t_out)[0], where))
+
+
+def spdp_totals(h, N_gk=None, T_gk=None, B_wk=None, B_k=None):
+    where = _where(N_gk, T_gk, B_wk, B_k)
+    _check(lib().spdp_totals(h, _buf(N_gk)[0], _buf(T_gk)[0], _buf(B_wk)[0], _buf(B_k)[0], where))
+
+
+def spdp_loglik(h) -> float:
+    out = C.c_double()
+    _check(lib().spdp_loglik(h, C.byref(out)))
+    return float(out.value)
+
+
+def spdp_destroy(h):
+    if h:
+        lib().spdp_destroy(h)
+
+
+def spdp_get_assignments(h, z_out=None, r_out=None):
+    where = _where(z_out, r_out)
+    _check(lib().spdp_get_assignments(h, _buf(z_out)[0], _buf(r_out)[0], where))
+
+
+def spdp_set_assignments(h, z, r):
+    if isinstance(z, np.ndarray):
+        z = np.ascontiguousarray(z, dtype=np.int32)
+        r = np.ascontiguousarray(r, dtype=np.uint8)
+    where = _where(z, r)
+    _check(lib().spdp_set_assignments(h, _buf(z)[0], _buf(r)[0], where))
+
+
+def spdp_debug_conditionals(h, sweep, seed, tok_begin, tok_end, w_out=None, u_out=None,
+                            zr_out=None):
+    where = _where(w_out, u_out, zr_out)
+    _check(lib().spdp_debug_conditionals(h, int(sweep) & 0xFFFFFFFF, int(seed) & (2**64 - 1),
+                                         int(tok_begin), int(tok_end), _buf(w_out)[0],
+                                         _buf(u_out)[0], _buf(zr_out)[0], where))
+
+
+def spdp_stats(h):
+    c, r = C.c_int64(), C.c_int64()
+    _check(lib().spdp_stats(h, C.byref(c), C.byref(r)))
+    return int(c.value), int(r.value)
+
+
+def spdp_kernel_timing(h, enable: bool):
+    _check(lib().spdp_kernel_timing(h, 1 if enable else 0))
+
+
+def spdp_kernel_times(h):
+    ms = np.zeros(SPDP_NKERNELS, dtype=np.float64)
+    n = np.zeros(SPDP_NKERNELS, dtype=np.int64)
+    _check(lib().spdp_kernel_times(h, ms.ctypes.data, n.ctypes.data))
+    return {k: (float(ms[i]), int(n[i])) for i, k in enumerate(KERNEL_CLASSES)}
+
+
+def spdp_info(h) -> dict:
+    out = np.zeros(8, dtype=np.int64)
+    _check(lib().spdp_info(h, out.ctypes.data))
+    keys = ("N", "D", "V", "G", "K", "Kp", "ncap", "device_bytes")
+    return {k: int(v) for k, v in zip(keys, out)}
+
+
+# ---------------------------------------------------------------------------
+# Convenience wrapper (host numpy in and out)
+# ---------------------------------------------------------------------------
+class Sampler:
+    """Owns one library state; thin host-side helpers around the entry points."""
+
+    def __init__(self, words, doc_offsets, doc_group, n_groups, vocab, K, alpha, a, b, gamma,
+                 init_seed=0, hip_stream=None):
+        self.h = spdp_create(words, doc_offsets, doc_group, n_groups, vocab, K, alpha, a, b, gamma,
+                             init_seed, hip_stream)
+        self.info = spdp_info(self.h)
+        self.N, self.G, self.V, self.K = (self.info["N"], self.info["G"], self.info["V"],
+                                          self.info["K"])
+
+    def close(self):
+        if self.h:
+            spdp_destroy(self.h)
+            self.h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def sweep(self, sweep, seed):
+        spdp_sweep(self.h, sweep, seed)
+
+    def assignments(self):
+        z = np.empty(self.N, dtype=np.int32)
+        r = np.empty(self.N, dtype=np.uint8)
+        spdp_get_assignments(self.h, z, r)
+        return z, r
+
+    def set_assignments(self, z, r):
+        spdp_set_assignments(self.h, z, r)
+
+    def counts(self, g_begin=0, g_end=None):
+        """n, t as [g][w][k] int32 arrays."""
+        g_end = self.G if g_end is None else g_end
+        n = np.empty((g_end - g_begin, self.V, self.K), dtype=np.int32)
+        t = np.empty_like(n)
+        spdp_counts(self.h, g_begin, g_end, n, t)
+        return n, t
+
+    def totals(self):
+        N = np.empty((self.G, self.K), dtype=np.int32)
+        T = np.empty_like(N)
+        B = np.empty((self.V, self.K), dtype=np.int32)
+        Bk = np.empty(self.K, dtype=np.int32)
+        spdp_totals(self.h, N, T, B, Bk)
+        return N, T, B, Bk
+
+    def loglik(self):
+        return spdp_loglik(self.h)
+
+    def conditionals(self, sweep, seed, tok_begin, tok_end):
+        T = tok_end - tok_begin
+        w = np.zeros((T, 2 * self.K), dtype=np.float32)
+        u = np.zeros(T, dtype=np.float32)
+        zr = np.zeros(T, dtype=np.int32)
+        spdp_debug_conditionals(self.h, sweep, seed, tok_begin, tok_end, w, u, zr)
+        return w, u, zr
+
+    def stats(self):
+        return spdp_stats(self.h)

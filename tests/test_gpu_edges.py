@@ -1,0 +1,108 @@
+"""GPU edge cases: empty and ragged documents, tiny corpora, topic-count
+boundaries of the sampler's lane layout, maximum K, a = 0."""
+import math
+
+import numpy as np
+import pytest
+
+import oracle
+import synth
+from tests import parity
+
+pytestmark = pytest.mark.gpu
+
+
+def say(*a):
+    print(*a, flush=True)
+
+
+class W:  # minimal workload stand-in
+    def __init__(self, K, alpha=0.1, a=0.5, b=10.0, gamma=0.01):
+        self.K, self.alpha, self.a, self.b, self.gamma = K, alpha, a, b, gamma
+
+
+def corpus_from_docs(docs, vocab):
+    words = np.array([w for _, d in docs for w in d], np.int32)
+    doc_off = np.cumsum([0] + [len(d) for _, d in docs]).astype(np.int64)
+    doc_group = np.array([g for g, _ in docs], np.int32)
+    return synth.Corpus(words, doc_off, doc_group, np.zeros_like(words),
+                        np.zeros(len(words), np.uint8), int(doc_group.max()) + 1, vocab)
+
+
+def test_single_token_closed_form():
+    say("single-token corpus")
+    cp = corpus_from_docs([(0, [3])], vocab=7)
+    wl = W(K=4)
+    s, m = parity.make_pair(cp, wl)
+    w, u, zr = s.conditionals(0, 1, 0, 1)
+    np.testing.assert_allclose(w[0, 0::2], wl.alpha / 7, rtol=1e-6)
+    assert np.all(w[0, 1::2] == 0)
+    assert zr[0] & 1 == 1
+    for sw in range(4):
+        parity.one_step(s, m, sw, 3)
+    s.close()
+
+
+def test_empty_and_ragged_documents():
+    say("empty and ragged documents")
+    rng = np.random.default_rng(1)
+    docs = []
+    for d in range(300):
+        L = [0, 1, 2, 63, 64, 65, 127, 128, 129, 200][d % 10] if d % 3 else int(rng.integers(0, 40))
+        docs.append((d % 3, list(rng.integers(0, 50, size=L))))
+    cp = corpus_from_docs(docs, vocab=50)
+    wl = W(K=13)
+    s, m = parity.make_pair(cp, wl)
+    for sw in range(5):
+        rep, ch, rp = parity.one_step(s, m, sw, 11)
+        say(f"  {rep}")
+    s.close()
+
+
+@pytest.mark.parametrize("K", [1, 2, 63, 64, 65, 128, 129, 256, 257, 500, 512, 513, 768, 769, 1024])
+def test_topic_count_boundaries(K):
+    say(f"K = {K}")
+    rng = np.random.default_rng(K)
+    docs = [(d % 2, list(rng.zipf(1.3, size=int(rng.integers(1, 120))) % 300)) for d in range(120)]
+    cp = corpus_from_docs(docs, vocab=300)
+    wl = W(K=K, alpha=0.2, a=0.6, b=5.0, gamma=0.05)
+    s, m = parity.make_pair(cp, wl)
+    for sw in range(3):
+        rep, ch, rp = parity.one_step(s, m, sw, 5 + K)
+    ll_o = m.loglik(*s.assignments(), m.rebuild(*s.assignments()))
+    assert abs(s.loglik() - ll_o) <= 1e-6 * abs(ll_o)
+    s.close()
+
+
+def test_discount_zero_and_large_concentration():
+    say("a = 0 (Dirichlet process restaurants)")
+    cp = synth.generate(synth.workload(0), 3)
+    wl = W(K=10, alpha=0.3, a=0.0, b=200.0, gamma=0.5)
+    s, m = parity.make_pair(cp, wl)
+    for sw in range(3):
+        parity.one_step(s, m, sw, 8)
+    s.close()
+
+
+def test_invalid_arguments():
+    from paper_1510_06549_amd import spdp as sp
+
+    say("invalid arguments")
+    words = np.array([0, 1, 2], np.int32)
+    off = np.array([0, 3], np.int64)
+    grp = np.array([0], np.int32)
+    bad = [
+        dict(K=0), dict(K=2000), dict(alpha=0.0), dict(a=1.0), dict(b=0.0), dict(gamma=-1.0),
+    ]
+    for kw in bad:
+        args = dict(K=4, alpha=0.1, a=0.5, b=1.0, gamma=0.1)
+        args.update(kw)
+        with pytest.raises(sp.SpdpError) as e:
+            sp.spdp_create(words, off, grp, 1, 3, args["K"], args["alpha"], args["a"], args["b"],
+                           args["gamma"])
+        assert e.value.code == sp.SPDP_E_ARG
+    with pytest.raises(sp.SpdpError):  # word id out of range
+        sp.spdp_create(np.array([0, 5], np.int32), np.array([0, 2], np.int64), grp, 1, 3, 4, 0.1,
+                       0.5, 1.0, 0.1)
+    with pytest.raises(sp.SpdpError):  # group out of range
+        sp.spdp_create(words, off, np.array([1], np.int32), 1, 3, 4, 0.1, 0.5, 1.0, 0.1)
