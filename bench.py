@@ -1,0 +1,207 @@
+#!/usr/bin/env python3
+"""Throughput of the SPDP Gibbs sweep on one MI355X.
+
+One step = one full sweep of the hot path (sampling kernel, count update,
+repair, totals) over every token of a synthetic SPDP corpus resident in HBM.
+Prints ONE JSON line: tokens resampled per second, the HBM roofline fraction
+of the sampling kernel (algorithmic bytes per launch over its HIP-event
+duration) and the fp64 oracle timed on the host cores over a bounded sample
+of documents.
+
+Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME|IDX]
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "tokens resampled/sec per Gibbs sweep (1 GPU) + % of HBM roofline"
+HBM_PEAK_GBS = 8000.0  # MI355X datasheet HBM3E bandwidth
+DEFAULT_WORKLOAD = "g20-d50000-k500"
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def algorithmic_sample_bytes(n_tokens: int, K: int) -> int:
+    """Bytes the sampling step must move: per token the three K-entry int32
+    rows n[g][w][.], t[g][w][.], B[w][.] and the token stream (row index and
+    state in, state out)."""
+    return n_tokens * (12 * K + 12)
+
+
+def cpu_baseline(cp, wl, z, r, target_s: float):
+    import numpy as np
+
+    import oracle
+
+    t0 = time.time()
+    m = oracle.Model(cp.words, cp.doc_off, cp.doc_group, cp.n_groups, wl.K, wl.vocab, wl.alpha,
+                     wl.a, wl.b, wl.gamma)
+    c = m.rebuild(z, r)
+    log(f"[bench] oracle model + dense counts ready in {time.time() - t0:.1f}s")
+    threads = oracle.num_threads()
+    # calibrate on a few documents, then size the sample to about target_s
+    zs, rs = z.copy(), r.copy()
+    d_cal = min(64, m.D)
+    t0 = time.perf_counter()
+    m.sample_docs(c, zs, rs, 0, 1, 0, d_cal)
+    dt = max(time.perf_counter() - t0, 1e-6)
+    tok_cal = int(m.doc_off[d_cal])
+    per_tok = dt / max(tok_cal, 1)
+    want_tok = int(target_s / per_tok)
+    d_s = int(np.searchsorted(m.doc_off, want_tok))
+    d_s = max(d_cal, min(d_s, m.D))
+    zs, rs = z.copy(), r.copy()
+    t0 = time.perf_counter()
+    m.sample_docs(c, zs, rs, 0, 1, 0, d_s)
+    dt = time.perf_counter() - t0
+    toks = int(m.doc_off[d_s])
+    return {
+        "value": toks / dt,
+        "unit": "tokens/s",
+        "cores": threads,
+        "kind": "oracle",
+        "sample": (f"sampling step of the first {d_s} documents ({toks} tokens) against the full "
+                   f"sweep-start counts, fp64, OpenMP over documents, {dt:.1f}s; count rebuild "
+                   f"excluded"),
+    }
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=5)
+    ap.add_argument("--warmup", type=int, default=1)
+    ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
+    ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--copy-probe-mib", type=int, default=0,
+                    help="also run a plain device copy of this size (counter calibration)")
+    args = ap.parse_args()
+
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU: the multi-GPU (group-sharded) sweep is not built; "
+              "run with --gpus 1", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    import synth
+    from paper_1510_06549_amd import spdp as sp
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    torch.cuda.set_device(0)
+    wl = synth.workload(int(args.workload) if args.workload.isdigit() else args.workload)
+
+    t0 = time.time()
+    cp = synth.generate(wl, args.seed)
+    log(f"[bench] workload {wl.name}: {cp.n_tokens} tokens, {cp.n_docs} docs, generated in "
+        f"{time.time() - t0:.1f}s")
+
+    stream = torch.cuda.current_stream()
+    t0 = time.time()
+    s = sp.Sampler(cp.words, cp.doc_off, cp.doc_group, cp.n_groups, wl.vocab, wl.K, wl.alpha,
+                   wl.a, wl.b, wl.gamma, init_seed=args.seed, hip_stream=stream.cuda_stream)
+    torch.cuda.synchronize()
+    info = s.info
+    log(f"[bench] state created in {time.time() - t0:.1f}s: {info}")
+
+    if args.copy_probe_mib > 0:
+        nbytes = args.copy_probe_mib << 20
+        src = torch.ones(nbytes // 4, dtype=torch.int32, device="cuda")
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        log(f"[bench] copy probe: {nbytes} bytes read + {nbytes} bytes written")
+        del src, dst
+
+    seed = 1000 + args.seed
+    for w in range(args.warmup):
+        s.sweep(w, seed)
+    torch.cuda.synchronize()
+    log(f"[bench] {args.warmup} warm-up sweep(s) done")
+
+    sp.spdp_kernel_timing(s.h, True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for k in range(args.steps):
+        s.sweep(args.warmup + k, seed)
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    kt = sp.spdp_kernel_times(s.h)
+    sp.spdp_kernel_timing(s.h, False)
+    changed, repaired = s.stats()
+    log(f"[bench] {args.steps} timed sweeps in {elapsed:.3f}s; kernel ms {kt}; "
+        f"last sweep changed={changed} repaired={repaired}")
+
+    N = cp.n_tokens
+    ms_step = 1000.0 * elapsed / args.steps
+    value = N * args.steps / elapsed
+    ms_sample, n_sample = kt["sample"]
+    avg_sample_s = ms_sample / 1000.0 / max(n_sample, 1)
+    alg = algorithmic_sample_bytes(N, wl.K)
+    achieved = alg / avg_sample_s / 1e9
+    roofline = {
+        "bound": "hbm",
+        "kernel": "k_sample",
+        "achieved": round(achieved, 1),
+        "peak": HBM_PEAK_GBS,
+        "unit": "GB/s",
+        "frac": round(achieved / HBM_PEAK_GBS, 4),
+        "traffic": None,
+        "bytes_per_token": 12 * wl.K + 12,
+        "avg_launch_ms": round(avg_sample_s * 1000.0, 3),
+    }
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        z, r = s.assignments()
+        s.close()
+        cpu = cpu_baseline(cp, wl, z, r, args.cpu_seconds)
+        log(f"[bench] cpu baseline {cpu}")
+    else:
+        s.close()
+
+    out = {
+        "metric": METRIC,
+        "value": round(value, 1),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 3),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {
+            "workload": wl.name,
+            "groups": wl.n_groups,
+            "docs": cp.n_docs,
+            "tokens": N,
+            "vocab": wl.vocab,
+            "topics": wl.K,
+            "alpha": wl.alpha, "a": wl.a, "b": wl.b, "gamma": wl.gamma,
+        },
+        "kernels_ms_per_step": {k: round(v[0] / args.steps, 3) for k, v in kt.items()},
+        "roofline": roofline,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

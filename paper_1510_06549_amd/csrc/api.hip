@@ -123,7 +123,7 @@ int rebuild_state(spdp_state *s)
     // every row is a repair candidate
     HIP_TRY(launch_fill_u32(b.flags, ((int64_t)m.G * m.V + 31) / 32, 0xFFFFFFFFu, s->st));
     HIP_TRY(launch_fill_u64(b.ctr, 4, 0ull, s->st));
-    HIP_TRY(launch_fill_u64(b.ctr + 2, 1, 1ull, s->st));
+    HIP_TRY(launch_fill_u32(b.moved_part, (m.N + 255) / 256, 0u, s->st));
     HIP_TRY(launch_repair(m, b, zr, s->st));
     HIP_TRY(launch_totals(m, b, zr, s->st));
     return SPDP_OK;
@@ -285,6 +285,7 @@ int spdp_create(const spdp_corpus *corpus, const spdp_groups *groups, int32_t K,
     TRY(dev_alloc(s, &B.f0, (int64_t)G * m.Kp, "f0"));
     TRY(dev_alloc(s, &B.f1, (int64_t)G * m.Kp, "f1"));
     TRY(dev_alloc(s, &B.flags, (rows + 31) / 32, "repair flags"));
+    TRY(dev_alloc(s, &B.moved_part, (N + 255) / 256, "moved-token partial counts"));
     B.partial_len = loglik_partials_needed();
     TRY(dev_alloc(s, &B.partial, B.partial_len, "loglik partials"));
     s->cur = 0;
@@ -489,6 +490,7 @@ int spdp_stats(const spdp_state *s, int64_t *changed, int64_t *repaired)
     if (!s) return fail(SPDP_E_ARG, "state is NULL");
     HIP_TRY(hipSetDevice(s->device));
     unsigned long long c[4];
+    HIP_TRY(launch_moved_sum(s->m, s->b, s->st));
     HIP_TRY(hipMemcpyAsync(c, s->b.ctr, sizeof c, hipMemcpyDeviceToHost, s->st));
     int rc = sync(s);
     if (rc != SPDP_OK) return rc;

@@ -101,7 +101,8 @@ struct DeviceBuffers {
     double *logS = nullptr;       // [tri(ncap + 1)] log S^n_{t,a}
     double *lfact = nullptr;      // [ncap + 1] log n!
     uint32_t *flags = nullptr;    // [ceil(G V / 32)] rows whose t hit zero
-    unsigned long long *ctr = nullptr; // [4] changed, repaired, flagged rows, spare
+    unsigned long long *ctr = nullptr; // [4] changed (on demand), repaired
+    uint32_t *moved_part = nullptr;    // [ceil(N / 256)] per-block moved-token counts
     double *partial = nullptr;    // loglik block partials
     int64_t partial_len = 0;
     int32_t *err = nullptr;       // [2] device error flags
@@ -133,6 +134,7 @@ hipError_t launch_rebuild(const Model &m, const DeviceBuffers &b, const int32_t 
 hipError_t launch_update(const Model &m, const DeviceBuffers &b, const int32_t *zr_old,
                          const int32_t *zr_new, hipStream_t st);
 hipError_t launch_repair(const Model &m, const DeviceBuffers &b, int32_t *zr, hipStream_t st);
+hipError_t launch_moved_sum(const Model &m, const DeviceBuffers &b, hipStream_t st);
 hipError_t launch_totals(const Model &m, const DeviceBuffers &b, const int32_t *zr,
                          hipStream_t st);
 hipError_t launch_factors(const Model &m, const DeviceBuffers &b, hipStream_t st);
