@@ -81,6 +81,9 @@ void free_state(spdp_state *s)
     if (s->st) hipStreamSynchronize(s->st);
     else hipDeviceSynchronize();
     for (void *p : s->allocs) hipFree(p);
+    if (s->b.zr_dbg) hipFree(s->b.zr_dbg);
+    if (s->b.tr_w) hipFree(s->b.tr_w);
+    if (s->b.tr_u) hipFree(s->b.tr_u);
     for (auto &v : s->events)
         for (auto &ev : v) {
             hipEventDestroy(ev.a);
@@ -113,19 +116,20 @@ int timed(spdp_state *s, int cls, F launch)
     return SPDP_OK;
 }
 
-// Counts, repair of every cell and totals for the packed state in zr[cur].
+// Counts (with the repair of every cell left without a table), shadow base
+// and totals for the packed state in zr[cur]; the other state buffer gets a
+// copy so that the statistics of a fresh state read zero.
 int rebuild_state(spdp_state *s)
 {
     const Model &m = s->m;
     DeviceBuffers &b = s->b;
     int32_t *zr = b.zr[s->cur];
-    HIP_TRY(launch_rebuild(m, b, zr, s->st));
-    // every row is a repair candidate
-    HIP_TRY(launch_fill_u32(b.flags, ((int64_t)m.G * m.V + 31) / 32, 0xFFFFFFFFu, s->st));
-    HIP_TRY(launch_fill_u64(b.ctr, 4, 0ull, s->st));
-    HIP_TRY(launch_fill_u32(b.moved_part, (m.N + 255) / 256, 0u, s->st));
-    HIP_TRY(launch_repair(m, b, zr, s->st));
+    HIP_TRY(launch_rows(m, b, zr, s->st));
+    HIP_TRY(launch_base(m, b, s->st));
     HIP_TRY(launch_totals(m, b, zr, s->st));
+    if (m.N > 0)
+        HIP_TRY(hipMemcpyAsync(b.zr[1 - s->cur], zr, (size_t)m.N * sizeof(int32_t),
+                               hipMemcpyDeviceToDevice, s->st));
     return SPDP_OK;
 }
 
@@ -229,7 +233,7 @@ int spdp_create(const spdp_corpus *corpus, const spdp_groups *groups, int32_t K,
             TRY(fail(SPDP_E_NOMEM, "staging buffer for words"));
         }
         words_d = (int32_t *)tmp;
-        if (hipMalloc(&tmp, (size_t)rows * sizeof(int32_t)) != hipSuccess) {
+        if (hipMalloc(&tmp, (size_t)(rows + 1) * sizeof(int32_t)) != hipSuccess) {
             (void)hipGetLastError();
             hipFree(words_d);
             TRY(fail(SPDP_E_NOMEM, "staging buffer for word counts"));
@@ -250,18 +254,33 @@ int spdp_create(const spdp_corpus *corpus, const spdp_groups *groups, int32_t K,
     if (e == hipSuccess)
         e = hipMemcpyAsync(B.doc_group, groups->doc_group, (size_t)D * sizeof(int32_t),
                            hipMemcpyHostToDevice, s->st);
-    if (e == hipSuccess) e = launch_fill_i32(gw_count, rows, 0, s->st);
+    if (e == hipSuccess) e = launch_fill_i32(gw_count, rows + 1, 0, s->st);
     if (e == hipSuccess) e = launch_make_gw(m, words_d, B.doc_off, B.doc_group, B.gw, gw_count, B.err, s->st);
     if (e == hipSuccess) e = launch_max_i32(gw_count, rows, B.err + 1, s->st);
     int32_t herr[2] = {0, 0};
     if (e == hipSuccess) e = hipMemcpyAsync(herr, B.err, sizeof herr, hipMemcpyDeviceToHost, s->st);
     if (e == hipSuccess) e = hipStreamSynchronize(s->st);
-    cleanup_staging();
+    if (e != hipSuccess) cleanup_staging();
     TRY_HIP(e);
+    if ((herr[0] & 3) || herr[1] > kCountMax) cleanup_staging();
     if (herr[0] & 1) TRY(fail(SPDP_E_ARG, "doc_group out of [0, n_groups)"));
     if (herr[0] & 2) TRY(fail(SPDP_E_ARG, "word id out of [0, vocab)"));
+    if (herr[1] > kCountMax)
+        TRY(fail(SPDP_E_RANGE, "a (group, word) pair occurs %d times; packed counts hold %d",
+                 herr[1], kCountMax));
     m.ncap = herr[1] < 1 ? 1 : herr[1];
     TRY_HIP(launch_fill_i32(B.err, 2, 0, s->st));
+
+    // tokens grouped by count row (the count rebuild walks rows)
+    {
+        int rc2 = dev_alloc(s, &B.perm, N, "row-sorted tokens");
+        if (rc2 == SPDP_OK) rc2 = dev_alloc(s, &B.row_off, rows + 1, "row offsets");
+        if (rc2 != SPDP_OK) cleanup_staging();
+        TRY(rc2);
+        e = build_row_index(m, B, gw_count, s->st);
+        cleanup_staging();
+        TRY_HIP(e);
+    }
 
     // Stirling cache
     const int64_t n_logS = tri_index(m.ncap + 1, 0);  // rows 0..ncap
@@ -276,16 +295,16 @@ int spdp_create(const spdp_corpus *corpus, const spdp_groups *groups, int32_t K,
     // state and counts
     TRY(dev_alloc(s, &B.zr[0], N, "zr"));
     TRY(dev_alloc(s, &B.zr[1], N, "zr"));
-    TRY(dev_alloc(s, &B.n, rows * m.Kp, "customer counts"));
-    TRY(dev_alloc(s, &B.t, rows * m.Kp, "table counts"));
+    TRY(dev_alloc(s, &B.nt, rows * m.Kp, "packed customer/table counts"));
     TRY(dev_alloc(s, &B.B, (int64_t)V * m.Kp, "shadow-base table counts"));
+    TRY_HIP(launch_fill_i32(B.nt, rows * m.Kp, 0, s->st));
     TRY(dev_alloc(s, &B.Ngk, (int64_t)G * m.Kp, "N_gk"));
     TRY(dev_alloc(s, &B.Tgk, (int64_t)G * m.Kp, "T_gk"));
     TRY(dev_alloc(s, &B.Bk, m.Kp, "B_k"));
     TRY(dev_alloc(s, &B.f0, (int64_t)G * m.Kp, "f0"));
     TRY(dev_alloc(s, &B.f1, (int64_t)G * m.Kp, "f1"));
-    TRY(dev_alloc(s, &B.flags, (rows + 31) / 32, "repair flags"));
-    TRY(dev_alloc(s, &B.moved_part, (N + 255) / 256, "moved-token partial counts"));
+    TRY(dev_alloc(s, &B.rep_part, rows, "repair partial counts"));
+    TRY(dev_alloc(s, &B.part, stat_partials_needed(), "reduction partials"));
     B.partial_len = loglik_partials_needed();
     TRY(dev_alloc(s, &B.partial, B.partial_len, "loglik partials"));
     s->cur = 0;
@@ -313,9 +332,8 @@ int spdp_sweep(spdp_state *s, uint32_t sweep, uint64_t seed)
              return launch_sample(m, b, zr_old, zr_new, sweep, seed, nullptr, nullptr, 0, 0, s->st);
          })) != SPDP_OK)
         return rc;
-    if ((rc = timed(s, 1, [&] { return launch_update(m, b, zr_old, zr_new, s->st); })) != SPDP_OK)
-        return rc;
-    if ((rc = timed(s, 2, [&] { return launch_repair(m, b, zr_new, s->st); })) != SPDP_OK) return rc;
+    if ((rc = timed(s, 1, [&] { return launch_rows(m, b, zr_new, s->st); })) != SPDP_OK) return rc;
+    if ((rc = timed(s, 2, [&] { return launch_base(m, b, s->st); })) != SPDP_OK) return rc;
     if ((rc = timed(s, 3, [&] { return launch_totals(m, b, zr_new, s->st); })) != SPDP_OK) return rc;
     s->cur = 1 - s->cur;
     return SPDP_OK;
@@ -329,17 +347,36 @@ int spdp_counts(const spdp_state *s, int32_t g_begin, int32_t g_end, int32_t *n_
     if (g_begin < 0 || g_end > m.G || g_begin > g_end) return fail(SPDP_E_ARG, "bad group range");
     if (where != 0 && where != 1) return fail(SPDP_E_ARG, "where must be 0 or 1");
     HIP_TRY(hipSetDevice(s->device));
-    const hipMemcpyKind kind = where ? hipMemcpyDeviceToDevice : hipMemcpyDeviceToHost;
-    const size_t rows = (size_t)(g_end - g_begin) * m.V;
-    const size_t off = (size_t)g_begin * m.V * m.Kp;
-    if (rows > 0) {
-        if (n_gwk)
-            HIP_TRY(hipMemcpy2DAsync(n_gwk, (size_t)m.K * 4, s->b.n + off, (size_t)m.Kp * 4,
-                                     (size_t)m.K * 4, rows, kind, s->st));
-        if (t_gwk)
-            HIP_TRY(hipMemcpy2DAsync(t_gwk, (size_t)m.K * 4, s->b.t + off, (size_t)m.Kp * 4,
-                                     (size_t)m.K * 4, rows, kind, s->st));
+    if (!n_gwk && !t_gwk) return SPDP_OK;
+    const int64_t cells = (int64_t)m.V * m.K;
+    int32_t *stage_n = nullptr, *stage_t = nullptr;
+    if (where == 0) {
+        // one group at a time through device staging buffers
+        HIP_TRY(hipMalloc(&stage_n, (size_t)cells * 4));
+        hipError_t e = hipMalloc(&stage_t, (size_t)cells * 4);
+        if (e != hipSuccess) {
+            hipFree(stage_n);
+            HIP_TRY(e);
+        }
     }
+    hipError_t e = hipSuccess;
+    for (int32_t g = g_begin; g < g_end && e == hipSuccess; ++g) {
+        const int64_t off = (int64_t)(g - g_begin) * cells;
+        if (where == 1) {
+            e = launch_unpack_counts(m, s->b, g, n_gwk ? n_gwk + off : nullptr,
+                                     t_gwk ? t_gwk + off : nullptr, s->st);
+        } else {
+            e = launch_unpack_counts(m, s->b, g, stage_n, stage_t, s->st);
+            if (e == hipSuccess && n_gwk)
+                e = hipMemcpyAsync(n_gwk + off, stage_n, (size_t)cells * 4, hipMemcpyDeviceToHost, s->st);
+            if (e == hipSuccess && t_gwk)
+                e = hipMemcpyAsync(t_gwk + off, stage_t, (size_t)cells * 4, hipMemcpyDeviceToHost, s->st);
+            if (e == hipSuccess) e = hipStreamSynchronize(s->st);
+        }
+    }
+    if (stage_n) hipFree(stage_n);
+    if (stage_t) hipFree(stage_t);
+    HIP_TRY(e);
     return sync(s);
 }
 
@@ -472,9 +509,17 @@ int spdp_debug_conditionals(spdp_state *s, uint32_t sweep, uint64_t seed, int64_
         b.tr_u = (float *)p;
         b.tr_cap = T;
     }
+    if (!b.zr_dbg) {
+        void *p = nullptr;
+        if (hipMalloc(&p, (size_t)m.N * sizeof(int32_t)) != hipSuccess) {
+            (void)hipGetLastError();
+            return fail(SPDP_E_NOMEM, "debug state buffer");
+        }
+        b.zr_dbg = (int32_t *)p;
+    }
     HIP_TRY(launch_fill_i32((int32_t *)b.tr_w, T * 2 * m.K, 0, s->st));
     HIP_TRY(launch_fill_i32((int32_t *)b.tr_u, T, 0, s->st));
-    int32_t *zr_old = b.zr[s->cur], *zr_tmp = b.zr[1 - s->cur];
+    int32_t *zr_old = b.zr[s->cur], *zr_tmp = b.zr_dbg;
     HIP_TRY(launch_factors(m, b, s->st));
     HIP_TRY(launch_sample(m, b, zr_old, zr_tmp, sweep, seed, b.tr_w, b.tr_u, tok_begin, tok_end,
                           s->st));
@@ -490,7 +535,7 @@ int spdp_stats(const spdp_state *s, int64_t *changed, int64_t *repaired)
     if (!s) return fail(SPDP_E_ARG, "state is NULL");
     HIP_TRY(hipSetDevice(s->device));
     unsigned long long c[4];
-    HIP_TRY(launch_moved_sum(s->m, s->b, s->st));
+    HIP_TRY(launch_stat_sums(s->m, s->b, s->b.zr[s->cur], s->b.zr[1 - s->cur], s->st));
     HIP_TRY(hipMemcpyAsync(c, s->b.ctr, sizeof c, hipMemcpyDeviceToHost, s->st));
     int rc = sync(s);
     if (rc != SPDP_OK) return rc;

@@ -1,0 +1,263 @@
+// counts.hip -- exact count maintenance (gfx950).
+//
+// The customer and table counts of the thesis's collapsed joint are pure
+// functions of the per-token state (z, r).  They are held packed, one int32
+// per cell: n in the low 16 bits, t in the high 16 bits (every count is
+// bounded by the largest per-(group, word) token count, checked < 2^16 at
+// creation).
+//
+//   row index   tokens sorted by count row q = g V + w (stable, so each row's
+//               token list is in increasing token index), built once
+//   k_rows      per row: LDS histogram of its tokens' (z, r) -> the row's
+//               packed cells; then every cell left with customers but no
+//               table promotes the smallest-index token of that cell to table
+//               head (the repair of the parallel pass), and the row is written
+//   k_base      shadow-base table counts B[w][k] = sum_g t[g][w][k]
+//   k_unpack    export of n and t as separate int32 arrays
+#include <hipcub/hipcub.hpp>
+
+#include <climits>
+
+#include "spdp_internal.hpp"
+
+namespace spdp {
+
+namespace {
+
+constexpr int kBlock = 256;
+
+inline int64_t blocks_for(int64_t n, int per_block)
+{
+    int64_t b = (n + per_block - 1) / per_block;
+    return b < 1 ? 1 : b;
+}
+
+__global__ void k_iota(int32_t *__restrict__ x, int64_t n)
+{
+    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i < n) x[i] = (int32_t)i;
+}
+
+// One 64-lane block per count row.
+__global__ void __launch_bounds__(64) k_rows(int32_t Kp, const int32_t *__restrict__ row_off,
+                                             const int32_t *__restrict__ perm,
+                                             int32_t *__restrict__ zr, int32_t *__restrict__ nt,
+                                             uint32_t *__restrict__ rep_part)
+{
+    __shared__ int32_t h[SPDP_MAX_K];
+    __shared__ int32_t first[SPDP_MAX_K];
+    const int64_t q = blockIdx.x;
+    const int32_t lane = threadIdx.x;
+    const int32_t rs = row_off[q], re = row_off[q + 1];
+    uint32_t rep = 0;
+    if (rs < re) {
+        for (int32_t k = lane; k < Kp; k += 64) h[k] = 0;
+        __syncthreads();
+        for (int32_t j = rs + lane; j < re; j += 64) {
+            const int32_t v = zr[perm[j]];
+            atomicAdd(&h[v >> 1], 1 + ((v & 1) << 16));
+        }
+        __syncthreads();
+        int broken = 0;
+        for (int32_t k = lane; k < Kp; k += 64) {
+            const int32_t x = h[k];
+            const bool br = (x != 0) && ((x >> 16) == 0);
+            first[k] = br ? INT_MAX : -1;
+            broken |= br;
+        }
+        if (__syncthreads_or(broken)) {
+            // a cell without a table holds only r = 0 tokens; its first one
+            // in token order (= first in the row list) becomes the head
+            for (int32_t j = rs + lane; j < re; j += 64) {
+                const int32_t k = zr[perm[j]] >> 1;
+                if (first[k] >= 0) atomicMin(&first[k], j);
+            }
+            __syncthreads();
+            for (int32_t k = lane; k < Kp; k += 64) {
+                const int32_t j = first[k];
+                if (j >= 0 && j != INT_MAX) {
+                    const int32_t tok = perm[j];
+                    zr[tok] = zr[tok] | 1;
+                    h[k] += 1 << 16;
+                    ++rep;
+                }
+            }
+            __syncthreads();
+        }
+        int32_t *__restrict__ row = nt + q * Kp;
+        for (int32_t k = lane; k < Kp; k += 64) row[k] = h[k];
+    }
+    for (int o = 32; o > 0; o >>= 1) rep += __shfl_xor(rep, o);
+    if (lane == 0) rep_part[q] = rep;
+}
+
+// B[w][k] = sum_g t[g][w][k]
+__global__ void k_base(int32_t G, int32_t V, int32_t Kp, const int32_t *__restrict__ nt,
+                       int32_t *__restrict__ B)
+{
+    const int64_t j = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    const int64_t cells = (int64_t)V * Kp;
+    if (j >= cells) return;
+    int32_t s = 0;
+    for (int32_t g = 0; g < G; ++g) s += nt[(int64_t)g * cells + j] >> 16;
+    B[j] = s;
+}
+
+__global__ void k_unpack(int32_t V, int32_t K, int32_t Kp, const int32_t *__restrict__ nt_g,
+                         int32_t *__restrict__ n_out, int32_t *__restrict__ t_out)
+{
+    const int64_t j = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (j >= (int64_t)V * K) return;
+    const int64_t w = j / K, k = j % K;
+    const int32_t x = nt_g[w * Kp + k];
+    if (n_out) n_out[j] = x & 0xFFFF;
+    if (t_out) t_out[j] = x >> 16;
+}
+
+// Sum of x[0..n) into *out (fixed-order two-level reduction).
+__global__ void __launch_bounds__(kBlock) k_sum_u32(const uint32_t *__restrict__ x, int64_t n,
+                                                    unsigned long long *__restrict__ part)
+{
+    unsigned long long s = 0;
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride) s += x[i];
+    for (int o = 32; o > 0; o >>= 1) s += __shfl_xor(s, o);
+    __shared__ unsigned long long p[kBlock / 64];
+    if ((threadIdx.x & 63) == 0) p[threadIdx.x >> 6] = s;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        unsigned long long t = 0;
+        for (int j = 0; j < kBlock / 64; ++j) t += p[j];
+        part[blockIdx.x] = t;
+    }
+}
+
+__global__ void __launch_bounds__(kBlock) k_count_diff(const int32_t *__restrict__ a,
+                                                       const int32_t *__restrict__ b, int64_t n,
+                                                       unsigned long long *__restrict__ part)
+{
+    unsigned long long s = 0;
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride)
+        s += (a[i] != b[i]) ? 1ull : 0ull;
+    for (int o = 32; o > 0; o >>= 1) s += __shfl_xor(s, o);
+    __shared__ unsigned long long p[kBlock / 64];
+    if ((threadIdx.x & 63) == 0) p[threadIdx.x >> 6] = s;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        unsigned long long t = 0;
+        for (int j = 0; j < kBlock / 64; ++j) t += p[j];
+        part[blockIdx.x] = t;
+    }
+}
+
+__global__ void __launch_bounds__(kBlock) k_sum_u64(const unsigned long long *__restrict__ part,
+                                                    int n, unsigned long long *__restrict__ out)
+{
+    __shared__ unsigned long long p[kBlock];
+    unsigned long long s = 0;
+    for (int i = threadIdx.x; i < n; i += blockDim.x) s += part[i];
+    p[threadIdx.x] = s;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        unsigned long long t = 0;
+        for (int j = 0; j < kBlock; ++j) t += p[j];
+        *out = t;
+    }
+}
+
+constexpr int kReduceBlocks = 1024;
+
+}  // namespace
+
+hipError_t build_row_index(const Model &m, DeviceBuffers &b, const int32_t *gw_count,
+                           hipStream_t st)
+{
+    const int64_t rows = (int64_t)m.G * m.V;
+    hipError_t e;
+    // row offsets: exclusive sum of the per-row token counts (rows + 1 entries,
+    // the last count being zero)
+    size_t scan_bytes = 0;
+    e = hipcub::DeviceScan::ExclusiveSum(nullptr, scan_bytes, gw_count, b.row_off, rows + 1, st);
+    if (e != hipSuccess) return e;
+    // stable radix sort of (row, token) pairs
+    int end_bit = 1;
+    while ((1ll << end_bit) < rows) ++end_bit;
+    int32_t *keys_out = nullptr, *vals_in = nullptr;
+    size_t sort_bytes = 0;
+    e = hipcub::DeviceRadixSort::SortPairs(nullptr, sort_bytes, b.gw, keys_out, vals_in, b.perm,
+                                           (int)m.N, 0, end_bit, st);
+    if (e != hipSuccess) return e;
+    void *temp = nullptr;
+    const size_t temp_bytes = scan_bytes > sort_bytes ? scan_bytes : sort_bytes;
+    if ((e = hipMalloc(&temp, temp_bytes > 0 ? temp_bytes : 1)) != hipSuccess) return e;
+    if ((e = hipMalloc(&keys_out, (size_t)(m.N > 0 ? m.N : 1) * 4)) != hipSuccess) {
+        hipFree(temp);
+        return e;
+    }
+    if ((e = hipMalloc(&vals_in, (size_t)(m.N > 0 ? m.N : 1) * 4)) != hipSuccess) {
+        hipFree(temp);
+        hipFree(keys_out);
+        return e;
+    }
+    size_t tb = temp_bytes;
+    e = hipcub::DeviceScan::ExclusiveSum(temp, tb, gw_count, b.row_off, rows + 1, st);
+    if (e == hipSuccess && m.N > 0) {
+        hipLaunchKernelGGL(k_iota, dim3((unsigned)blocks_for(m.N, kBlock)), dim3(kBlock), 0, st,
+                           vals_in, m.N);
+        e = hipGetLastError();
+        if (e == hipSuccess) {
+            tb = temp_bytes;
+            e = hipcub::DeviceRadixSort::SortPairs(temp, tb, b.gw, keys_out, vals_in, b.perm,
+                                                   (int)m.N, 0, end_bit, st);
+        }
+    }
+    hipError_t e2 = hipStreamSynchronize(st);
+    hipFree(temp);
+    hipFree(keys_out);
+    hipFree(vals_in);
+    return e != hipSuccess ? e : e2;
+}
+
+hipError_t launch_rows(const Model &m, const DeviceBuffers &b, int32_t *zr, hipStream_t st)
+{
+    const int64_t rows = (int64_t)m.G * m.V;
+    hipLaunchKernelGGL(k_rows, dim3((unsigned)rows), dim3(64), 0, st, m.Kp, b.row_off, b.perm, zr,
+                       b.nt, b.rep_part);
+    return hipGetLastError();
+}
+
+hipError_t launch_base(const Model &m, const DeviceBuffers &b, hipStream_t st)
+{
+    const int64_t cells = (int64_t)m.V * m.Kp;
+    hipLaunchKernelGGL(k_base, dim3((unsigned)blocks_for(cells, kBlock)), dim3(kBlock), 0, st, m.G,
+                       m.V, m.Kp, b.nt, b.B);
+    return hipGetLastError();
+}
+
+hipError_t launch_unpack_counts(const Model &m, const DeviceBuffers &b, int32_t g,
+                                int32_t *n_out, int32_t *t_out, hipStream_t st)
+{
+    const int64_t cells = (int64_t)m.V * m.K;
+    hipLaunchKernelGGL(k_unpack, dim3((unsigned)blocks_for(cells, kBlock)), dim3(kBlock), 0, st,
+                       m.V, m.K, m.Kp, b.nt + (int64_t)g * m.V * m.Kp, n_out, t_out);
+    return hipGetLastError();
+}
+
+hipError_t launch_stat_sums(const Model &m, const DeviceBuffers &b, const int32_t *zr_now,
+                            const int32_t *zr_before, hipStream_t st)
+{
+    // ctr[0] = tokens whose state differs, ctr[1] = heads promoted by repair
+    const int64_t rows = (int64_t)m.G * m.V;
+    hipLaunchKernelGGL(k_count_diff, dim3(kReduceBlocks), dim3(kBlock), 0, st, zr_now, zr_before,
+                       m.N, b.part);
+    hipLaunchKernelGGL(k_sum_u64, dim3(1), dim3(kBlock), 0, st, b.part, kReduceBlocks, b.ctr);
+    hipLaunchKernelGGL(k_sum_u32, dim3(kReduceBlocks), dim3(kBlock), 0, st, b.rep_part, rows,
+                       b.part);
+    hipLaunchKernelGGL(k_sum_u64, dim3(1), dim3(kBlock), 0, st, b.part, kReduceBlocks, b.ctr + 1);
+    return hipGetLastError();
+}
+
+int64_t stat_partials_needed() { return kReduceBlocks; }
+
+}  // namespace spdp

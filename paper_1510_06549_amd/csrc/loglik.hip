@@ -37,8 +37,7 @@ __device__ double block_sum(double v)
 }
 
 __global__ void __launch_bounds__(kLBlock) k_ll_cells(int64_t ncell, int32_t ncap,
-                                                      const int32_t *__restrict__ n,
-                                                      const int32_t *__restrict__ t,
+                                                      const int32_t *__restrict__ nt,
                                                       const double *__restrict__ logS,
                                                       const double *__restrict__ lfact,
                                                       double *__restrict__ partial,
@@ -48,7 +47,8 @@ __global__ void __launch_bounds__(kLBlock) k_ll_cells(int64_t ncell, int32_t nca
     bool bad = false;
     const int64_t stride = (int64_t)gridDim.x * blockDim.x;
     for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < ncell; i += stride) {
-        const int32_t nn = n[i], tt = t[i];
+        const int32_t x = nt[i];
+        const int32_t nn = x & kCountMax, tt = x >> kCountBits;
         if (nn == 0 && tt == 0) continue;
         if (tt <= 0 || tt > nn || nn > ncap) {
             bad = true;
@@ -159,7 +159,7 @@ hipError_t launch_loglik(const Model &m, const DeviceBuffers &b, const int32_t *
 {
     double *p = b.partial;
     hipLaunchKernelGGL(k_ll_cells, dim3(kCellBlocks), dim3(kLBlock), 0, st,
-                       (int64_t)m.G * m.V * m.Kp, m.ncap, b.n, b.t, b.logS, b.lfact, p, b.err);
+                       (int64_t)m.G * m.V * m.Kp, m.ncap, b.nt, b.logS, b.lfact, p, b.err);
     p += kCellBlocks;
     hipLaunchKernelGGL(k_ll_base, dim3(kBaseBlocks), dim3(kLBlock), 0, st, m.V, m.K, m.Kp, m.gamma,
                        b.B, b.Bk, p);

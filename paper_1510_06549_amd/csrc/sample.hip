@@ -6,9 +6,9 @@
 // documents are independent and the result does not depend on scheduling.
 //
 // Lane l owns the KPL contiguous topics [l KPL, l KPL + KPL) and, for each
-// token, loads its slices of the rows n[g][w][.], t[g][w][.], B[w][.]
-// (coalesced 16-byte loads; the next token's rows are in flight while the
-// current token is sampled).  The 2K unnormalised weights of the thesis's
+// token, loads its slices of the packed count row (n | t << 16)[g][w][.] and
+// of the shadow-base row B[w][.] (coalesced 16-byte loads; the next token's
+// rows are in flight while the current token is sampled).  The 2K unnormalised weights of the thesis's
 // conditionals (Eq. SPDP-sampling-w-z-r0 / -r1, P = I), with the token
 // removed from its own cell:
 //   W(k, r=1) = (alpha + c'_k) f1[g][k] (gamma + B'_wk) Q1(n', t')
@@ -31,8 +31,7 @@ struct SampleArgs {
     const int32_t *doc_group;
     const int32_t *zr_old;
     int32_t *zr_new;
-    const int32_t *n;
-    const int32_t *t;
+    const int32_t *nt;
     const int32_t *B;
     const int32_t *Ngk;
     const int32_t *Tgk;
@@ -46,6 +45,7 @@ struct SampleArgs {
     int64_t tr_begin, tr_end;
     uint64_t seed;
     int32_t D, V, K, Kp, ncap;
+    int64_t nQ;
     int32_t docs_per_xcd;
     uint32_t sweep;
     float alpha, gamma;
@@ -117,12 +117,12 @@ struct Exact {
 };
 
 template <int KPL>
-__device__ Exact exact_pair(const SampleArgs &A, int32_t k, int32_t k0, int32_t r0, int32_t n_raw,
-                            int32_t t_raw, int32_t b_raw, int32_t c_raw, const int32_t *Ng,
-                            const int32_t *Tg)
+__device__ Exact exact_pair(const SampleArgs &A, int32_t k, int32_t k0, int32_t r0, int32_t nt_raw,
+                            int32_t b_raw, int32_t c_raw, const int32_t *Ng, const int32_t *Tg)
 {
     Exact e{0.0, 0.0};
     if (k >= A.K) return e;
+    const int32_t n_raw = nt_raw & kCountMax, t_raw = nt_raw >> kCountBits;
     const int32_t del = (k == k0) ? 1 : 0;
     const int64_t nn = n_raw - del, tt = t_raw - del * r0;
     const double bw = (double)(b_raw - del * r0);
@@ -145,14 +145,63 @@ __device__ Exact exact_pair(const SampleArgs &A, int32_t k, int32_t k0, int32_t 
     return e;
 }
 
+// Wave64 inclusive prefix sum with DPP: Hillis-Steele inside each row of 16
+// lanes (row_shr 1, 2, 4, 8), then row 0's total into row 1 and row 2's into
+// row 3 (row_bcast:15), then lane 31's running total into rows 2 and 3
+// (row_bcast:31).  Lanes whose DPP source is disabled add 0.
+template <int CTRL, int ROW_MASK, bool BOUND>
+__device__ __forceinline__ float dpp_src(float x)
+{
+    return __int_as_float(
+        __builtin_amdgcn_update_dpp(0, __float_as_int(x), CTRL, ROW_MASK, 0xF, BOUND));
+}
+
+__device__ __forceinline__ float wave_inclusive_sum(float x)
+{
+    x += dpp_src<0x111, 0xF, true>(x);   // row_shr:1
+    x += dpp_src<0x112, 0xF, true>(x);   // row_shr:2
+    x += dpp_src<0x114, 0xF, true>(x);   // row_shr:4
+    x += dpp_src<0x118, 0xF, true>(x);   // row_shr:8
+    x += dpp_src<0x142, 0xA, false>(x);  // row_bcast:15 -> rows 1, 3
+    x += dpp_src<0x143, 0xC, false>(x);  // row_bcast:31 -> rows 2, 3
+    return x;
+}
+
+// value of lane - 1 (0 in lane 0)
+__device__ __forceinline__ float wave_shift_right(float x) { return dpp_src<0x138, 0xF, true>(x); }
+
+template <int KPL>
+__device__ __forceinline__ void lds_slice(float (&v)[KPL], const float *base)
+{
+    if constexpr (KPL % 4 == 0) {
+#pragma unroll
+        for (int c = 0; c < KPL / 4; ++c) {
+            const float4 x = reinterpret_cast<const float4 *>(base)[c];
+            v[4 * c + 0] = x.x;
+            v[4 * c + 1] = x.y;
+            v[4 * c + 2] = x.z;
+            v[4 * c + 3] = x.w;
+        }
+    } else if constexpr (KPL == 2) {
+        const float2 x = *reinterpret_cast<const float2 *>(base);
+        v[0] = x.x;
+        v[1] = x.y;
+    } else {
+        v[0] = base[0];
+    }
+}
+
 template <int KPL, bool TRACE>
 __global__ void __launch_bounds__(64, (KPL <= 8 ? 4 : 2)) k_sample(SampleArgs A)
 {
     constexpr int NO = 2 * KPL;  // outcomes per lane
-    // live document row c[k] and the per-(g, k) constants of the document's group
+    // live document row c[k], the group's per-topic constants f0, f1 and the
+    // products a0 = (alpha + c) f0, a1 = (alpha + c) f1 (kept in step with c)
     __shared__ int32_t c_lds[64 * KPL];
     __shared__ float f0_lds[64 * KPL];
     __shared__ float f1_lds[64 * KPL];
+    __shared__ __attribute__((aligned(16))) float a0_lds[64 * KPL];
+    __shared__ __attribute__((aligned(16))) float a1_lds[64 * KPL];
 
     // blocks are dealt round-robin over the 8 XCDs; give each XCD a
     // contiguous range of documents so a group's hot rows stay in its L2
@@ -182,6 +231,13 @@ __global__ void __launch_bounds__(64, (KPL <= 8 ? 4 : 2)) k_sample(SampleArgs A)
     __syncthreads();
     for (int64_t i = beg + lane; i < end; i += 64) atomicAdd(&c_lds[A.zr_old[i] >> 1], 1);
     __syncthreads();
+#pragma unroll
+    for (int j = 0; j < KPL; ++j) {
+        const float doc = A.alpha + (float)c_lds[kbase + j];
+        a0_lds[kbase + j] = doc * f0_lds[kbase + j];
+        a1_lds[kbase + j] = doc * f1_lds[kbase + j];
+    }
+    __syncthreads();
 
     // token stream: 64 tokens per chunk, lane l holds token base + l
     int64_t cbase = beg;
@@ -189,12 +245,12 @@ __global__ void __launch_bounds__(64, (KPL <= 8 ? 4 : 2)) k_sample(SampleArgs A)
     int32_t zr_c = (beg + lane < end) ? A.zr_old[beg + lane] : 0;
     int32_t gw_n = 0, zr_n = 0;
     int32_t out_c = 0;
+    const uint32_t q_last = (uint32_t)(A.nQ - 1);
 
-    Slice<KPL> rn, rt, rb;  // rows of the current token
+    Slice<KPL> rc, rb;  // packed count row and shadow-base row of the current token
     {
         const int32_t q = readlane(gw_c, 0);
-        load_slice<KPL>(rn, A.n + (int64_t)q * A.Kp, kbase, A.Kp);
-        load_slice<KPL>(rt, A.t + (int64_t)q * A.Kp, kbase, A.Kp);
+        load_slice<KPL>(rc, A.nt + (int64_t)q * A.Kp, kbase, A.Kp);
         load_slice<KPL>(rb, A.B + (int64_t)(q - gV) * A.Kp, kbase, A.Kp);
     }
 
@@ -207,58 +263,72 @@ __global__ void __launch_bounds__(64, (KPL <= 8 ? 4 : 2)) k_sample(SampleArgs A)
         }
         const int32_t zr0 = readlane(zr_c, idx);
         const int32_t k0 = zr0 >> 1, r0 = zr0 & 1;
-        // totals of the token's own topic (uniform loads)
-        const int32_t N0 = Ng[k0], T0 = Tg[k0], B0 = A.Bk[k0];
+        const int32_t q = readlane(gw_c, idx);
+        // the token's own cell and topic totals (uniform loads)
+        const int32_t nt0 = A.nt[(int64_t)q * A.Kp + k0];
+        const int32_t b0 = A.B[(int64_t)(q - gV) * A.Kp + k0];
+        const int32_t N0 = Ng[k0], T0 = Tg[k0], Bk0 = A.Bk[k0];
+        const int32_t n0 = nt0 & kCountMax, t0 = nt0 >> kCountBits;
+        // only head of a cell that keeps other customers: point mass
+        const bool sole = r0 && t0 == 1 && n0 > 1;
 
-        // removal-corrected state of the token's own cell and the Stirling
-        // ratio pairs (gathered before the next token's rows are requested)
+        // Stirling ratio pairs of every topic's cell as it stands (the token's
+        // own topic is recomputed below with the token removed); gathered
+        // before the next token's rows are requested
         float2 qv[KPL];
-        bool sole = false;
 #pragma unroll
         for (int j = 0; j < KPL; ++j) {
-            const int32_t del = (kbase + j == k0) ? 1 : 0;
-            if (del && r0 && rt.v[j] == 1 && rn.v[j] > 1) sole = true;
-            int32_t a_n = rn.v[j] - del;
-            a_n = a_n < 0 ? 0 : (a_n >= A.ncap ? A.ncap - 1 : a_n);
-            int32_t a_t = rt.v[j] - del * r0;
-            a_t = a_t < 0 ? 0 : (a_t > a_n ? a_n : a_t);
-            qv[j] = (a_n == 0) ? make_float2(0.0f, 1.0f)
-                               : A.Q[(int64_t)a_n * (a_n + 1) / 2 + a_t];
+            const uint32_t cn = (uint32_t)rc.v[j] & kCountMax;
+            const uint32_t ct = (uint32_t)rc.v[j] >> kCountBits;
+            uint32_t ix = ((cn * (cn + 1)) >> 1) + ct;
+            ix = ix < q_last ? ix : q_last;
+            qv[j] = A.Q[ix];
         }
 
         // next token's rows
-        Slice<KPL> xn, xt, xb;
+        Slice<KPL> xc, xb;
         const bool have_next = (i + 1 < end);
         if (have_next) {
             const int32_t q1 = (idx + 1 < 64) ? readlane(gw_c, idx + 1) : readlane(gw_n, 0);
-            load_slice<KPL>(xn, A.n + (int64_t)q1 * A.Kp, kbase, A.Kp);
-            load_slice<KPL>(xt, A.t + (int64_t)q1 * A.Kp, kbase, A.Kp);
+            load_slice<KPL>(xc, A.nt + (int64_t)q1 * A.Kp, kbase, A.Kp);
             load_slice<KPL>(xb, A.B + (int64_t)(q1 - gV) * A.Kp, kbase, A.Kp);
         }
 
         int32_t result = zr0;
         float u = -1.0f;
-        if (!__any(sole)) {
-            // constants of the token's own topic with the token removed (fp64,
-            // rounded once, as for the other topics)
+        if (!sole) {
+            // the token's own topic with the token removed: fp64 constants
+            // rounded once, as for the other topics
+            const int32_t n0r = n0 - 1, t0r = t0 - r0;
+            uint32_t ix0 = (uint32_t)(((n0r * (n0r + 1)) >> 1) + t0r);
+            ix0 = ix0 < q_last ? ix0 : q_last;
+            const float2 q0v = A.Q[ix0];
+            const int32_t c0 = c_lds[k0];
             const double inv = 1.0 / (A.b + (double)(N0 - 1));
             const float f0k = (float)inv;
             const float f1k =
-                (float)((A.b + A.a * (double)(T0 - r0)) * inv / (A.Vgamma + (double)(B0 - r0)));
+                (float)((A.b + A.a * (double)(T0 - r0)) * inv / (A.Vgamma + (double)(Bk0 - r0)));
+            const float doc0 = A.alpha + (float)(c0 - 1);
+            const float w1k0 = doc0 * f1k * (A.gamma + (float)(b0 - r0)) * q0v.y;
+            const float w0k0 = doc0 * f0k * q0v.x;
+
             // weights and lane-local inclusive prefix sums
+            float a0[KPL], a1[KPL];
+            lds_slice<KPL>(a0, a0_lds + kbase);
+            lds_slice<KPL>(a1, a1_lds + kbase);
             float s[NO];
             float acc = 0.0f;
 #pragma unroll
             for (int j = 0; j < KPL; ++j) {
-                const int32_t k = kbase + j;
-                const int32_t del = (k == k0) ? 1 : 0;
-                const float doc = A.alpha + (float)(c_lds[k] - del);
-                const float bw = A.gamma + (float)(rb.v[j] - del * r0);
-                const float w1 = doc * (del ? f1k : f1_lds[k]) * bw * qv[j].y;
-                const float w0 = doc * (del ? f0k : f0_lds[k]) * qv[j].x;
+                const bool own = (kbase + j == k0);
+                const float bw = A.gamma + (float)rb.v[j];
+                float w1 = a1[j] * bw * qv[j].y;
+                float w0 = a0[j] * qv[j].x;
+                w1 = own ? w1k0 : w1;
+                w0 = own ? w0k0 : w0;
                 if constexpr (TRACE) {
-                    if (i >= A.tr_begin && i < A.tr_end && k < A.K) {
-                        float *o = A.tr_w + (i - A.tr_begin) * 2 * (int64_t)A.K + 2 * k;
+                    if (i >= A.tr_begin && i < A.tr_end && kbase + j < A.K) {
+                        float *o = A.tr_w + (i - A.tr_begin) * 2 * (int64_t)A.K + 2 * (kbase + j);
                         o[0] = w1;
                         o[1] = w0;
                     }
@@ -268,61 +338,47 @@ __global__ void __launch_bounds__(64, (KPL <= 8 ? 4 : 2)) k_sample(SampleArgs A)
                 acc += w0;
                 s[2 * j + 1] = acc;
             }
-            // wave inclusive scan of the lane totals
-            float incl = acc;
-#pragma unroll
-            for (int o = 1; o < 64; o <<= 1) {
-                const float y = __shfl_up(incl, o);
-                if (lane >= o) incl += y;
-            }
-            float excl = __shfl_up(incl, 1);
-            if (lane == 0) excl = 0.0f;
-            const float total = __shfl(incl, 63);
+            const float incl = wave_inclusive_sum(acc);
+            const float excl = wave_shift_right(incl);
+            const float total = readlane_f(incl, 63);
 
             const uint32_t x = philox_x0(A.seed, (uint64_t)i, A.sweep, kPurposeSample);
             u = (float)(x >> 8) * (1.0f / 16777216.0f);
             const float target = u * total;
 
-            // first outcome whose prefix exceeds the target; an outcome of zero
-            // weight can only be first at a lane's start (s[0] == 0), so the
-            // guard is needed there only
-            int32_t cand = -1;
-            float lo = 0.0f, hi = 0.0f;
+            // count the prefixes at or below the target (prefixes are
+            // monotone, so the first crossing of this lane is outcome cnt) and
+            // flag any prefix within rounding distance of the target
+            const float rel = target - excl;
+            const float margin = kFixMargin * total;
+            int32_t cnt = 0;
+            bool near = false;
 #pragma unroll
-            for (int j = NO - 1; j >= 0; --j) {
-                const bool pos = (j == 0) ? (s[0] > 0.0f) : (s[j] > s[j - 1]);
-                if (pos && excl + s[j] > target) {
-                    cand = j;
-                    hi = excl + s[j];
-                    lo = excl + (j == 0 ? 0.0f : s[j - 1]);
-                }
+            for (int j = 0; j < NO; ++j) {
+                const float dlt = s[j] - rel;
+                cnt += (dlt <= 0.0f) ? 1 : 0;
+                near |= (fabsf(dlt) < margin);
             }
+            const unsigned long long cross = __ballot(cnt < NO);
             int32_t jstar = -1;
-            bool fix = true;
-            const unsigned long long m1 = __ballot(cand >= 0);
-            if (m1) {
-                const int32_t L = __ffsll((long long)m1) - 1;
-                jstar = L * NO + readlane(cand, L);
-                const float margin = kFixMargin * total;
-                fix = (target - readlane_f(lo, L) < margin) || (readlane_f(hi, L) - target < margin);
-            }
-            if (fix) {
+            if (cross && !__any(near)) {
+                const int32_t L = __ffsll((long long)cross) - 1;
+                jstar = L * NO + readlane(cnt, L);
+            } else {
                 // The draw is within rounding distance of a CDF boundary (or the
                 // fp32 scan found no crossing): take it again with fp64 weights
-                // from the integer counts, fp64 prefix sums and the same uniform.
+                // from the integer counts, fp64 prefix sums and the same uniform
                 // (rolled loops re-reading the current rows from memory keep
-                // this rare path from raising the kernel's register count)
-                const int64_t qrow = (int64_t)readlane(gw_c, idx);
-                const int32_t *__restrict__ nrow = A.n + qrow * A.Kp;
-                const int32_t *__restrict__ trow = A.t + qrow * A.Kp;
-                const int32_t *__restrict__ brow = A.B + (qrow - gV) * A.Kp;
+                // this rare path from raising the kernel's register count).
+                const int32_t *__restrict__ crow = A.nt + (int64_t)q * A.Kp;
+                const int32_t *__restrict__ brow = A.B + (int64_t)(q - gV) * A.Kp;
                 double acc64 = 0.0;
 #pragma unroll 1
                 for (int j = 0; j < KPL; ++j) {
                     const int32_t k = kbase + j;
                     if (k >= A.K) break;
-                    const Exact e = exact_pair<KPL>(A, k, k0, r0, nrow[k], trow[k], brow[k],
-                                                    c_lds[k], Ng, Tg);
+                    const Exact e = exact_pair<KPL>(A, k, k0, r0, crow[k], brow[k], c_lds[k],
+                                                    Ng, Tg);
                     acc64 += e.w1;
                     acc64 += e.w0;
                 }
@@ -341,8 +397,8 @@ __global__ void __launch_bounds__(64, (KPL <= 8 ? 4 : 2)) k_sample(SampleArgs A)
                 for (int j = 0; j < KPL; ++j) {
                     const int32_t k = kbase + j;
                     if (k >= A.K) break;
-                    const Exact e = exact_pair<KPL>(A, k, k0, r0, nrow[k], trow[k], brow[k],
-                                                    c_lds[k], Ng, Tg);
+                    const Exact e = exact_pair<KPL>(A, k, k0, r0, crow[k], brow[k], c_lds[k],
+                                                    Ng, Tg);
                     run += e.w1;
                     if (e.w1 > 0.0) {
                         last64 = 2 * j;
@@ -370,10 +426,16 @@ __global__ void __launch_bounds__(64, (KPL <= 8 ? 4 : 2)) k_sample(SampleArgs A)
                 const int32_t k1 = jstar >> 1, r1 = 1 - (jstar & 1);
                 result = zr_pack(k1, r1);
                 // DS operations of one wave execute in order, so the next
-                // token's reads of c_lds see this update
-                if (lane == 0) {
-                    c_lds[k0] -= 1;
-                    c_lds[k1] += 1;
+                // token's reads of the LDS rows see this update
+                if (lane == 0 && k1 != k0) {
+                    const int32_t ca = c_lds[k0] - 1, cb = c_lds[k1] + 1;
+                    c_lds[k0] = ca;
+                    c_lds[k1] = cb;
+                    const float da = A.alpha + (float)ca, db = A.alpha + (float)cb;
+                    a0_lds[k0] = da * f0_lds[k0];
+                    a1_lds[k0] = da * f1_lds[k0];
+                    a0_lds[k1] = db * f0_lds[k1];
+                    a1_lds[k1] = db * f1_lds[k1];
                 }
             }
         }
@@ -392,8 +454,7 @@ __global__ void __launch_bounds__(64, (KPL <= 8 ? 4 : 2)) k_sample(SampleArgs A)
             zr_c = zr_n;
         }
         if (have_next) {
-            rn = xn;
-            rt = xt;
+            rc = xc;
             rb = xb;
         }
     }
@@ -440,8 +501,7 @@ hipError_t launch_sample(const Model &m, const DeviceBuffers &b, const int32_t *
     A.doc_group = b.doc_group;
     A.zr_old = zr_old;
     A.zr_new = zr_new;
-    A.n = b.n;
-    A.t = b.t;
+    A.nt = b.nt;
     A.B = b.B;
     A.Ngk = b.Ngk;
     A.Tgk = b.Tgk;
@@ -460,6 +520,7 @@ hipError_t launch_sample(const Model &m, const DeviceBuffers &b, const int32_t *
     A.K = m.K;
     A.Kp = m.Kp;
     A.ncap = m.ncap;
+    A.nQ = tri_index(m.ncap, 0);
     A.docs_per_xcd = (m.D + 7) / 8;
     A.sweep = sweep;
     A.alpha = (float)m.alpha;

@@ -5,13 +5,8 @@
 //                  Corollary 17 passage) and the folded ratio pairs used by the
 //                  sampler (Eq. SPDP-sampling-w-z-r0 / -r1 with P = I)
 //   init_z         initial topics from Philox (purpose INIT), r = 0
-//   rebuild        counts n, t, B from (z, r) with integer atomics
-//   update         per-token count deltas after a sweep (integer atomics)
-//   repair         promote the smallest-index token of every cell left with
-//                  customers but no table (atomicMin on an encoded index)
 //   totals         N_gk, T_gk by an LDS-privatised histogram; B_k = sum_g T_gk
 //   factors        per-(g, k) sweep constants of the conditionals
-#include <algorithm>
 #include <climits>
 
 #include "spdp_internal.hpp"
@@ -187,163 +182,6 @@ __global__ void k_unpack_zr(int64_t N, const int32_t *__restrict__ zr, int32_t *
     if (r) r[i] = (uint8_t)(v & 1);
 }
 
-// ---------------------------------------------------------------- rebuild
-__global__ void k_rebuild(int64_t N, int32_t V, int32_t Kp, FastDiv divV,
-                          const int32_t *__restrict__ gw, const int32_t *__restrict__ zr,
-                          int32_t *__restrict__ n, int32_t *__restrict__ t, int32_t *__restrict__ B)
-{
-    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (i >= N) return;
-    const int32_t q = gw[i];
-    const int32_t v = zr[i];
-    const int32_t k = v >> 1;
-    atomicAdd(n + (int64_t)q * Kp + k, 1);
-    if (v & 1) {
-        const int32_t g = (int32_t)fastdiv((uint32_t)q, divV);
-        const int32_t w = q - g * V;
-        atomicAdd(t + (int64_t)q * Kp + k, 1);
-        atomicAdd(B + (int64_t)w * Kp + k, 1);
-    }
-}
-
-// ----------------------------------------------------------------- update
-// Apply the change of every token whose (z, r) moved.  A table count that
-// drops to zero flags its row for the repair step.  Statistics are summed per
-// block (repair: one atomic per block; update: one partial per block, reduced
-// only when the statistics are read).
-constexpr int kStatBlocks = 4096;
-
-__device__ __forceinline__ void block_count(unsigned long long *dst, uint32_t mine)
-{
-    __shared__ uint32_t acc;
-    if (threadIdx.x == 0) acc = 0;
-    __syncthreads();
-    uint32_t v = mine;
-    for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
-    if ((threadIdx.x & 63) == 0 && v) atomicAdd(&acc, v);
-    __syncthreads();
-    if (threadIdx.x == 0 && acc) atomicAdd(dst, (unsigned long long)acc);
-}
-
-__global__ void __launch_bounds__(kBlock) k_update(int64_t N, int32_t V, int32_t Kp, FastDiv divV,
-                                                   const int32_t *__restrict__ gw,
-                                                   const int32_t *__restrict__ zr_old,
-                                                   const int32_t *__restrict__ zr_new,
-                                                   int32_t *__restrict__ n, int32_t *__restrict__ t,
-                                                   int32_t *__restrict__ B,
-                                                   uint32_t *__restrict__ flags,
-                                                   uint32_t *__restrict__ moved_part)
-{
-    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    uint32_t moved = 0;
-    if (i < N) {
-        const int32_t vo = zr_old[i], vn = zr_new[i];
-        if (vo != vn) {
-            moved = 1;
-            const int32_t q = gw[i];
-            const int32_t g = (int32_t)fastdiv((uint32_t)q, divV);
-            const int32_t w = q - g * V;
-            const int32_t k0 = vo >> 1, k1 = vn >> 1;
-            const int64_t row = (int64_t)q * Kp;
-            if (k0 != k1) {
-                atomicSub(n + row + k0, 1);
-                atomicAdd(n + row + k1, 1);
-            }
-            if (vo & 1) {
-                const int32_t old = atomicSub(t + row + k0, 1);
-                atomicSub(B + (int64_t)w * Kp + k0, 1);
-                if (old == 1) atomicOr(flags + (q >> 5), 1u << (q & 31));
-            }
-            if (vn & 1) {
-                atomicAdd(t + row + k1, 1);
-                atomicAdd(B + (int64_t)w * Kp + k1, 1);
-            }
-        }
-    }
-    // per-block count of moved tokens (summed only when statistics are read)
-    __shared__ uint32_t acc;
-    if (threadIdx.x == 0) acc = 0;
-    __syncthreads();
-    uint32_t v = moved;
-    for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
-    if ((threadIdx.x & 63) == 0 && v) atomicAdd(&acc, v);
-    __syncthreads();
-    if (threadIdx.x == 0) moved_part[blockIdx.x] = acc;
-}
-
-__global__ void __launch_bounds__(kBlock) k_sum_u32(const uint32_t *__restrict__ x, int64_t n,
-                                                    unsigned long long *__restrict__ out)
-{
-    unsigned long long s = 0;
-    for (int64_t i = threadIdx.x; i < n; i += blockDim.x) s += x[i];
-    for (int o = 32; o > 0; o >>= 1) s += __shfl_xor(s, o);
-    __shared__ unsigned long long part[kBlock / 64];
-    if ((threadIdx.x & 63) == 0) part[threadIdx.x >> 6] = s;
-    __syncthreads();
-    if (threadIdx.x == 0) {
-        unsigned long long tot = 0;
-        for (int j = 0; j < kBlock / 64; ++j) tot += part[j];
-        *out = tot;
-    }
-}
-
-// ----------------------------------------------------------------- repair
-// Pass 1: tokens with r = 0 in a flagged row whose cell has no table bid for
-// the head with atomicMin(t, INT_MIN + i) (t <= 0 there, so the minimum
-// encodes the smallest token index).  Pass 2: the winner becomes the head.
-__device__ __forceinline__ bool row_flagged(const uint32_t *flags, int32_t q)
-{
-    return (flags[q >> 5] >> (q & 31)) & 1u;
-}
-
-__global__ void __launch_bounds__(kBlock) k_repair_bid(int64_t N, int32_t Kp,
-                                                       const int32_t *__restrict__ gw,
-                                                       const int32_t *__restrict__ zr,
-                                                       int32_t *__restrict__ t,
-                                                       const uint32_t *__restrict__ flags)
-{
-    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
-    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < N; i += stride) {
-        const int32_t v = zr[i];
-        if (v & 1) continue;
-        const int32_t q = gw[i];
-        if (!row_flagged(flags, q)) continue;
-        int32_t *cell = t + (int64_t)q * Kp + (v >> 1);
-        if (__hip_atomic_load(cell, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) <= 0)
-            atomicMin(cell, INT_MIN + (int32_t)i);
-    }
-}
-
-__global__ void __launch_bounds__(kBlock) k_repair_apply(int64_t N, int32_t V, int32_t Kp,
-                                                         FastDiv divV,
-                                                         const int32_t *__restrict__ gw,
-                                                         int32_t *__restrict__ zr,
-                                                         int32_t *__restrict__ t,
-                                                         int32_t *__restrict__ B,
-                                                         const uint32_t *__restrict__ flags,
-                                                         unsigned long long *__restrict__ ctr)
-{
-    uint32_t won = 0;
-    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
-    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < N; i += stride) {
-        const int32_t v = zr[i];
-        if (v & 1) continue;
-        const int32_t q = gw[i];
-        if (!row_flagged(flags, q)) continue;
-        const int32_t k = v >> 1;
-        int32_t *cell = t + (int64_t)q * Kp + k;
-        if (__hip_atomic_load(cell, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) ==
-            INT_MIN + (int32_t)i) {
-            ++won;
-            zr[i] = v | 1;
-            __hip_atomic_store(cell, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            const int32_t g = (int32_t)fastdiv((uint32_t)q, divV);
-            atomicAdd(B + (int64_t)(q - g * V) * Kp + k, 1);
-        }
-    }
-    block_count(ctr + 1, won);
-}
-
 // ----------------------------------------------------------------- totals
 // Per block, a chunk of at most 65535 tokens is histogrammed into LDS bins of
 // (g, k), each bin packing customers (low 16 bits) and tables (high 16 bits);
@@ -489,50 +327,6 @@ hipError_t launch_unpack_zr(const Model &m, const int32_t *zr, int32_t *z, uint8
     if (m.N <= 0) return hipSuccess;
     hipLaunchKernelGGL(k_unpack_zr, dim3((unsigned)blocks_for(m.N, kBlock)), dim3(kBlock), 0, st,
                        m.N, zr, z, r);
-    return hipGetLastError();
-}
-
-hipError_t launch_rebuild(const Model &m, const DeviceBuffers &b, const int32_t *zr, hipStream_t st)
-{
-    hipError_t e;
-    if ((e = fill(b.n, (int64_t)m.G * m.V * m.Kp, 0, st)) != hipSuccess) return e;
-    if ((e = fill(b.t, (int64_t)m.G * m.V * m.Kp, 0, st)) != hipSuccess) return e;
-    if ((e = fill(b.B, (int64_t)m.V * m.Kp, 0, st)) != hipSuccess) return e;
-    if (m.N <= 0) return hipSuccess;
-    hipLaunchKernelGGL(k_rebuild, dim3((unsigned)blocks_for(m.N, kBlock)), dim3(kBlock), 0, st, m.N,
-                       m.V, m.Kp, m.divV, b.gw, zr, b.n, b.t, b.B);
-    return hipGetLastError();
-}
-
-hipError_t launch_update(const Model &m, const DeviceBuffers &b, const int32_t *zr_old,
-                         const int32_t *zr_new, hipStream_t st)
-{
-    hipError_t e;
-    if ((e = fill(b.flags, ((int64_t)m.G * m.V + 31) / 32, 0u, st)) != hipSuccess) return e;
-    if ((e = fill(b.ctr, 2, 0ull, st)) != hipSuccess) return e;
-    if (m.N <= 0) return hipSuccess;
-    hipLaunchKernelGGL(k_update, dim3((unsigned)blocks_for(m.N, kBlock)), dim3(kBlock), 0, st, m.N,
-                       m.V, m.Kp, m.divV, b.gw, zr_old, zr_new, b.n, b.t, b.B, b.flags, b.moved_part);
-    return hipGetLastError();
-}
-
-hipError_t launch_repair(const Model &m, const DeviceBuffers &b, int32_t *zr, hipStream_t st)
-{
-    if (m.N <= 0) return hipSuccess;
-    const unsigned nb = (unsigned)std::min<int64_t>(blocks_for(m.N, kBlock), kStatBlocks);
-    hipLaunchKernelGGL(k_repair_bid, dim3(nb), dim3(kBlock), 0, st, m.N, m.Kp, b.gw, zr, b.t,
-                       b.flags);
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(k_repair_apply, dim3(nb), dim3(kBlock), 0, st, m.N, m.V, m.Kp, m.divV, b.gw,
-                       zr, b.t, b.B, b.flags, b.ctr);
-    return hipGetLastError();
-}
-
-hipError_t launch_moved_sum(const Model &m, const DeviceBuffers &b, hipStream_t st)
-{
-    hipLaunchKernelGGL(k_sum_u32, dim3(1), dim3(kBlock), 0, st, b.moved_part,
-                       blocks_for(m.N, kBlock), b.ctr);
     return hipGetLastError();
 }
 

@@ -71,10 +71,13 @@ __host__ __device__ __forceinline__ int64_t tri_index(int64_t n, int64_t t)
 }
 
 // ---------------------------------------------------------------------------
-// Device state.  Count rows: row index q = g V + w; row q of n / t holds the
-// Kp topic entries of (g, w) (Kp = K rounded up to the sampler's vector width,
-// padding entries stay zero).  B rows are indexed by w.
+// Device state.  Count rows: row index q = g V + w; row q of nt holds the Kp
+// topic cells of (g, w) (Kp = K rounded up to the sampler's vector width,
+// padding cells stay zero), each cell packing the customer count n in bits
+// 0..15 and the table count t in bits 16..31.  B rows are indexed by w.
 // ---------------------------------------------------------------------------
+constexpr int32_t kCountBits = 16;
+constexpr int32_t kCountMax = (1 << kCountBits) - 1;  // largest n a packed cell holds
 struct Model {
     int64_t N;
     int32_t D, V, G, K, Kp;
@@ -89,9 +92,10 @@ struct DeviceBuffers {
     int64_t *doc_off = nullptr;   // [D+1]
     int32_t *doc_group = nullptr; // [D]
     int32_t *zr[2] = {nullptr, nullptr}; // [N] current / next packed state
-    int32_t *n = nullptr;         // [G V][Kp]
-    int32_t *t = nullptr;         // [G V][Kp]
-    int32_t *B = nullptr;         // [V][Kp]
+    int32_t *nt = nullptr;        // [G V][Kp] packed n | t << 16
+    int32_t *B = nullptr;         // [V][Kp]   shadow-base table counts
+    int32_t *perm = nullptr;      // [N] tokens sorted by row (stable)
+    int32_t *row_off = nullptr;   // [G V + 1] offsets of each row's tokens in perm
     int32_t *Ngk = nullptr;       // [G][Kp]
     int32_t *Tgk = nullptr;       // [G][Kp]
     int32_t *Bk = nullptr;        // [Kp]
@@ -100,14 +104,15 @@ struct DeviceBuffers {
     float2 *Q = nullptr;          // [tri(ncap)] (Q0, Q1) folded Stirling ratios
     double *logS = nullptr;       // [tri(ncap + 1)] log S^n_{t,a}
     double *lfact = nullptr;      // [ncap + 1] log n!
-    uint32_t *flags = nullptr;    // [ceil(G V / 32)] rows whose t hit zero
-    unsigned long long *ctr = nullptr; // [4] changed (on demand), repaired
-    uint32_t *moved_part = nullptr;    // [ceil(N / 256)] per-block moved-token counts
+    uint32_t *rep_part = nullptr; // [G V] heads promoted per row in the last rebuild
+    unsigned long long *part = nullptr; // reduction partials
+    unsigned long long *ctr = nullptr;  // [4] changed, repaired (filled on demand)
     double *partial = nullptr;    // loglik block partials
     int64_t partial_len = 0;
     int32_t *err = nullptr;       // [2] device error flags
     double *scalar = nullptr;     // [1] reduction result
     // debug-conditional buffers (allocated on demand)
+    int32_t *zr_dbg = nullptr;
     float *tr_w = nullptr;
     float *tr_u = nullptr;
     int64_t tr_cap = 0;
@@ -129,12 +134,15 @@ hipError_t launch_pack_zr(const Model &m, const int32_t *z, const uint8_t *r, in
                           int32_t *bad, hipStream_t st);
 hipError_t launch_unpack_zr(const Model &m, const int32_t *zr, int32_t *z, uint8_t *r,
                             hipStream_t st);
-hipError_t launch_rebuild(const Model &m, const DeviceBuffers &b, const int32_t *zr,
-                          hipStream_t st);
-hipError_t launch_update(const Model &m, const DeviceBuffers &b, const int32_t *zr_old,
-                         const int32_t *zr_new, hipStream_t st);
-hipError_t launch_repair(const Model &m, const DeviceBuffers &b, int32_t *zr, hipStream_t st);
-hipError_t launch_moved_sum(const Model &m, const DeviceBuffers &b, hipStream_t st);
+hipError_t build_row_index(const Model &m, DeviceBuffers &b, const int32_t *gw_count,
+                           hipStream_t st);
+hipError_t launch_rows(const Model &m, const DeviceBuffers &b, int32_t *zr, hipStream_t st);
+hipError_t launch_base(const Model &m, const DeviceBuffers &b, hipStream_t st);
+hipError_t launch_unpack_counts(const Model &m, const DeviceBuffers &b, int32_t g,
+                                int32_t *n_out, int32_t *t_out, hipStream_t st);
+hipError_t launch_stat_sums(const Model &m, const DeviceBuffers &b, const int32_t *zr_now,
+                            const int32_t *zr_before, hipStream_t st);
+int64_t stat_partials_needed();
 hipError_t launch_totals(const Model &m, const DeviceBuffers &b, const int32_t *zr,
                          hipStream_t st);
 hipError_t launch_factors(const Model &m, const DeviceBuffers &b, hipStream_t st);
