@@ -49,7 +49,7 @@ extern "C" {
 #define SPDP_E_ARG (-1)   /* invalid argument (null pointer, value out of range) */
 #define SPDP_E_NOMEM (-2) /* device or host allocation failed                   */
 #define SPDP_E_HIP (-3)   /* a HIP runtime call failed                          */
-#define SPDP_E_RANGE (-4) /* the Stirling cache would exceed its memory budget   */
+#define SPDP_E_RANGE (-4) /* a size limit of the state would be exceeded          */
 #define SPDP_E_STATE (-5) /* an invariant of the count state is violated         */
 
 #define SPDP_MAX_K 1024
@@ -84,7 +84,8 @@ typedef struct {
  *   a      Pitman-Yor discount, 0 <= a < 1
  *   b      Pitman-Yor concentration, > 0
  *   gamma  symmetric Dirichlet prior of the shadow base phi0_k, > 0
- * Errors: E_ARG, E_NOMEM, E_HIP, E_RANGE (Stirling cache beyond 4 GiB).
+ * Errors: E_ARG, E_NOMEM, E_HIP, E_RANGE (Stirling cache beyond 4 GiB, or a
+ * (group, word) pair occurring 65536 times or more: counts are held in 16 bits).
  * On success *out holds the new state; on error *out is NULL.
  */
 int spdp_create(const spdp_corpus *corpus, const spdp_groups *groups, int32_t K, double alpha,
@@ -151,7 +152,9 @@ int spdp_set_assignments(spdp_state *s, const int32_t *z, const uint8_t *r, int 
  * fp32 unnormalised weights of all 2K outcomes (w_out, [(tok_end - tok_begin)
  * * 2K], outcome order as in spdp_sweep), the uniform (u_out, -1 for a token
  * kept by the sole-head rule) and the sampled packed outcome (zr_out, value
- * 2 z + r, may be NULL).  Uses the same kernel as spdp_sweep.  Synchronises.
+ * 2 z + r, may be NULL).  With w_out and u_out both NULL no trace is kept and
+ * any token range may be requested (the sampled state before the count update
+ * and repair).  Uses the same kernel as spdp_sweep.  Synchronises.
  * Errors: E_ARG, E_NOMEM, E_HIP.
  */
 int spdp_debug_conditionals(spdp_state *s, uint32_t sweep, uint64_t seed, int64_t tok_begin,
@@ -168,7 +171,8 @@ int spdp_stats(const spdp_state *s, int64_t *changed, int64_t *repaired);
  * Per-kernel timing with HIP events on the state's stream.  enable = 1 starts
  * recording (and clears the accumulators), 0 stops.  spdp_kernel_times writes
  * the accumulated milliseconds and launch counts of the SPDP_NKERNELS kernel
- * classes (order: sample, update, repair, totals).  Synchronises.
+ * classes, in this order: sampling; count rebuild with repair; shadow base;
+ * per-restaurant totals and per-sweep constants.  Synchronises.
  */
 #define SPDP_NKERNELS 4
 int spdp_kernel_timing(spdp_state *s, int enable);

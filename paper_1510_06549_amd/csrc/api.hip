@@ -490,7 +490,16 @@ int spdp_debug_conditionals(spdp_state *s, uint32_t sweep, uint64_t seed, int64_
     DeviceBuffers &b = s->b;
     const int64_t T = tok_end - tok_begin;
     if (T == 0) return SPDP_OK;
-    if (T > b.tr_cap) {
+    if (!b.zr_dbg) {
+        void *p = nullptr;
+        if (hipMalloc(&p, (size_t)m.N * sizeof(int32_t)) != hipSuccess) {
+            (void)hipGetLastError();
+            return fail(SPDP_E_NOMEM, "debug state buffer");
+        }
+        b.zr_dbg = (int32_t *)p;
+    }
+    const bool trace = (w_out != nullptr || u_out != nullptr);
+    if (trace && T > b.tr_cap) {
         if (b.tr_w) hipFree(b.tr_w);
         if (b.tr_u) hipFree(b.tr_u);
         b.tr_w = nullptr;
@@ -509,20 +518,14 @@ int spdp_debug_conditionals(spdp_state *s, uint32_t sweep, uint64_t seed, int64_
         b.tr_u = (float *)p;
         b.tr_cap = T;
     }
-    if (!b.zr_dbg) {
-        void *p = nullptr;
-        if (hipMalloc(&p, (size_t)m.N * sizeof(int32_t)) != hipSuccess) {
-            (void)hipGetLastError();
-            return fail(SPDP_E_NOMEM, "debug state buffer");
-        }
-        b.zr_dbg = (int32_t *)p;
+    if (trace) {
+        HIP_TRY(launch_fill_i32((int32_t *)b.tr_w, T * 2 * m.K, 0, s->st));
+        HIP_TRY(launch_fill_i32((int32_t *)b.tr_u, T, 0, s->st));
     }
-    HIP_TRY(launch_fill_i32((int32_t *)b.tr_w, T * 2 * m.K, 0, s->st));
-    HIP_TRY(launch_fill_i32((int32_t *)b.tr_u, T, 0, s->st));
     int32_t *zr_old = b.zr[s->cur], *zr_tmp = b.zr_dbg;
     HIP_TRY(launch_factors(m, b, s->st));
-    HIP_TRY(launch_sample(m, b, zr_old, zr_tmp, sweep, seed, b.tr_w, b.tr_u, tok_begin, tok_end,
-                          s->st));
+    HIP_TRY(launch_sample(m, b, zr_old, zr_tmp, sweep, seed, trace ? b.tr_w : nullptr,
+                          trace ? b.tr_u : nullptr, tok_begin, tok_end, s->st));
     const hipMemcpyKind kind = where ? hipMemcpyDeviceToDevice : hipMemcpyDeviceToHost;
     if (w_out) HIP_TRY(hipMemcpyAsync(w_out, b.tr_w, (size_t)T * 2 * m.K * 4, kind, s->st));
     if (u_out) HIP_TRY(hipMemcpyAsync(u_out, b.tr_u, (size_t)T * 4, kind, s->st));

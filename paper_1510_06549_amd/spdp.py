@@ -23,7 +23,7 @@ SPDP_E_RANGE = -4
 SPDP_E_STATE = -5
 SPDP_MAX_K = 1024
 SPDP_NKERNELS = 4
-KERNEL_CLASSES = ("sample", "update", "repair", "totals")
+KERNEL_CLASSES = ("sample", "rebuild", "base", "totals")
 
 # Every entry point of include/spdp.h, in declaration order.
 EXPORTS = (
@@ -283,6 +283,13 @@ class Sampler:
         zr = np.zeros(T, dtype=np.int32)
         spdp_debug_conditionals(self.h, sweep, seed, tok_begin, tok_end, w, u, zr)
         return w, u, zr
+
+    def sampled(self, sweep, seed, tok_begin=0, tok_end=None):
+        """Packed 2z + r of the sampling step only (before update and repair)."""
+        tok_end = self.N if tok_end is None else tok_end
+        zr = np.zeros(tok_end - tok_begin, dtype=np.int32)
+        spdp_debug_conditionals(self.h, sweep, seed, tok_begin, tok_end, None, None, zr)
+        return zr
 
     def stats(self):
         return spdp_stats(self.h)
