@@ -303,8 +303,27 @@ int spdp_create(const spdp_corpus *corpus, const spdp_groups *groups, int32_t K,
     TRY(dev_alloc(s, &B.Bk, m.Kp, "B_k"));
     TRY(dev_alloc(s, &B.f0, (int64_t)G * m.Kp, "f0"));
     TRY(dev_alloc(s, &B.f1, (int64_t)G * m.Kp, "f1"));
+    TRY(dev_alloc(s, &B.fk, 3 * (int64_t)G * m.Kp, "removal factors"));
     TRY(dev_alloc(s, &B.rep_part, rows, "repair partial counts"));
     TRY(dev_alloc(s, &B.part, stat_partials_needed(), "reduction partials"));
+    {
+        TRY(dev_alloc(s, &B.exact, 1, "sampler context"));
+        ExactCtx x{};
+        x.Ngk = B.Ngk;
+        x.Tgk = B.Tgk;
+        x.Bk = B.Bk;
+        x.B = B.B;
+        x.logS = B.logS;
+        x.a = a;
+        x.b = b;
+        x.Vgamma = (double)V * gamma;
+        x.alpha = alpha;
+        x.gamma = gamma;
+        x.K = K;
+        x.ncap = m.ncap;
+        TRY_HIP(hipMemcpyAsync(B.exact, &x, sizeof x, hipMemcpyHostToDevice, s->st));
+        TRY_HIP(hipStreamSynchronize(s->st));
+    }
     B.partial_len = loglik_partials_needed();
     TRY(dev_alloc(s, &B.partial, B.partial_len, "loglik partials"));
     s->cur = 0;

@@ -5,20 +5,23 @@
 // doc-topic row c[k] is live in LDS and its tokens run in order, so
 // documents are independent and the result does not depend on scheduling.
 //
-// Lane l owns the KPL contiguous topics [l KPL, l KPL + KPL) and, for each
-// token, loads its slices of the packed count row (n | t << 16)[g][w][.] and
-// of the shadow-base row B[w][.] (coalesced 16-byte loads; the next token's
-// rows are in flight while the current token is sampled).  The 2K unnormalised weights of the thesis's
-// conditionals (Eq. SPDP-sampling-w-z-r0 / -r1, P = I), with the token
-// removed from its own cell:
+// Lane l owns the KPL contiguous topics [l KPL, l KPL + KPL).  For each token
+// the wave loads its packed count row (n | t << 16)[g][w][.] and its
+// shadow-base row B[w][.] with coalesced 16-byte loads, two tokens ahead of
+// use (three register sets rotate, so no copy ever waits on a load in
+// flight), and gathers the folded Stirling ratios (Q0, Q1) of every cell.  The
+// 2K unnormalised weights of the thesis's conditionals (Eq.
+// SPDP-sampling-w-z-r0 / -r1, P = I), with the token removed from its own
+// cell, are
 //   W(k, r=1) = (alpha + c'_k) f1[g][k] (gamma + B'_wk) Q1(n', t')
 //   W(k, r=0) = (alpha + c'_k) f0[g][k] Q0(n', t')
-// where f0 = 1/(b + N'), f1 = (b + a T')/(b + N')/(V gamma + B'_k) are the
-// per-(group, topic) sweep constants (recomputed in fp64 for the token's own
-// topic) and (Q0, Q1) the folded Stirling ratios.  Outcome j = 2k is (k, r=1),
-// j = 2k+1 is (k, r=0); the lane-local inclusive prefix sums plus a wave scan
-// of the lane totals give the CDF, and the draw is the first outcome whose
-// prefix exceeds u * total, u the 24-bit Philox uniform of the token.
+// with f0 = 1/(b + N'), f1 = (b + a T')/(b + N')/(V gamma + B'_k) the
+// per-(group, topic) sweep constants, taken for the token's own topic from
+// the removed-customer table fk.  Outcome j = 2k is (k, r=1), j = 2k+1 is
+// (k, r=0); the lane-local inclusive prefix sums plus a wave scan of the lane
+// totals give the CDF, and the draw is the first outcome whose prefix exceeds
+// u * total, u the 24-bit Philox uniform of the token.  A draw within fp32
+// rounding distance of a CDF boundary is taken again in fp64.
 #include "spdp_internal.hpp"
 
 namespace spdp {
@@ -33,34 +36,32 @@ struct SampleArgs {
     int32_t *zr_new;
     const int32_t *nt;
     const int32_t *B;
-    const int32_t *Ngk;
-    const int32_t *Tgk;
-    const int32_t *Bk;
     const float *f0;
     const float *f1;
+    const float *fk;
     const float2 *Q;
-    const double *logS;
+    const ExactCtx *exact;
     float *tr_w;
     float *tr_u;
     int64_t tr_begin, tr_end;
     uint64_t seed;
-    int32_t D, V, K, Kp, ncap;
-    int64_t nQ;
+    int32_t D, V, K, Kp;
+    int64_t nQ, GK;
     int32_t docs_per_xcd;
     uint32_t sweep;
     float alpha, gamma;
-    double alpha_d, gamma_d, a, b, Vgamma;
 };
+
+// Tokens per step of the token stream.  The stream registers hold 64 tokens
+// (lane l: token base + l); advancing by 48 leaves the next two tokens of
+// every position in the same registers, and 48 is a multiple of the three
+// rotating row buffers.
+constexpr int32_t kChunk = 48;
 
 // KPL consecutive int32 of one row, loaded with the widest aligned vector
 // loads; chunks that start at or beyond the row length are zero.
 template <int KPL>
-struct Slice {
-    int32_t v[KPL];
-};
-
-template <int KPL>
-__device__ __forceinline__ void load_slice(Slice<KPL> &s, const int32_t *__restrict__ row,
+__device__ __forceinline__ void load_slice(int32_t (&v)[KPL], const int32_t *__restrict__ row,
                                            int32_t kbase, int32_t Kp)
 {
     if constexpr (KPL % 4 == 0) {
@@ -68,19 +69,50 @@ __device__ __forceinline__ void load_slice(Slice<KPL> &s, const int32_t *__restr
         for (int c = 0; c < KPL / 4; ++c) {
             int4 x = make_int4(0, 0, 0, 0);
             if (kbase + 4 * c < Kp) x = *reinterpret_cast<const int4 *>(row + kbase + 4 * c);
-            s.v[4 * c + 0] = x.x;
-            s.v[4 * c + 1] = x.y;
-            s.v[4 * c + 2] = x.z;
-            s.v[4 * c + 3] = x.w;
+            v[4 * c + 0] = x.x;
+            v[4 * c + 1] = x.y;
+            v[4 * c + 2] = x.z;
+            v[4 * c + 3] = x.w;
         }
     } else if constexpr (KPL == 2) {
         int2 x = make_int2(0, 0);
         if (kbase < Kp) x = *reinterpret_cast<const int2 *>(row + kbase);
-        s.v[0] = x.x;
-        s.v[1] = x.y;
+        v[0] = x.x;
+        v[1] = x.y;
     } else {
         static_assert(KPL == 1, "KPL must be 1, 2 or a multiple of 4");
-        s.v[0] = (kbase < Kp) ? row[kbase] : 0;
+        v[0] = (kbase < Kp) ? row[kbase] : 0;
+    }
+}
+
+// This lane's KPL cells of a count or shadow-base row for the token loop.
+// Every lane issues every load, so the number of loads in flight is the same
+// on every path and a wait for one load never has to assume that later ones
+// were skipped.  A chunk past the row end reads the row's first chunk instead:
+// those cells belong to padding topics, whose weights are zero through the
+// zero constants f0 = f1 = 0 whatever the cell values, and the values are
+// used as loaded (no select that would wait for the load).
+template <int KPL>
+__device__ __forceinline__ void load_row(int32_t (&v)[KPL], const int32_t *__restrict__ row,
+                                         int32_t kbase, int32_t Kp)
+{
+    if constexpr (KPL % 4 == 0) {
+#pragma unroll
+        for (int c = 0; c < KPL / 4; ++c) {
+            const int32_t off = (kbase + 4 * c < Kp) ? kbase + 4 * c : 0;
+            const int4 x = *reinterpret_cast<const int4 *>(row + off);
+            v[4 * c + 0] = x.x;
+            v[4 * c + 1] = x.y;
+            v[4 * c + 2] = x.z;
+            v[4 * c + 3] = x.w;
+        }
+    } else if constexpr (KPL == 2) {
+        const int2 x = *reinterpret_cast<const int2 *>(row + (kbase < Kp ? kbase : 0));
+        v[0] = x.x;
+        v[1] = x.y;
+    } else {
+        static_assert(KPL == 1, "KPL must be 1, 2 or a multiple of 4");
+        v[0] = row[kbase < Kp ? kbase : 0];
     }
 }
 
@@ -88,10 +120,10 @@ template <int KPL>
 __device__ __forceinline__ void load_slice_f(float (&s)[KPL], const float *__restrict__ row,
                                              int32_t kbase, int32_t Kp)
 {
-    Slice<KPL> tmp;
+    int32_t tmp[KPL];
     load_slice<KPL>(tmp, reinterpret_cast<const int32_t *>(row), kbase, Kp);
 #pragma unroll
-    for (int j = 0; j < KPL; ++j) s[j] = __int_as_float(tmp.v[j]);
+    for (int j = 0; j < KPL; ++j) s[j] = __int_as_float(tmp[j]);
 }
 
 __device__ __forceinline__ int32_t readlane(int32_t x, int32_t lane)
@@ -104,20 +136,39 @@ __device__ __forceinline__ float readlane_f(float x, int32_t lane)
     return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(x), lane));
 }
 
+// Hides a uniform value from loop-invariant hoisting: the Philox round keys
+// are then derived per token with scalar adds instead of being held (and
+// spilled) across the token loop.
+__device__ __forceinline__ uint64_t opaque_u64(uint64_t x)
+{
+    uint32_t lo = (uint32_t)x, hi = (uint32_t)(x >> 32);
+    asm volatile("" : "+s"(lo), "+s"(hi));
+    return ((uint64_t)hi << 32) | lo;
+}
+
+// Marks a wave-uniform offset as per-lane, so that the load using it is a
+// vector load: vector loads complete in issue order on one counter, which
+// lets a load issued two tokens ahead be waited for without waiting for the
+// loads issued after it.
+__device__ __forceinline__ int64_t as_vector(int64_t x)
+{
+    asm volatile("" : "+v"(x));
+    return x;
+}
+
 // Relative distance from a CDF boundary below which the fp32 decision is
 // re-taken in fp64.  The fp32 prefix sums are within about 3e-6 of the exact
 // ones (at most 7 roundings per weight, at most 2 KPL + 6 additions per
 // prefix, KPL <= 16), so outside this margin both decisions agree.
 constexpr float kFixMargin = 8e-6f;
 
-// fp64 weights of outcome pair j of this lane, evaluated directly from the
-// integer counts and the fp64 log Stirling table (the rare boundary path).
+// fp64 weights of outcome pair k, evaluated directly from the integer counts
+// and the fp64 log Stirling table (the rare boundary path).
 struct Exact {
     double w1, w0;
 };
 
-template <int KPL>
-__device__ Exact exact_pair(const SampleArgs &A, int32_t k, int32_t k0, int32_t r0, int32_t nt_raw,
+__device__ Exact exact_pair(const ExactCtx &A, int32_t k, int32_t k0, int32_t r0, int32_t nt_raw,
                             int32_t b_raw, int32_t c_raw, const int32_t *Ng, const int32_t *Tg)
 {
     Exact e{0.0, 0.0};
@@ -128,7 +179,7 @@ __device__ Exact exact_pair(const SampleArgs &A, int32_t k, int32_t k0, int32_t 
     const double bw = (double)(b_raw - del * r0);
     const double N = (double)(Ng[k] - del), T = (double)(Tg[k] - del * r0);
     const double Bt = (double)(A.Bk[k] - del * r0);
-    const double doc = (double)A.alpha_d + (double)(c_raw - del);
+    const double doc = A.alpha + (double)(c_raw - del);
     double q0, q1;
     if (nn <= 0) {
         q0 = 0.0;
@@ -141,7 +192,7 @@ __device__ Exact exact_pair(const SampleArgs &A, int32_t k, int32_t k0, int32_t 
         q1 = (double)(t_ + 1) / (double)(n_ + 1) * exp(A.logS[tri_index(n_ + 1, t_ + 1)] - ls);
     }
     e.w0 = doc / (A.b + N) * q0;
-    e.w1 = doc * (A.b + A.a * T) / (A.b + N) * ((double)A.gamma_d + bw) / (A.Vgamma + Bt) * q1;
+    e.w1 = doc * (A.b + A.a * T) / (A.b + N) * (A.gamma + bw) / (A.Vgamma + Bt) * q1;
     return e;
 }
 
@@ -170,33 +221,268 @@ __device__ __forceinline__ float wave_inclusive_sum(float x)
 // value of lane - 1 (0 in lane 0)
 __device__ __forceinline__ float wave_shift_right(float x) { return dpp_src<0x138, 0xF, true>(x); }
 
+// Interleaved LDS rows: the KPL values of lane l sit in 16-byte chunks
+// (chunk c of lane l at (c * 64 + l) * 4), so a wave's vector read of one
+// chunk touches 64 consecutive 16-byte words and no bank twice.
 template <int KPL>
-__device__ __forceinline__ void lds_slice(float (&v)[KPL], const float *base)
+__device__ __forceinline__ int32_t lds_pos(int32_t k)
+{
+    const int32_t l = k / KPL, j = k % KPL;
+    if constexpr (KPL % 4 == 0) return ((j >> 2) * 64 + l) * 4 + (j & 3);
+    else return j * 64 + l;
+}
+
+template <int KPL>
+__device__ __forceinline__ void lds_row(float (&v)[KPL], const float *base, int32_t lane)
 {
     if constexpr (KPL % 4 == 0) {
 #pragma unroll
         for (int c = 0; c < KPL / 4; ++c) {
-            const float4 x = reinterpret_cast<const float4 *>(base)[c];
+            const float4 x = reinterpret_cast<const float4 *>(base)[c * 64 + lane];
             v[4 * c + 0] = x.x;
             v[4 * c + 1] = x.y;
             v[4 * c + 2] = x.z;
             v[4 * c + 3] = x.w;
         }
-    } else if constexpr (KPL == 2) {
-        const float2 x = *reinterpret_cast<const float2 *>(base);
-        v[0] = x.x;
-        v[1] = x.y;
     } else {
-        v[0] = base[0];
+#pragma unroll
+        for (int j = 0; j < KPL; ++j) v[j] = base[j * 64 + lane];
     }
+}
+
+// The rows one token needs: this lane's slices of its packed count row and
+// of its shadow-base row.
+template <int KPL>
+struct Rows {
+    int32_t n[KPL];
+    int32_t b[KPL];
+};
+
+// Per-wave state of one document.
+template <int KPL>
+struct DocWave {
+    int32_t lane, kbase, gV;
+    int64_t gK, cb, end;
+    int32_t *c_lds;
+    float *f0_lds, *f1_lds, *a0_lds, *a1_lds;
+    // token stream: lane l holds (row index, packed state) of token cb + l,
+    // lanes past the document's end repeat its last token
+    int32_t gw_c, zr_c, out_c;
+};
+
+template <int KPL>
+__device__ __forceinline__ void load_rows(const SampleArgs &A, const DocWave<KPL> &W, int32_t x,
+                                          Rows<KPL> &R)
+{
+    const int32_t q = readlane(W.gw_c, x);
+    load_row<KPL>(R.n, A.nt + (int64_t)q * A.Kp, W.kbase, A.Kp);
+    load_row<KPL>(R.b, A.B + (int64_t)(q - W.gV) * A.Kp, W.kbase, A.Kp);
+}
+
+// Stream registers of the tokens from W.cb on (lanes past the document's end
+// repeat its last token).  They are waited for here, once per 48 tokens, so
+// that no token's wait on its prefetched rows has to cover them.
+template <int KPL>
+__device__ __forceinline__ void load_stream(const SampleArgs &A, DocWave<KPL> &W, int64_t last)
+{
+    const int64_t t = min(W.cb + W.lane, last);
+    W.gw_c = A.gw[t];
+    W.zr_c = A.zr_old[t];
+    asm volatile("" ::"v"(W.gw_c), "v"(W.zr_c));
+}
+
+// Token cb + x: sample it with the rows in `cur` and request the rows of the
+// token two places ahead into `fill`.
+template <int KPL, bool TRACE>
+__device__ __forceinline__ void sample_token(const SampleArgs &A, DocWave<KPL> &W, int32_t x,
+                                             const Rows<KPL> &cur, Rows<KPL> &fill)
+{
+    constexpr int NO = 2 * KPL;  // outcomes per lane
+    const int32_t lane = W.lane, kbase = W.kbase;
+    const int64_t i = W.cb + x;
+
+    const int32_t zr0 = readlane(W.zr_c, x);
+    const int32_t k0 = zr0 >> 1, r0 = zr0 & 1;
+    const uint32_t q_last = (uint32_t)(A.nQ - 1);
+    // the token leaves its cell: one customer, and one table if it is a head
+    const int32_t dv = 1 + (r0 << kCountBits);
+
+    // Stirling ratio pairs of every cell, the own cell without the token
+    float2 qv[KPL];
+    int32_t own_nt = 0;
+#pragma unroll
+    for (int j = 0; j < KPL; ++j) {
+        const bool own = (kbase + j == k0);
+        own_nt = own ? cur.n[j] : own_nt;
+        const uint32_t v = (uint32_t)(cur.n[j] - (own ? dv : 0));
+        const uint32_t cn = v & kCountMax, ct = v >> kCountBits;
+        uint32_t ix = ((cn * (cn + 1)) >> 1) + ct;
+        ix = ix < q_last ? ix : q_last;
+        qv[j] = A.Q[ix];
+    }
+    // removed-customer constants of the own topic (a small table that stays
+    // in cache; requested with the gathers)
+    const float f0k = A.fk[as_vector(W.gK + k0)];
+    const float f1k = A.fk[as_vector((int64_t)(1 + r0) * A.GK + W.gK + k0)];
+    // rows of token i + 2 (past the end: the last token's rows again,
+    // unused), requested after the gathers so that waiting for the gathers
+    // does not wait for them
+    asm volatile("" ::: "memory");
+    load_rows<KPL>(A, W, x + 2, fill);
+    // only head of a cell that keeps other customers: point mass
+    const int32_t nt0 = readlane(own_nt, k0 / KPL);
+    const bool sole = r0 && (nt0 >> kCountBits) == 1 && (nt0 & kCountMax) > 1;
+
+    int32_t result = zr0;
+    float u = -1.0f;
+    if (!sole) {
+        const float doc0 = A.alpha + (float)(W.c_lds[k0] - 1);
+        const float m1k0 = doc0 * f1k, m0k0 = doc0 * f0k;
+
+        // weights and lane-local inclusive prefix sums
+        float a0[KPL], a1[KPL];
+        lds_row<KPL>(a0, W.a0_lds, lane);
+        lds_row<KPL>(a1, W.a1_lds, lane);
+        float s[NO];
+        float acc = 0.0f;
+#pragma unroll
+        for (int j = 0; j < KPL; ++j) {
+            const bool own = (kbase + j == k0);
+            const float bw = A.gamma + (float)(cur.b[j] - (own ? r0 : 0));
+            const float m1 = own ? m1k0 : a1[j];
+            const float m0 = own ? m0k0 : a0[j];
+            const float w1 = m1 * bw * qv[j].y;
+            const float w0 = m0 * qv[j].x;
+            if constexpr (TRACE) {
+                if (i >= A.tr_begin && i < A.tr_end && kbase + j < A.K) {
+                    float *o = A.tr_w + (i - A.tr_begin) * 2 * (int64_t)A.K + 2 * (kbase + j);
+                    o[0] = w1;
+                    o[1] = w0;
+                }
+            }
+            acc += w1;
+            s[2 * j] = acc;
+            acc += w0;
+            s[2 * j + 1] = acc;
+        }
+        const float incl = wave_inclusive_sum(acc);
+        const float excl = wave_shift_right(incl);
+        const float total = readlane_f(incl, 63);
+
+        const uint32_t xr = philox_x0(opaque_u64(A.seed), (uint64_t)i, A.sweep, kPurposeSample);
+        u = (float)(xr >> 8) * (1.0f / 16777216.0f);
+        const float target = u * total;
+
+        // prefixes are monotone, so the number of this lane's prefixes at or
+        // below the target is the index of its first crossing
+        const float rel = target - excl;
+        int32_t cnt = 0;
+#pragma unroll
+        for (int j = 0; j < NO; ++j) cnt += (s[j] <= rel) ? 1 : 0;
+        const unsigned long long cross = __ballot(cnt < NO);
+        int32_t jstar = -1;
+        bool fix = true;
+        if (cross) {
+            const int32_t L = __ffsll((long long)cross) - 1;
+            const int32_t cL = readlane(cnt, L);
+            // the two prefixes around the crossing; re-decide in fp64 if the
+            // target is within rounding distance of either
+            const float hi = readlane_f(excl + s[cL], L);
+            const float lo = readlane_f(cL > 0 ? excl + s[cL > 0 ? cL - 1 : 0] : excl, L);
+            const float margin = kFixMargin * total;
+            fix = (target - lo < margin) || (hi - target < margin);
+            jstar = L * NO + cL;
+        }
+        if (fix) {
+            // The draw is within rounding distance of a CDF boundary (or the
+            // fp32 scan found no crossing): take it again with fp64 weights
+            // from the integer counts, fp64 prefix sums and the same uniform
+            // (rolled loops re-reading the current rows from memory keep this
+            // rare path from raising the kernel's register count).
+            const int32_t q = readlane(W.gw_c, x);
+            const ExactCtx &X = *A.exact;
+            const int32_t *__restrict__ Ng = X.Ngk + W.gK;
+            const int32_t *__restrict__ Tg = X.Tgk + W.gK;
+            const int32_t *__restrict__ crow = A.nt + (int64_t)q * A.Kp;
+            const int32_t *__restrict__ brow = X.B + (int64_t)(q - W.gV) * A.Kp;
+            double acc64 = 0.0;
+#pragma unroll 1
+            for (int j = 0; j < KPL; ++j) {
+                const int32_t k = kbase + j;
+                if (k >= A.K) break;
+                const Exact e = exact_pair(X, k, k0, r0, crow[k], brow[k], W.c_lds[k], Ng, Tg);
+                acc64 += e.w1;
+                acc64 += e.w0;
+            }
+            double incl64 = acc64;
+#pragma unroll
+            for (int o = 1; o < 64; o <<= 1) {
+                const double y = __shfl_up(incl64, o);
+                if (lane >= o) incl64 += y;
+            }
+            double run = __shfl_up(incl64, 1);
+            if (lane == 0) run = 0.0;
+            const double total64 = __shfl(incl64, 63);
+            const double target64 = (double)u * total64;
+            int32_t cand64 = -1, last64 = -1;
+#pragma unroll 1
+            for (int j = 0; j < KPL; ++j) {
+                const int32_t k = kbase + j;
+                if (k >= A.K) break;
+                const Exact e = exact_pair(X, k, k0, r0, crow[k], brow[k], W.c_lds[k], Ng, Tg);
+                run += e.w1;
+                if (e.w1 > 0.0) {
+                    last64 = 2 * j;
+                    if (cand64 < 0 && run > target64) cand64 = 2 * j;
+                }
+                run += e.w0;
+                if (e.w0 > 0.0) {
+                    last64 = 2 * j + 1;
+                    if (cand64 < 0 && run > target64) cand64 = 2 * j + 1;
+                }
+            }
+            jstar = -1;
+            const unsigned long long m2 = __ballot(cand64 >= 0);
+            if (m2) {
+                const int32_t L = __ffsll((long long)m2) - 1;
+                jstar = L * NO + readlane(cand64, L);
+            } else {
+                const unsigned long long m3 = __ballot(last64 >= 0);
+                if (m3) {
+                    const int32_t L = 63 - __clzll((long long)m3);
+                    jstar = L * NO + readlane(last64, L);
+                }
+            }
+        }
+        if (jstar >= 0) {
+            const int32_t k1 = jstar >> 1, r1 = 1 - (jstar & 1);
+            result = zr_pack(k1, r1);
+            // DS operations of one wave execute in order, so the next token's
+            // reads of the LDS rows see this update
+            if (lane == 0 && k1 != k0) {
+                const int32_t ca = W.c_lds[k0] - 1, cb = W.c_lds[k1] + 1;
+                W.c_lds[k0] = ca;
+                W.c_lds[k1] = cb;
+                const float da = A.alpha + (float)ca, db = A.alpha + (float)cb;
+                W.a0_lds[lds_pos<KPL>(k0)] = da * W.f0_lds[k0];
+                W.a1_lds[lds_pos<KPL>(k0)] = da * W.f1_lds[k0];
+                W.a0_lds[lds_pos<KPL>(k1)] = db * W.f0_lds[k1];
+                W.a1_lds[lds_pos<KPL>(k1)] = db * W.f1_lds[k1];
+            }
+        }
+    }
+    if constexpr (TRACE) {
+        if (lane == 0 && i >= A.tr_begin && i < A.tr_end) A.tr_u[i - A.tr_begin] = u;
+    }
+    if (lane == x) W.out_c = result;
 }
 
 template <int KPL, bool TRACE>
 __global__ void __launch_bounds__(64, (KPL <= 8 ? 4 : 2)) k_sample(SampleArgs A)
 {
-    constexpr int NO = 2 * KPL;  // outcomes per lane
     // live document row c[k], the group's per-topic constants f0, f1 and the
-    // products a0 = (alpha + c) f0, a1 = (alpha + c) f1 (kept in step with c)
+    // products a0 = (alpha + c) f0, a1 = (alpha + c) f1 (kept in step with c;
+    // interleaved layout)
     __shared__ int32_t c_lds[64 * KPL];
     __shared__ float f0_lds[64 * KPL];
     __shared__ float f1_lds[64 * KPL];
@@ -208,19 +494,27 @@ __global__ void __launch_bounds__(64, (KPL <= 8 ? 4 : 2)) k_sample(SampleArgs A)
     const int32_t b = blockIdx.x;
     const int32_t d = (b & 7) * A.docs_per_xcd + (b >> 3);
     if (d >= A.D) return;
-    const int64_t beg = A.doc_off[d], end = A.doc_off[d + 1];
-    if (beg >= end) return;
-    const int32_t lane = threadIdx.x;
+    DocWave<KPL> W;
+    const int64_t beg = A.doc_off[d];
+    W.end = A.doc_off[d + 1];
+    if (beg >= W.end) return;
+    W.lane = threadIdx.x;
     const int32_t g = A.doc_group[d];
-    const int32_t kbase = lane * KPL;
-    const int32_t gV = g * A.V;
-    const int32_t *__restrict__ Ng = A.Ngk + (int64_t)g * A.Kp;
-    const int32_t *__restrict__ Tg = A.Tgk + (int64_t)g * A.Kp;
+    W.kbase = W.lane * KPL;
+    W.gV = g * A.V;
+    W.gK = (int64_t)g * A.Kp;
+    W.c_lds = c_lds;
+    W.f0_lds = f0_lds;
+    W.f1_lds = f1_lds;
+    W.a0_lds = a0_lds;
+    W.a1_lds = a1_lds;
+    const int32_t lane = W.lane, kbase = W.kbase;
+    const int64_t end = W.end, last = end - 1;
 
     {
         float f0[KPL], f1[KPL];
-        load_slice_f<KPL>(f0, A.f0 + (int64_t)g * A.Kp, kbase, A.Kp);
-        load_slice_f<KPL>(f1, A.f1 + (int64_t)g * A.Kp, kbase, A.Kp);
+        load_slice_f<KPL>(f0, A.f0 + W.gK, kbase, A.Kp);
+        load_slice_f<KPL>(f1, A.f1 + W.gK, kbase, A.Kp);
 #pragma unroll
         for (int j = 0; j < KPL; ++j) {
             c_lds[kbase + j] = 0;
@@ -233,231 +527,34 @@ __global__ void __launch_bounds__(64, (KPL <= 8 ? 4 : 2)) k_sample(SampleArgs A)
     __syncthreads();
 #pragma unroll
     for (int j = 0; j < KPL; ++j) {
-        const float doc = A.alpha + (float)c_lds[kbase + j];
-        a0_lds[kbase + j] = doc * f0_lds[kbase + j];
-        a1_lds[kbase + j] = doc * f1_lds[kbase + j];
+        const int32_t k = kbase + j;
+        const float doc = A.alpha + (float)c_lds[k];
+        a0_lds[lds_pos<KPL>(k)] = doc * f0_lds[k];
+        a1_lds[lds_pos<KPL>(k)] = doc * f1_lds[k];
     }
     __syncthreads();
 
-    // token stream: 64 tokens per chunk, lane l holds token base + l
-    int64_t cbase = beg;
-    int32_t gw_c = (beg + lane < end) ? A.gw[beg + lane] : 0;
-    int32_t zr_c = (beg + lane < end) ? A.zr_old[beg + lane] : 0;
-    int32_t gw_n = 0, zr_n = 0;
-    int32_t out_c = 0;
-    const uint32_t q_last = (uint32_t)(A.nQ - 1);
+    W.cb = beg;
+    W.out_c = 0;
+    load_stream<KPL>(A, W, last);
 
-    Slice<KPL> rc, rb;  // packed count row and shadow-base row of the current token
-    {
-        const int32_t q = readlane(gw_c, 0);
-        load_slice<KPL>(rc, A.nt + (int64_t)q * A.Kp, kbase, A.Kp);
-        load_slice<KPL>(rb, A.B + (int64_t)(q - gV) * A.Kp, kbase, A.Kp);
+    // three row buffers: the current token's and the next two tokens'
+    Rows<KPL> ra, rb, rc;
+    load_rows<KPL>(A, W, 0, ra);
+    load_rows<KPL>(A, W, 1, rb);
+    int32_t x = 0;  // position of token i in the stream registers
+    for (int64_t i = beg; i < end; i += 3, x += 3) {
+        if (x == kChunk) {
+            if (lane < kChunk) A.zr_new[W.cb + lane] = W.out_c;
+            W.cb += kChunk;
+            x = 0;
+            load_stream<KPL>(A, W, last);
+        }
+        sample_token<KPL, TRACE>(A, W, x, ra, rc);
+        if (i + 1 < end) sample_token<KPL, TRACE>(A, W, x + 1, rb, ra);
+        if (i + 2 < end) sample_token<KPL, TRACE>(A, W, x + 2, rc, rb);
     }
-
-    for (int64_t i = beg; i < end; ++i) {
-        const int32_t idx = (int32_t)(i - cbase);
-        if (idx == 0 && cbase + 64 < end) {
-            // next chunk of the token stream
-            gw_n = (cbase + 64 + lane < end) ? A.gw[cbase + 64 + lane] : 0;
-            zr_n = (cbase + 64 + lane < end) ? A.zr_old[cbase + 64 + lane] : 0;
-        }
-        const int32_t zr0 = readlane(zr_c, idx);
-        const int32_t k0 = zr0 >> 1, r0 = zr0 & 1;
-        const int32_t q = readlane(gw_c, idx);
-        // the token's own cell and topic totals (uniform loads)
-        const int32_t nt0 = A.nt[(int64_t)q * A.Kp + k0];
-        const int32_t b0 = A.B[(int64_t)(q - gV) * A.Kp + k0];
-        const int32_t N0 = Ng[k0], T0 = Tg[k0], Bk0 = A.Bk[k0];
-        const int32_t n0 = nt0 & kCountMax, t0 = nt0 >> kCountBits;
-        // only head of a cell that keeps other customers: point mass
-        const bool sole = r0 && t0 == 1 && n0 > 1;
-
-        // Stirling ratio pairs of every topic's cell as it stands (the token's
-        // own topic is recomputed below with the token removed); gathered
-        // before the next token's rows are requested
-        float2 qv[KPL];
-#pragma unroll
-        for (int j = 0; j < KPL; ++j) {
-            const uint32_t cn = (uint32_t)rc.v[j] & kCountMax;
-            const uint32_t ct = (uint32_t)rc.v[j] >> kCountBits;
-            uint32_t ix = ((cn * (cn + 1)) >> 1) + ct;
-            ix = ix < q_last ? ix : q_last;
-            qv[j] = A.Q[ix];
-        }
-
-        // next token's rows
-        Slice<KPL> xc, xb;
-        const bool have_next = (i + 1 < end);
-        if (have_next) {
-            const int32_t q1 = (idx + 1 < 64) ? readlane(gw_c, idx + 1) : readlane(gw_n, 0);
-            load_slice<KPL>(xc, A.nt + (int64_t)q1 * A.Kp, kbase, A.Kp);
-            load_slice<KPL>(xb, A.B + (int64_t)(q1 - gV) * A.Kp, kbase, A.Kp);
-        }
-
-        int32_t result = zr0;
-        float u = -1.0f;
-        if (!sole) {
-            // the token's own topic with the token removed: fp64 constants
-            // rounded once, as for the other topics
-            const int32_t n0r = n0 - 1, t0r = t0 - r0;
-            uint32_t ix0 = (uint32_t)(((n0r * (n0r + 1)) >> 1) + t0r);
-            ix0 = ix0 < q_last ? ix0 : q_last;
-            const float2 q0v = A.Q[ix0];
-            const int32_t c0 = c_lds[k0];
-            const double inv = 1.0 / (A.b + (double)(N0 - 1));
-            const float f0k = (float)inv;
-            const float f1k =
-                (float)((A.b + A.a * (double)(T0 - r0)) * inv / (A.Vgamma + (double)(Bk0 - r0)));
-            const float doc0 = A.alpha + (float)(c0 - 1);
-            const float w1k0 = doc0 * f1k * (A.gamma + (float)(b0 - r0)) * q0v.y;
-            const float w0k0 = doc0 * f0k * q0v.x;
-
-            // weights and lane-local inclusive prefix sums
-            float a0[KPL], a1[KPL];
-            lds_slice<KPL>(a0, a0_lds + kbase);
-            lds_slice<KPL>(a1, a1_lds + kbase);
-            float s[NO];
-            float acc = 0.0f;
-#pragma unroll
-            for (int j = 0; j < KPL; ++j) {
-                const bool own = (kbase + j == k0);
-                const float bw = A.gamma + (float)rb.v[j];
-                float w1 = a1[j] * bw * qv[j].y;
-                float w0 = a0[j] * qv[j].x;
-                w1 = own ? w1k0 : w1;
-                w0 = own ? w0k0 : w0;
-                if constexpr (TRACE) {
-                    if (i >= A.tr_begin && i < A.tr_end && kbase + j < A.K) {
-                        float *o = A.tr_w + (i - A.tr_begin) * 2 * (int64_t)A.K + 2 * (kbase + j);
-                        o[0] = w1;
-                        o[1] = w0;
-                    }
-                }
-                acc += w1;
-                s[2 * j] = acc;
-                acc += w0;
-                s[2 * j + 1] = acc;
-            }
-            const float incl = wave_inclusive_sum(acc);
-            const float excl = wave_shift_right(incl);
-            const float total = readlane_f(incl, 63);
-
-            const uint32_t x = philox_x0(A.seed, (uint64_t)i, A.sweep, kPurposeSample);
-            u = (float)(x >> 8) * (1.0f / 16777216.0f);
-            const float target = u * total;
-
-            // count the prefixes at or below the target (prefixes are
-            // monotone, so the first crossing of this lane is outcome cnt) and
-            // flag any prefix within rounding distance of the target
-            const float rel = target - excl;
-            const float margin = kFixMargin * total;
-            int32_t cnt = 0;
-            bool near = false;
-#pragma unroll
-            for (int j = 0; j < NO; ++j) {
-                const float dlt = s[j] - rel;
-                cnt += (dlt <= 0.0f) ? 1 : 0;
-                near |= (fabsf(dlt) < margin);
-            }
-            const unsigned long long cross = __ballot(cnt < NO);
-            int32_t jstar = -1;
-            if (cross && !__any(near)) {
-                const int32_t L = __ffsll((long long)cross) - 1;
-                jstar = L * NO + readlane(cnt, L);
-            } else {
-                // The draw is within rounding distance of a CDF boundary (or the
-                // fp32 scan found no crossing): take it again with fp64 weights
-                // from the integer counts, fp64 prefix sums and the same uniform
-                // (rolled loops re-reading the current rows from memory keep
-                // this rare path from raising the kernel's register count).
-                const int32_t *__restrict__ crow = A.nt + (int64_t)q * A.Kp;
-                const int32_t *__restrict__ brow = A.B + (int64_t)(q - gV) * A.Kp;
-                double acc64 = 0.0;
-#pragma unroll 1
-                for (int j = 0; j < KPL; ++j) {
-                    const int32_t k = kbase + j;
-                    if (k >= A.K) break;
-                    const Exact e = exact_pair<KPL>(A, k, k0, r0, crow[k], brow[k], c_lds[k],
-                                                    Ng, Tg);
-                    acc64 += e.w1;
-                    acc64 += e.w0;
-                }
-                double incl64 = acc64;
-#pragma unroll
-                for (int o = 1; o < 64; o <<= 1) {
-                    const double y = __shfl_up(incl64, o);
-                    if (lane >= o) incl64 += y;
-                }
-                double run = __shfl_up(incl64, 1);
-                if (lane == 0) run = 0.0;
-                const double total64 = __shfl(incl64, 63);
-                const double target64 = (double)u * total64;
-                int32_t cand64 = -1, last64 = -1;
-#pragma unroll 1
-                for (int j = 0; j < KPL; ++j) {
-                    const int32_t k = kbase + j;
-                    if (k >= A.K) break;
-                    const Exact e = exact_pair<KPL>(A, k, k0, r0, crow[k], brow[k], c_lds[k],
-                                                    Ng, Tg);
-                    run += e.w1;
-                    if (e.w1 > 0.0) {
-                        last64 = 2 * j;
-                        if (cand64 < 0 && run > target64) cand64 = 2 * j;
-                    }
-                    run += e.w0;
-                    if (e.w0 > 0.0) {
-                        last64 = 2 * j + 1;
-                        if (cand64 < 0 && run > target64) cand64 = 2 * j + 1;
-                    }
-                }
-                const unsigned long long m2 = __ballot(cand64 >= 0);
-                if (m2) {
-                    const int32_t L = __ffsll((long long)m2) - 1;
-                    jstar = L * NO + readlane(cand64, L);
-                } else {
-                    const unsigned long long m3 = __ballot(last64 >= 0);
-                    if (m3) {
-                        const int32_t L = 63 - __clzll((long long)m3);
-                        jstar = L * NO + readlane(last64, L);
-                    }
-                }
-            }
-            if (jstar >= 0) {
-                const int32_t k1 = jstar >> 1, r1 = 1 - (jstar & 1);
-                result = zr_pack(k1, r1);
-                // DS operations of one wave execute in order, so the next
-                // token's reads of the LDS rows see this update
-                if (lane == 0 && k1 != k0) {
-                    const int32_t ca = c_lds[k0] - 1, cb = c_lds[k1] + 1;
-                    c_lds[k0] = ca;
-                    c_lds[k1] = cb;
-                    const float da = A.alpha + (float)ca, db = A.alpha + (float)cb;
-                    a0_lds[k0] = da * f0_lds[k0];
-                    a1_lds[k0] = da * f1_lds[k0];
-                    a0_lds[k1] = db * f0_lds[k1];
-                    a1_lds[k1] = db * f1_lds[k1];
-                }
-            }
-        }
-        if constexpr (TRACE) {
-            if (lane == 0 && i >= A.tr_begin && i < A.tr_end) A.tr_u[i - A.tr_begin] = u;
-        }
-
-        // buffer the result; write 64 tokens at a time
-        if (lane == idx) out_c = result;
-        if (idx == 63 || i + 1 == end) {
-            if (lane <= idx) A.zr_new[cbase + lane] = out_c;
-        }
-        if (idx == 63) {
-            cbase += 64;
-            gw_c = gw_n;
-            zr_c = zr_n;
-        }
-        if (have_next) {
-            rc = xc;
-            rb = xb;
-        }
-    }
+    if (lane < end - W.cb) A.zr_new[W.cb + lane] = W.out_c;
 }
 
 template <int KPL>
@@ -503,13 +600,11 @@ hipError_t launch_sample(const Model &m, const DeviceBuffers &b, const int32_t *
     A.zr_new = zr_new;
     A.nt = b.nt;
     A.B = b.B;
-    A.Ngk = b.Ngk;
-    A.Tgk = b.Tgk;
-    A.Bk = b.Bk;
     A.f0 = b.f0;
     A.f1 = b.f1;
+    A.fk = b.fk;
     A.Q = b.Q;
-    A.logS = b.logS;
+    A.exact = b.exact;
     A.tr_w = tr_w;
     A.tr_u = tr_u;
     A.tr_begin = tr_begin;
@@ -519,17 +614,12 @@ hipError_t launch_sample(const Model &m, const DeviceBuffers &b, const int32_t *
     A.V = m.V;
     A.K = m.K;
     A.Kp = m.Kp;
-    A.ncap = m.ncap;
     A.nQ = tri_index(m.ncap, 0);
+    A.GK = (int64_t)m.G * m.Kp;
     A.docs_per_xcd = (m.D + 7) / 8;
     A.sweep = sweep;
     A.alpha = (float)m.alpha;
     A.gamma = (float)m.gamma;
-    A.alpha_d = m.alpha;
-    A.gamma_d = m.gamma;
-    A.a = m.a;
-    A.b = m.b;
-    A.Vgamma = (double)m.V * m.gamma;
     const bool trace = (tr_w != nullptr);
     switch (sampler_kpl(m.K)) {
     case 1: return launch_kpl<1>(A, trace, st);

@@ -237,26 +237,40 @@ __global__ void k_topic_tables(int32_t G, int32_t Kp, const int32_t *__restrict_
 }
 
 // ---------------------------------------------------------------- factors
-// f0[g][k] = 1 / (b + N_gk)
-// f1[g][k] = (b + a T_gk) / (b + N_gk) / (V gamma + B_k)
-// computed in fp64 and rounded once; padding topics (k >= K) get 0, so their
-// outcomes carry zero weight.
+// Per-(g, k) constants of the conditionals, computed in fp64 and rounded once:
+//   f0 = 1 / (b + N_gk),   f1 = (b + a T_gk) / (b + N_gk) / (V gamma + B_k)
+// and, for the topic a token is removed from (N >= 1 there),
+//   fk[0] = 1 / (b + N - 1)
+//   fk[1] = (b + a T) / (b + N - 1) / (V gamma + B_k)            (r = 0 removed)
+//   fk[2] = (b + a (T - 1)) / (b + N - 1) / (V gamma + B_k - 1)  (r = 1 removed)
+// Padding topics (k >= K) get 0, so their outcomes carry zero weight.
 __global__ void k_factors(int32_t G, int32_t K, int32_t Kp, double a, double b, double Vgamma,
                           const int32_t *__restrict__ Ngk, const int32_t *__restrict__ Tgk,
                           const int32_t *__restrict__ Bk, float *__restrict__ f0,
-                          float *__restrict__ f1)
+                          float *__restrict__ f1, float *__restrict__ fk)
 {
     const int64_t j = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (j >= (int64_t)G * Kp) return;
+    const int64_t GK = (int64_t)G * Kp;
+    if (j >= GK) return;
     const int32_t k = (int32_t)(j % Kp);
     if (k >= K) {
-        f0[j] = 0.0f;
-        f1[j] = 0.0f;
+        f0[j] = f1[j] = 0.0f;
+        fk[j] = fk[GK + j] = fk[2 * GK + j] = 0.0f;
         return;
     }
-    const double inv = 1.0 / (b + (double)Ngk[j]);
+    const double N = (double)Ngk[j], T = (double)Tgk[j], B = (double)Bk[k];
+    const double inv = 1.0 / (b + N);
     f0[j] = (float)inv;
-    f1[j] = (float)((b + a * (double)Tgk[j]) * inv / (Vgamma + (double)Bk[k]));
+    f1[j] = (float)((b + a * T) * inv / (Vgamma + B));
+    if (Ngk[j] >= 1) {
+        const double invm = 1.0 / (b + N - 1.0);
+        fk[j] = (float)invm;
+        fk[GK + j] = (float)((b + a * T) * invm / (Vgamma + B));
+        fk[2 * GK + j] =
+            Tgk[j] >= 1 ? (float)((b + a * (T - 1.0)) * invm / (Vgamma + B - 1.0)) : 0.0f;
+    } else {
+        fk[j] = fk[GK + j] = fk[2 * GK + j] = 0.0f;
+    }
 }
 
 }  // namespace
@@ -360,7 +374,8 @@ hipError_t launch_factors(const Model &m, const DeviceBuffers &b, hipStream_t st
 {
     const int64_t n = (int64_t)m.G * m.Kp;
     hipLaunchKernelGGL(k_factors, dim3((unsigned)blocks_for(n, kBlock)), dim3(kBlock), 0, st, m.G,
-                       m.K, m.Kp, m.a, m.b, (double)m.V * m.gamma, b.Ngk, b.Tgk, b.Bk, b.f0, b.f1);
+                       m.K, m.Kp, m.a, m.b, (double)m.V * m.gamma, b.Ngk, b.Tgk, b.Bk, b.f0, b.f1,
+                       b.fk);
     return hipGetLastError();
 }
 

@@ -87,6 +87,15 @@ struct Model {
     FastDiv divV;  // q -> g
 };
 
+// Inputs of the sampler's rare fp64 re-decision path, kept in device memory
+// so that they occupy no scalar registers on the common path.
+struct ExactCtx {
+    const int32_t *Ngk, *Tgk, *Bk, *B;
+    const double *logS;
+    double a, b, Vgamma, alpha, gamma;
+    int32_t K, ncap;
+};
+
 struct DeviceBuffers {
     int32_t *gw = nullptr;        // [N]  row index g V + w of each token
     int64_t *doc_off = nullptr;   // [D+1]
@@ -101,6 +110,8 @@ struct DeviceBuffers {
     int32_t *Bk = nullptr;        // [Kp]
     float *f0 = nullptr;          // [G][Kp] 1 / (b + N_gk)
     float *f1 = nullptr;          // [G][Kp] (b + a T_gk) / (b + N_gk) / (V gamma + B_k)
+    float *fk = nullptr;          // [3][G][Kp] the same with one customer removed:
+                                  //   1/(b + N - 1), and f1 for a removed non-head / head
     float2 *Q = nullptr;          // [tri(ncap)] (Q0, Q1) folded Stirling ratios
     double *logS = nullptr;       // [tri(ncap + 1)] log S^n_{t,a}
     double *lfact = nullptr;      // [ncap + 1] log n!
@@ -111,6 +122,7 @@ struct DeviceBuffers {
     int64_t partial_len = 0;
     int32_t *err = nullptr;       // [2] device error flags
     double *scalar = nullptr;     // [1] reduction result
+    ExactCtx *exact = nullptr;    // [1] the sampler's fp64 re-decision inputs
     // debug-conditional buffers (allocated on demand)
     int32_t *zr_dbg = nullptr;
     float *tr_w = nullptr;
