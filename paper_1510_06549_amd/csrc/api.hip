@@ -297,6 +297,8 @@ int spdp_create(const spdp_corpus *corpus, const spdp_groups *groups, int32_t K,
     TRY(dev_alloc(s, &B.zr[1], N, "zr"));
     TRY(dev_alloc(s, &B.nt, rows * m.Kp, "packed customer/table counts"));
     TRY(dev_alloc(s, &B.B, (int64_t)V * m.Kp, "shadow-base table counts"));
+    TRY(dev_alloc(s, &B.B16, (int64_t)V * m.Kp, "16-bit shadow-base table counts"));
+    TRY(dev_alloc(s, &B.wide, 1, "shadow-base width flag"));
     TRY_HIP(launch_fill_i32(B.nt, rows * m.Kp, 0, s->st));
     TRY(dev_alloc(s, &B.Ngk, (int64_t)G * m.Kp, "N_gk"));
     TRY(dev_alloc(s, &B.Tgk, (int64_t)G * m.Kp, "T_gk"));

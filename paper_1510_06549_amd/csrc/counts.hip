@@ -12,7 +12,9 @@
 //               packed cells; then every cell left with customers but no
 //               table promotes the smallest-index token of that cell to table
 //               head (the repair of the parallel pass), and the row is written
-//   k_base      shadow-base table counts B[w][k] = sum_g t[g][w][k]
+//   k_base      shadow-base table counts B[w][k] = sum_g t[g][w][k], and the
+//               16-bit copy the sampler reads (with a flag raised when a count
+//               does not fit, in which case the sampler reads B itself)
 //   k_unpack    export of n and t as separate int32 arrays
 #include <hipcub/hipcub.hpp>
 
@@ -91,16 +93,22 @@ __global__ void __launch_bounds__(64) k_rows(int32_t Kp, const int32_t *__restri
     if (lane == 0) rep_part[q] = rep;
 }
 
-// B[w][k] = sum_g t[g][w][k]
+// B[w][k] = sum_g t[g][w][k];  B16 = min(B, 65535), *wide = 1 if any B > 65535
 __global__ void k_base(int32_t G, int32_t V, int32_t Kp, const int32_t *__restrict__ nt,
-                       int32_t *__restrict__ B)
+                       int32_t *__restrict__ B, uint16_t *__restrict__ B16,
+                       int32_t *__restrict__ wide)
 {
     const int64_t j = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     const int64_t cells = (int64_t)V * Kp;
-    if (j >= cells) return;
-    int32_t s = 0;
-    for (int32_t g = 0; g < G; ++g) s += nt[(int64_t)g * cells + j] >> 16;
-    B[j] = s;
+    bool over = false;
+    if (j < cells) {
+        int32_t s = 0;
+        for (int32_t g = 0; g < G; ++g) s += nt[(int64_t)g * cells + j] >> 16;
+        B[j] = s;
+        over = s > 0xFFFF;
+        B16[j] = (uint16_t)(over ? 0xFFFF : s);
+    }
+    if (__any(over) && (threadIdx.x & 63) == 0) atomicOr(wide, 1);
 }
 
 __global__ void k_unpack(int32_t V, int32_t K, int32_t Kp, const int32_t *__restrict__ nt_g,
@@ -230,8 +238,10 @@ hipError_t launch_rows(const Model &m, const DeviceBuffers &b, int32_t *zr, hipS
 hipError_t launch_base(const Model &m, const DeviceBuffers &b, hipStream_t st)
 {
     const int64_t cells = (int64_t)m.V * m.Kp;
+    hipError_t e = launch_fill_i32(b.wide, 1, 0, st);
+    if (e != hipSuccess) return e;
     hipLaunchKernelGGL(k_base, dim3((unsigned)blocks_for(cells, kBlock)), dim3(kBlock), 0, st, m.G,
-                       m.V, m.Kp, b.nt, b.B);
+                       m.V, m.Kp, b.nt, b.B, b.B16, b.wide);
     return hipGetLastError();
 }
 

@@ -36,6 +36,8 @@ struct SampleArgs {
     int32_t *zr_new;
     const int32_t *nt;
     const int32_t *B;
+    const uint16_t *B16;
+    const int32_t *wide;
     const float *f0;
     const float *f1;
     const float *fk;
@@ -113,6 +115,40 @@ __device__ __forceinline__ void load_row(int32_t (&v)[KPL], const int32_t *__res
     } else {
         static_assert(KPL == 1, "KPL must be 1, 2 or a multiple of 4");
         v[0] = row[kbase < Kp ? kbase : 0];
+    }
+}
+
+// The same for a row of 16-bit counts: this lane's KPL values, two per
+// 32-bit word (low half first), with the same unconditional loads.
+template <int KPL>
+__device__ __forceinline__ void load_half_row(uint32_t (&v)[(KPL + 1) / 2],
+                                              const uint16_t *__restrict__ row, int32_t kbase,
+                                              int32_t Kp)
+{
+    constexpr int NW = KPL / 2;
+    if constexpr (KPL == 1) {
+        v[0] = row[kbase < Kp ? kbase : 0];
+    } else if constexpr (NW % 4 == 0) {
+#pragma unroll
+        for (int c = 0; c < NW / 4; ++c) {
+            const int32_t off = (kbase + 8 * c < Kp) ? kbase + 8 * c : 0;
+            const uint4 x = *reinterpret_cast<const uint4 *>(row + off);
+            v[4 * c + 0] = x.x;
+            v[4 * c + 1] = x.y;
+            v[4 * c + 2] = x.z;
+            v[4 * c + 3] = x.w;
+        }
+    } else if constexpr (NW % 2 == 0) {
+#pragma unroll
+        for (int c = 0; c < NW / 2; ++c) {
+            const int32_t off = (kbase + 4 * c < Kp) ? kbase + 4 * c : 0;
+            const uint2 x = *reinterpret_cast<const uint2 *>(row + off);
+            v[2 * c + 0] = x.x;
+            v[2 * c + 1] = x.y;
+        }
+    } else {
+        static_assert(KPL == 2, "KPL must be 1, 2 or a multiple of 4");
+        v[0] = *reinterpret_cast<const uint32_t *>(row + (kbase < Kp ? kbase : 0));
     }
 }
 
@@ -252,10 +288,16 @@ __device__ __forceinline__ void lds_row(float (&v)[KPL], const float *base, int3
 
 // The rows one token needs: this lane's slices of its packed count row and
 // of its shadow-base row.
-template <int KPL>
+template <int KPL, bool WIDE>
 struct Rows {
+    static constexpr int NB = WIDE ? KPL : (KPL + 1) / 2;
     int32_t n[KPL];
-    int32_t b[KPL];
+    uint32_t bw[NB];  // shadow-base counts: one per word, or two 16-bit ones
+    __device__ __forceinline__ int32_t b(int j) const
+    {
+        if constexpr (WIDE) return (int32_t)bw[j];
+        else return (int32_t)((bw[j >> 1] >> (16 * (j & 1))) & 0xFFFFu);
+    }
 };
 
 // Per-wave state of one document.
@@ -270,13 +312,17 @@ struct DocWave {
     int32_t gw_c, zr_c, out_c;
 };
 
-template <int KPL>
+template <int KPL, bool WIDE>
 __device__ __forceinline__ void load_rows(const SampleArgs &A, const DocWave<KPL> &W, int32_t x,
-                                          Rows<KPL> &R)
+                                          Rows<KPL, WIDE> &R)
 {
     const int32_t q = readlane(W.gw_c, x);
+    const int64_t wrow = (int64_t)(q - W.gV) * A.Kp;
     load_row<KPL>(R.n, A.nt + (int64_t)q * A.Kp, W.kbase, A.Kp);
-    load_row<KPL>(R.b, A.B + (int64_t)(q - W.gV) * A.Kp, W.kbase, A.Kp);
+    if constexpr (WIDE)
+        load_row<KPL>(reinterpret_cast<int32_t(&)[KPL]>(R.bw), A.B + wrow, W.kbase, A.Kp);
+    else
+        load_half_row<KPL>(R.bw, A.B16 + wrow, W.kbase, A.Kp);
 }
 
 // Stream registers of the tokens from W.cb on (lanes past the document's end
@@ -293,9 +339,9 @@ __device__ __forceinline__ void load_stream(const SampleArgs &A, DocWave<KPL> &W
 
 // Token cb + x: sample it with the rows in `cur` and request the rows of the
 // token two places ahead into `fill`.
-template <int KPL, bool TRACE>
+template <int KPL, bool TRACE, bool WIDE>
 __device__ __forceinline__ void sample_token(const SampleArgs &A, DocWave<KPL> &W, int32_t x,
-                                             const Rows<KPL> &cur, Rows<KPL> &fill)
+                                             const Rows<KPL, WIDE> &cur, Rows<KPL, WIDE> &fill)
 {
     constexpr int NO = 2 * KPL;  // outcomes per lane
     const int32_t lane = W.lane, kbase = W.kbase;
@@ -328,7 +374,7 @@ __device__ __forceinline__ void sample_token(const SampleArgs &A, DocWave<KPL> &
     // unused), requested after the gathers so that waiting for the gathers
     // does not wait for them
     asm volatile("" ::: "memory");
-    load_rows<KPL>(A, W, x + 2, fill);
+    load_rows<KPL, WIDE>(A, W, x + 2, fill);
     // only head of a cell that keeps other customers: point mass
     const int32_t nt0 = readlane(own_nt, k0 / KPL);
     const bool sole = r0 && (nt0 >> kCountBits) == 1 && (nt0 & kCountMax) > 1;
@@ -348,7 +394,7 @@ __device__ __forceinline__ void sample_token(const SampleArgs &A, DocWave<KPL> &
 #pragma unroll
         for (int j = 0; j < KPL; ++j) {
             const bool own = (kbase + j == k0);
-            const float bw = A.gamma + (float)(cur.b[j] - (own ? r0 : 0));
+            const float bw = A.gamma + (float)(cur.b(j) - (own ? r0 : 0));
             const float m1 = own ? m1k0 : a1[j];
             const float m0 = own ? m0k0 : a0[j];
             const float w1 = m1 * bw * qv[j].y;
@@ -477,7 +523,9 @@ __device__ __forceinline__ void sample_token(const SampleArgs &A, DocWave<KPL> &
     if (lane == x) W.out_c = result;
 }
 
-template <int KPL, bool TRACE>
+// Launched twice per sweep, once per width of the shadow-base rows; the
+// launch that does not match the flag set by the count rebuild returns.
+template <int KPL, bool TRACE, bool WIDE>
 __global__ void __launch_bounds__(64, (KPL <= 8 ? 4 : 2)) k_sample(SampleArgs A)
 {
     // live document row c[k], the group's per-topic constants f0, f1 and the
@@ -491,6 +539,7 @@ __global__ void __launch_bounds__(64, (KPL <= 8 ? 4 : 2)) k_sample(SampleArgs A)
 
     // blocks are dealt round-robin over the 8 XCDs; give each XCD a
     // contiguous range of documents so a group's hot rows stay in its L2
+    if ((*A.wide != 0) != WIDE) return;
     const int32_t b = blockIdx.x;
     const int32_t d = (b & 7) * A.docs_per_xcd + (b >> 3);
     if (d >= A.D) return;
@@ -539,9 +588,9 @@ __global__ void __launch_bounds__(64, (KPL <= 8 ? 4 : 2)) k_sample(SampleArgs A)
     load_stream<KPL>(A, W, last);
 
     // three row buffers: the current token's and the next two tokens'
-    Rows<KPL> ra, rb, rc;
-    load_rows<KPL>(A, W, 0, ra);
-    load_rows<KPL>(A, W, 1, rb);
+    Rows<KPL, WIDE> ra, rb, rc;
+    load_rows<KPL, WIDE>(A, W, 0, ra);
+    load_rows<KPL, WIDE>(A, W, 1, rb);
     int32_t x = 0;  // position of token i in the stream registers
     for (int64_t i = beg; i < end; i += 3, x += 3) {
         if (x == kChunk) {
@@ -550,9 +599,9 @@ __global__ void __launch_bounds__(64, (KPL <= 8 ? 4 : 2)) k_sample(SampleArgs A)
             x = 0;
             load_stream<KPL>(A, W, last);
         }
-        sample_token<KPL, TRACE>(A, W, x, ra, rc);
-        if (i + 1 < end) sample_token<KPL, TRACE>(A, W, x + 1, rb, ra);
-        if (i + 2 < end) sample_token<KPL, TRACE>(A, W, x + 2, rc, rb);
+        sample_token<KPL, TRACE, WIDE>(A, W, x, ra, rc);
+        if (i + 1 < end) sample_token<KPL, TRACE, WIDE>(A, W, x + 1, rb, ra);
+        if (i + 2 < end) sample_token<KPL, TRACE, WIDE>(A, W, x + 2, rc, rb);
     }
     if (lane < end - W.cb) A.zr_new[W.cb + lane] = W.out_c;
 }
@@ -561,10 +610,13 @@ template <int KPL>
 hipError_t launch_kpl(const SampleArgs &A, bool trace, hipStream_t st)
 {
     const unsigned grid = (unsigned)(8 * A.docs_per_xcd);
-    if (trace)
-        hipLaunchKernelGGL((k_sample<KPL, true>), dim3(grid), dim3(64), 0, st, A);
-    else
-        hipLaunchKernelGGL((k_sample<KPL, false>), dim3(grid), dim3(64), 0, st, A);
+    if (trace) {
+        hipLaunchKernelGGL((k_sample<KPL, true, false>), dim3(grid), dim3(64), 0, st, A);
+        hipLaunchKernelGGL((k_sample<KPL, true, true>), dim3(grid), dim3(64), 0, st, A);
+    } else {
+        hipLaunchKernelGGL((k_sample<KPL, false, false>), dim3(grid), dim3(64), 0, st, A);
+        hipLaunchKernelGGL((k_sample<KPL, false, true>), dim3(grid), dim3(64), 0, st, A);
+    }
     return hipGetLastError();
 }
 
@@ -580,12 +632,9 @@ int sampler_kpl(int32_t K)
     return 16;
 }
 
-int32_t padded_K(int32_t K)
-{
-    const int kpl = sampler_kpl(K);
-    const int align = kpl >= 4 ? 4 : kpl;
-    return (K + align - 1) / align * align;
-}
+// Rows are padded to whole 128-byte lines of int32 cells (so a row read
+// touches no partial line); 64 KPL >= Kp always holds.
+int32_t padded_K(int32_t K) { return (K + 31) / 32 * 32; }
 
 hipError_t launch_sample(const Model &m, const DeviceBuffers &b, const int32_t *zr_old,
                          int32_t *zr_new, uint32_t sweep, uint64_t seed, float *tr_w, float *tr_u,
@@ -600,6 +649,8 @@ hipError_t launch_sample(const Model &m, const DeviceBuffers &b, const int32_t *
     A.zr_new = zr_new;
     A.nt = b.nt;
     A.B = b.B;
+    A.B16 = b.B16;
+    A.wide = b.wide;
     A.f0 = b.f0;
     A.f1 = b.f1;
     A.fk = b.fk;

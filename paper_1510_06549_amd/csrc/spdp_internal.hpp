@@ -103,6 +103,8 @@ struct DeviceBuffers {
     int32_t *zr[2] = {nullptr, nullptr}; // [N] current / next packed state
     int32_t *nt = nullptr;        // [G V][Kp] packed n | t << 16
     int32_t *B = nullptr;         // [V][Kp]   shadow-base table counts
+    uint16_t *B16 = nullptr;      // [V][Kp]   min(B, 65535): the sampler's copy
+    int32_t *wide = nullptr;      // [1] 1 if some B exceeds 65535 (the sampler then reads B)
     int32_t *perm = nullptr;      // [N] tokens sorted by row (stable)
     int32_t *row_off = nullptr;   // [G V + 1] offsets of each row's tokens in perm
     int32_t *Ngk = nullptr;       // [G][Kp]

@@ -106,3 +106,29 @@ def test_invalid_arguments():
                        0.5, 1.0, 0.1)
     with pytest.raises(sp.SpdpError):  # group out of range
         sp.spdp_create(words, off, np.array([1], np.int32), 1, 3, 4, 0.1, 0.5, 1.0, 0.1)
+
+
+def test_shadow_base_counts_beyond_16_bits():
+    """A shadow-base count above 65535 (the sampler then reads the 32-bit
+    shadow-base rows instead of their 16-bit copy): 4 groups each with 16400
+    occurrences of word 0, all seated at their own table of topic 0, give
+    B[0][0] = 65600."""
+    say("shadow-base count beyond 16 bits")
+    rng = np.random.default_rng(7)
+    docs = []
+    for g in range(4):
+        for _ in range(4):
+            d = [0] * 4100 + list(rng.integers(1, 3, size=20))
+            rng.shuffle(d)
+            docs.append((g, d))
+    cp = corpus_from_docs(docs, vocab=3)
+    wl = W(K=3, alpha=0.5, a=0.3, b=50.0, gamma=0.1)
+    s, m = parity.make_pair(cp, wl)
+    z = np.zeros(cp.n_tokens, np.int32)
+    r = np.ones(cp.n_tokens, np.uint8)
+    s.set_assignments(z, r)
+    _, _, B, _ = s.totals()
+    assert B[0, 0] == 65600
+    rep, ch, rp = parity.one_step(s, m, 0, 21)
+    say(f"  {rep}")
+    s.close()
