@@ -31,12 +31,39 @@ def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
-def sample_bytes_per_token(K: int) -> int:
-    """Bytes the sampling step must move per token: the K-cell count row of
-    (group, word) (customers and tables packed in one int32 per cell), the
-    K-entry int32 shadow-base row of the word, and the token stream (row
-    index and state in, state out)."""
-    return 8 * K + 12
+def sample_bytes_per_token(K: int, wide: bool) -> int:
+    """Bytes the sampling kernel must move per token in this library's layout:
+    the K-cell count row of (group, word) (customers and tables packed in one
+    int32 per cell), the K-entry shadow-base row of the word (16-bit counts,
+    or int32 once some count exceeds 65535), and the token stream (row index
+    and state in, state out)."""
+    return 4 * K + (4 if wide else 2) * K + 12
+
+
+def dense_bytes_per_token(K: int) -> int:
+    """The same for separate int32 rows n[g,w,:], t[g,w,:] and B[w,:]."""
+    return 12 * K + 12
+
+
+def recorded_traffic(workload: str):
+    """HBM bytes per k_sample launch measured with rocprofv3 counters, if they
+    were taken on the current sampler source (profiles/traffic_*.txt holds
+    the figure with the SHA-256 of sample.hip at the time), else None."""
+    import hashlib
+
+    path = os.path.join(ROOT, "profiles", f"traffic_k_sample_{workload}.txt")
+    src = os.path.join(ROOT, "paper_1510_06549_amd", "csrc", "sample.hip")
+    if not os.path.exists(path):
+        return None
+    kv = {}
+    for line in open(path):
+        if ":" in line and not line.startswith("#"):
+            k, v = line.split(":", 1)
+            kv[k.strip()] = v.strip()
+    sha = hashlib.sha256(open(src, "rb").read()).hexdigest()
+    if kv.get("sample_hip_sha256") != sha or "bytes_per_launch" not in kv:
+        return None
+    return float(kv["bytes_per_launch"])
 
 
 def cpu_baseline(cp, wl, z, r, target_s: float):
@@ -133,6 +160,8 @@ def main():
         s.sweep(w, seed)
     torch.cuda.synchronize()
     log(f"[bench] {args.warmup} warm-up sweep(s) done")
+    # width of the shadow-base rows the timed sweeps read (set by each rebuild)
+    wide = bool(s.totals()[2].max() > 0xFFFF)
 
     sp.spdp_kernel_timing(s.h, True)
     torch.cuda.synchronize()
@@ -144,6 +173,7 @@ def main():
     kt = sp.spdp_kernel_times(s.h)
     sp.spdp_kernel_timing(s.h, False)
     changed, repaired = s.stats()
+    wide = wide or bool(s.totals()[2].max() > 0xFFFF)
     log(f"[bench] {args.steps} timed sweeps in {elapsed:.3f}s; kernel ms {kt}; "
         f"last sweep changed={changed} repaired={repaired}")
 
@@ -152,8 +182,9 @@ def main():
     value = N * args.steps / elapsed
     ms_sample, n_sample = kt["sample"]
     avg_sample_s = ms_sample / 1000.0 / max(n_sample, 1)
-    alg = N * sample_bytes_per_token(wl.K)
+    alg = N * sample_bytes_per_token(wl.K, wide)
     achieved = alg / avg_sample_s / 1e9
+    traffic = recorded_traffic(wl.name)
     roofline = {
         "bound": "hbm",
         "kernel": "k_sample",
@@ -161,8 +192,13 @@ def main():
         "peak": HBM_PEAK_GBS,
         "unit": "GB/s",
         "frac": round(achieved / HBM_PEAK_GBS, 4),
-        "traffic": None,
-        "bytes_per_token": sample_bytes_per_token(wl.K),
+        "traffic": None if traffic is None else round(traffic / 1e9, 3),
+        "traffic_unit": "GB per launch",
+        "alg_bytes_per_launch_GB": round(alg / 1e9, 3),
+        "bytes_per_token": sample_bytes_per_token(wl.K, wide),
+        "shadow_base_bits": 32 if wide else 16,
+        "dense_int32_bytes_per_token": dense_bytes_per_token(wl.K),
+        "dense_int32_equiv_GBps": round(N * dense_bytes_per_token(wl.K) / avg_sample_s / 1e9, 1),
         "avg_launch_ms": round(avg_sample_s * 1000.0, 3),
     }
 
