@@ -172,16 +172,6 @@ __device__ __forceinline__ float readlane_f(float x, int32_t lane)
     return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(x), lane));
 }
 
-// Hides a uniform value from loop-invariant hoisting: the Philox round keys
-// are then derived per token with scalar adds instead of being held (and
-// spilled) across the token loop.
-__device__ __forceinline__ uint64_t opaque_u64(uint64_t x)
-{
-    uint32_t lo = (uint32_t)x, hi = (uint32_t)(x >> 32);
-    asm volatile("" : "+s"(lo), "+s"(hi));
-    return ((uint64_t)hi << 32) | lo;
-}
-
 // Marks a wave-uniform offset as per-lane, so that the load using it is a
 // vector load: vector loads complete in issue order on one counter, which
 // lets a load issued two tokens ahead be waited for without waiting for the
@@ -307,9 +297,10 @@ struct DocWave {
     int64_t gK, cb, end;
     int32_t *c_lds;
     float *f0_lds, *f1_lds, *a0_lds, *a1_lds;
-    // token stream: lane l holds (row index, packed state) of token cb + l,
-    // lanes past the document's end repeat its last token
+    // token stream: lane l holds the row index, packed state and uniform of
+    // token cb + l (lanes past the document's end repeat its last token)
     int32_t gw_c, zr_c, out_c;
+    float u_c;
 };
 
 template <int KPL, bool WIDE>
@@ -326,14 +317,18 @@ __device__ __forceinline__ void load_rows(const SampleArgs &A, const DocWave<KPL
 }
 
 // Stream registers of the tokens from W.cb on (lanes past the document's end
-// repeat its last token).  They are waited for here, once per 48 tokens, so
-// that no token's wait on its prefetched rows has to cover them.
+// repeat its last token), and the tokens' uniforms: Philox word 0 at counter
+// (token lo, token hi, sweep, 0), one token per lane, so the rounds run on the
+// vector unit once per 48 tokens.  The loads are waited for here, so that no
+// token's wait on its prefetched rows has to cover them.
 template <int KPL>
 __device__ __forceinline__ void load_stream(const SampleArgs &A, DocWave<KPL> &W, int64_t last)
 {
     const int64_t t = min(W.cb + W.lane, last);
     W.gw_c = A.gw[t];
     W.zr_c = A.zr_old[t];
+    const uint32_t xr = philox_x0(A.seed, (uint64_t)(W.cb + W.lane), A.sweep, kPurposeSample);
+    W.u_c = (float)(xr >> 8) * (1.0f / 16777216.0f);
     asm volatile("" ::"v"(W.gw_c), "v"(W.zr_c));
 }
 
@@ -364,7 +359,8 @@ __device__ __forceinline__ void sample_token(const SampleArgs &A, DocWave<KPL> &
         const uint32_t cn = v & kCountMax, ct = v >> kCountBits;
         uint32_t ix = ((cn * (cn + 1)) >> 1) + ct;
         ix = ix < q_last ? ix : q_last;
-        qv[j] = A.Q[ix];
+        // (byte offsets fit in 32 bits: the ratio table is below 4 GiB)
+        qv[j] = *reinterpret_cast<const float2 *>(reinterpret_cast<const char *>(A.Q) + (ix << 3));
     }
     // removed-customer constants of the own topic (a small table that stays
     // in cache; requested with the gathers)
@@ -415,8 +411,7 @@ __device__ __forceinline__ void sample_token(const SampleArgs &A, DocWave<KPL> &
         const float excl = wave_shift_right(incl);
         const float total = readlane_f(incl, 63);
 
-        const uint32_t xr = philox_x0(opaque_u64(A.seed), (uint64_t)i, A.sweep, kPurposeSample);
-        u = (float)(xr >> 8) * (1.0f / 16777216.0f);
+        u = readlane_f(W.u_c, x);
         const float target = u * total;
 
         // prefixes are monotone, so the number of this lane's prefixes at or
