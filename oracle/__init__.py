@@ -105,6 +105,10 @@ def lib():
         L.or_chain_histogram.restype = C.c_int
         L.or_num_threads.argtypes = []
         L.or_num_threads.restype = C.c_int
+        L.or_estimates.argtypes = [vp, vp, vp, vp, vp, vp]
+        L.or_estimates.restype = None
+        L.or_heldout.argtypes = [vp, vp, i32, vp, vp, vp, i32, u64, vp, vp]
+        L.or_heldout.restype = dbl
         _lib = L
     return _lib
 
@@ -250,6 +254,35 @@ class Model:
 
     def loglik(self, z, r, counts: "Counts") -> float:
         return float(lib().or_loglik(self.ref, _p(z), _p(r), counts.ref))
+
+    def estimates(self, z, counts: "Counts"):
+        """Point estimates (theta [D, K], phi0 [K, V], phig [G, K, V]) of a state."""
+        theta = np.zeros((self.D, self.K), dtype=np.float64)
+        phi0 = np.zeros((self.K, self.V), dtype=np.float64)
+        phig = np.zeros((self.G, self.K, self.V), dtype=np.float64)
+        lib().or_estimates(self.ref, _p(np.ascontiguousarray(z, dtype=np.int32)), counts.ref,
+                           _p(theta), _p(phi0), _p(phig))
+        return theta, phi0, phig
+
+    def heldout(self, phig, words, doc_off, doc_group, n_sweeps: int, seed: int):
+        """Fold-in of held-out documents with phi fixed at `phig` [G, K, V].
+
+        Returns (sum of log p(w_d), final topics z [N_test], log p per document).
+        """
+        phig = np.ascontiguousarray(phig, dtype=np.float64)
+        assert phig.shape == (self.G, self.K, self.V)
+        words = np.ascontiguousarray(words, dtype=np.int32)
+        doc_off = np.ascontiguousarray(doc_off, dtype=np.int64)
+        doc_group = np.ascontiguousarray(doc_group, dtype=np.int32)
+        D = int(doc_group.shape[0])
+        assert doc_off.shape[0] == D + 1 and doc_off[-1] == words.shape[0]
+        assert words.size == 0 or (words.min() >= 0 and words.max() < self.V)
+        assert D == 0 or (doc_group.min() >= 0 and doc_group.max() < self.G)
+        z = np.zeros(words.shape[0], dtype=np.int32)
+        ll_doc = np.zeros(D, dtype=np.float64)
+        total = lib().or_heldout(self.ref, _p(phig), D, _p(words), _p(doc_off), _p(doc_group),
+                                 int(n_sweeps), int(seed) & (2**64 - 1), _p(z), _p(ll_doc))
+        return float(total), z, ll_doc
 
 
 class Counts:

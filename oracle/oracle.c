@@ -50,6 +50,7 @@
 
 #define OR_PURPOSE_SAMPLE 0u
 #define OR_PURPOSE_INIT 1u
+/* (purposes 2 and 3 are the held-out fold-in, defined with it below) */
 
 /* ------------------------------------------------------------------------ */
 /* Model description.  All arrays are owned by the caller.                   */
@@ -513,4 +514,129 @@ int or_chain_histogram(const or_model *m, or_counts *c, int32_t *z, uint8_t *r,
         hist[code] += 1;
     }
     return 0;
+}
+
+/* ------------------------------------------------------------------------ */
+/* Point estimates of a state (thesis: estimates after convergence,         */
+/* Eq. spdp-topic-doc-estimate, Eq. spdp-word-topic-estimate and            */
+/* Eq. spdp-group-word-topic-estimate, with P = I so that q = t):            */
+/*   theta[d][k] = (c_dk + alpha) / (L_d + K alpha)                          */
+/*   phi0[k][w]  = (gamma + B_kw) / (V gamma + B_k)                          */
+/*   phig[g][k][w] = (n - a t + (b + a T_gk) phi0[k][w]) / (b + N_gk)        */
+/* The printed group estimate weights the base by a T / (b + N), which sums */
+/* over words to N / (b + N); the Pitman-Yor posterior predictive (a new    */
+/* customer joins a table serving w with weight n_w - a t_w, or opens a new */
+/* table with weight b + a T and takes its dish from the base) weights it   */
+/* by (b + a T) / (b + N), which sums to one: that is the reading here.     */
+/* Any output pointer may be NULL.                                           */
+/* ------------------------------------------------------------------------ */
+void or_estimates(const or_model *m, const int32_t *z, const or_counts *c, double *theta,
+                  double *phi0, double *phig)
+{
+    const int64_t G = m->n_groups, K = m->K, V = m->vocab;
+    if (theta) {
+        for (int32_t d = 0; d < m->n_docs; ++d) {
+            double *row = theta + (int64_t)d * K;
+            for (int64_t k = 0; k < K; ++k) row[k] = 0.0;
+            for (int64_t i = m->doc_off[d]; i < m->doc_off[d + 1]; ++i) row[z[i]] += 1.0;
+            const double len = (double)(m->doc_off[d + 1] - m->doc_off[d]);
+            for (int64_t k = 0; k < K; ++k)
+                row[k] = (row[k] + m->alpha) / (len + (double)K * m->alpha);
+        }
+    }
+    double *p0 = phi0 ? phi0 : (phig ? (double *)malloc(sizeof(double) * (size_t)(K * V)) : NULL);
+    if (p0) {
+        for (int64_t k = 0; k < K; ++k)
+            for (int64_t w = 0; w < V; ++w)
+                p0[k * V + w] = (m->gam + (double)c->Bkw[k * V + w]) /
+                                ((double)V * m->gam + (double)c->Bk[k]);
+    }
+    if (phig) {
+        for (int64_t g = 0; g < G; ++g)
+            for (int64_t k = 0; k < K; ++k) {
+                const double N = (double)c->Ngk[g * K + k], T = (double)c->Tgk[g * K + k];
+                for (int64_t w = 0; w < V; ++w) {
+                    const int64_t cell = (g * K + k) * V + w;
+                    phig[cell] = ((double)c->n[cell] - m->a * (double)c->t[cell] +
+                                  (m->b + m->a * T) * p0[k * V + w]) /
+                                 (m->b + N);
+                }
+            }
+    }
+    if (p0 && !phi0) free(p0);
+}
+
+/* ------------------------------------------------------------------------ */
+/* Held-out documents (thesis, section "Perplexity": documents held out per  */
+/* group; p(w_d | rest) = prod_n sum_k phi^i_{k,w_n} theta_{d,k}).  The      */
+/* thesis leaves open how a held-out document's theta is obtained; reading: */
+/* fold-in (query sampling) with phi fixed at the point estimate phig of    */
+/* the training state:                                                      */
+/*   1. z_n drawn uniformly: first Philox word with purpose FOLDIN_INIT (3), */
+/*      counter (test token n, 0), times K, high 32 bits;                    */
+/*   2. n_sweeps Gibbs sweeps, each over the document's tokens in order:     */
+/*      p(z_n = k | rest) proportional to (c_k without n + alpha) phig[g][k][w_n], */
+/*      u from Philox purpose FOLDIN (2) at counter (n, sweep), first k     */
+/*      whose inclusive prefix sum exceeds u * total;                        */
+/*   3. theta_k = (c_k + alpha) / (L + K alpha) from the final counts, and   */
+/*      log p(w_d) = sum_n log sum_k phig[g][k][w_n] theta_k.                */
+/* Documents are independent (any order, in parallel).  The test corpus has */
+/* its own token numbering.  z_out [N_test] receives the final topics;       */
+/* ll_doc [D_test] the per-document log p (either may be NULL).  Returns the */
+/* sum of log p over documents, added in document order.                     */
+/* ------------------------------------------------------------------------ */
+#define OR_PURPOSE_FOLDIN 2u
+#define OR_PURPOSE_FOLDIN_INIT 3u
+
+double or_heldout(const or_model *m, const double *phig, int32_t d_test, const int32_t *words,
+                  const int64_t *doc_off, const int32_t *doc_group, int32_t n_sweeps,
+                  uint64_t seed, int32_t *z_out, double *ll_doc)
+{
+    const int64_t K = m->K, V = m->vocab;
+    double *lld = ll_doc ? ll_doc : (double *)malloc(sizeof(double) * (size_t)(d_test > 0 ? d_test : 1));
+    int32_t *zz = z_out ? z_out : (int32_t *)malloc(sizeof(int32_t) * (size_t)(doc_off[d_test] > 0 ? doc_off[d_test] : 1));
+#pragma omp parallel
+    {
+        int64_t *c = (int64_t *)malloc(sizeof(int64_t) * (size_t)K);
+        double *w = (double *)malloc(sizeof(double) * (size_t)K);
+#pragma omp for schedule(dynamic, 16)
+        for (int32_t d = 0; d < d_test; ++d) {
+            const int64_t g = doc_group[d], beg = doc_off[d], end = doc_off[d + 1];
+            const double *ph = phig + g * K * V;
+            for (int64_t k = 0; k < K; ++k) c[k] = 0;
+            for (int64_t i = beg; i < end; ++i) {
+                const uint32_t x = or_philox_word0(seed, i, 0u, OR_PURPOSE_FOLDIN_INIT);
+                zz[i] = (int32_t)(((uint64_t)x * (uint64_t)K) >> 32);
+                c[zz[i]] += 1;
+            }
+            for (int32_t s = 0; s < n_sweeps; ++s) {
+                for (int64_t i = beg; i < end; ++i) {
+                    c[zz[i]] -= 1;
+                    for (int64_t k = 0; k < K; ++k)
+                        w[k] = ((double)c[k] + m->alpha) * ph[k * V + words[i]];
+                    const uint32_t x = or_philox_word0(seed, i, (uint32_t)s, OR_PURPOSE_FOLDIN);
+                    const double u = (double)(x >> 8) * (1.0 / 16777216.0);
+                    const int k1 = draw_outcome(w, K, u);
+                    zz[i] = k1;
+                    c[k1] += 1;
+                }
+            }
+            const double len = (double)(end - beg);
+            double ll = 0.0;
+            for (int64_t i = beg; i < end; ++i) {
+                double p = 0.0;
+                for (int64_t k = 0; k < K; ++k)
+                    p += ph[k * V + words[i]] * ((double)c[k] + m->alpha) / (len + (double)K * m->alpha);
+                ll += log(p);
+            }
+            lld[d] = ll;
+        }
+        free(c);
+        free(w);
+    }
+    double total = 0.0;
+    for (int32_t d = 0; d < d_test; ++d) total += lld[d];
+    if (!ll_doc) free(lld);
+    if (!z_out) free(zz);
+    return total;
 }
