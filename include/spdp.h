@@ -134,6 +134,42 @@ int spdp_loglik(spdp_state *s, double *out);
 void spdp_destroy(spdp_state *s);
 
 /*
+ * Point estimates of the current state (the thesis's estimates after
+ * convergence: Eq. spdp-topic-doc-estimate, Eq. spdp-word-topic-estimate and
+ * Eq. spdp-group-word-topic-estimate, with P = I), in fp64:
+ *   theta [D][K]   theta[d][k] = (c_dk + alpha) / (L_d + K alpha)
+ *   phi0  [V][K]   phi0[w][k]  = (gamma + B_wk) / (V gamma + B_k)
+ *   phi   [g_end - g_begin][V][K]
+ *                  phi[g][w][k] = (n - a t + (b + a T_gk) phi0[w][k]) / (b + N_gk)
+ * (the base weight b + a T is the Pitman-Yor seating rule's; the printed
+ * a T does not normalise).  Any pointer may be NULL; the group range applies
+ * to phi only.  `where` as for spdp_counts.  Synchronises.
+ * Errors: E_ARG (bad range), E_HIP.
+ */
+int spdp_estimates(spdp_state *s, int32_t g_begin, int32_t g_end, double *theta, double *phi0,
+                   double *phi, int where);
+
+/*
+ * Held-out perplexity (section "Perplexity") of test documents given as their
+ * own corpus (same vocabulary; `init_seed` and `hip_stream` are not used) and
+ * groups (same n_groups).  Each test document is folded in with phi fixed at
+ * the group estimate of the current state: topics drawn uniformly (first
+ * Philox word keyed by `seed` with purpose 3 at counter (test token, 0), times
+ * K, high 32 bits), then n_sweeps Gibbs sweeps over its tokens in order with
+ * p(z_n = k | rest) proportional to (c_k without token n + alpha) phi[g][w_n][k]
+ * (uniform: purpose 2 at counter (test token, sweep); first k whose prefix
+ * exceeds u * total); then log p(w_d) = sum_n log sum_k phi[g][w_n][k]
+ * theta_d[k] with theta_d from the final counts, in fp64.
+ * out2[0] = perplexity exp(-sum_d log p(w_d) / N_test) (NaN if N_test = 0),
+ * out2[1] = sum_d log p(w_d) (host pointer).  z_out [N_test] int32 receives
+ * the final fold-in topics (may be NULL; `where` applies to it).  The state
+ * is not changed.  Synchronises.
+ * Errors: E_ARG (sizes, vocabulary or groups differ, ids out of range), E_HIP.
+ */
+int spdp_heldout(spdp_state *s, const spdp_corpus *test, const spdp_groups *test_groups,
+                 int32_t n_sweeps, uint64_t seed, double *out2, int32_t *z_out, int where);
+
+/*
  * Checkpoint: export z [N] int32 and r [N] uint8 (either may be NULL).
  * Synchronises.  Errors: E_ARG, E_HIP.
  */

@@ -433,6 +433,110 @@ int spdp_loglik(spdp_state *s, double *out)
     return SPDP_OK;
 }
 
+int spdp_estimates(spdp_state *s, int32_t g_begin, int32_t g_end, double *theta, double *phi0,
+                   double *phi, int where)
+{
+    if (!s) return fail(SPDP_E_ARG, "state is NULL");
+    const Model &m = s->m;
+    if (where != 0 && where != 1) return fail(SPDP_E_ARG, "where must be 0 or 1");
+    if (phi && (g_begin < 0 || g_end > m.G || g_begin > g_end))
+        return fail(SPDP_E_ARG, "bad group range");
+    HIP_TRY(hipSetDevice(s->device));
+    const int64_t vk = (int64_t)m.V * m.K, dk = (int64_t)m.D * m.K;
+    // device destinations (the caller's buffers, or one staging buffer reused)
+    double *stage = nullptr;
+    if (where == 0) {
+        int64_t need = 0;
+        if (theta) need = dk;
+        if ((phi0 || phi) && vk > need) need = vk;
+        if (need > 0) HIP_TRY(hipMalloc(&stage, (size_t)need * sizeof(double)));
+    }
+    hipError_t e = hipSuccess;
+    auto out = [&](double *dst, int64_t n, auto &&launch) {
+        if (e != hipSuccess || !dst || n <= 0) return;
+        e = launch(where ? dst : stage);
+        if (e == hipSuccess && where == 0)
+            e = hipMemcpyAsync(dst, stage, (size_t)n * sizeof(double), hipMemcpyDeviceToHost,
+                               s->st);
+        if (e == hipSuccess && where == 0) e = hipStreamSynchronize(s->st);
+    };
+    out(theta, dk, [&](double *d) { return launch_theta(m, s->b, s->b.zr[s->cur], d, s->st); });
+    out(phi0, vk, [&](double *d) { return launch_phi0(m, s->b, d, s->st); });
+    for (int32_t g = g_begin; phi && g < g_end; ++g)
+        out(phi + (int64_t)(g - g_begin) * vk, vk,
+            [&](double *d) { return launch_phig(m, s->b, g, d, s->st); });
+    if (stage) hipFree(stage);
+    HIP_TRY(e);
+    return sync(s);
+}
+
+int spdp_heldout(spdp_state *s, const spdp_corpus *test, const spdp_groups *test_groups,
+                 int32_t n_sweeps, uint64_t seed, double *out2, int32_t *z_out, int where)
+{
+    if (!s || !test || !test_groups || !out2) return fail(SPDP_E_ARG, "null argument");
+    const Model &m = s->m;
+    if (where != 0 && where != 1) return fail(SPDP_E_ARG, "where must be 0 or 1");
+    if (n_sweeps < 0) return fail(SPDP_E_ARG, "n_sweeps < 0");
+    const int64_t N = test->n_tokens;
+    const int32_t D = test->n_docs;
+    if (N < 0 || N >= (1ll << 31) || D < 0) return fail(SPDP_E_ARG, "bad test corpus size");
+    if (test->vocab != m.V) return fail(SPDP_E_ARG, "test vocabulary differs from the state's");
+    if (test_groups->n_groups != m.G) return fail(SPDP_E_ARG, "test groups differ from the state's");
+    if ((N > 0 && !test->words) || !test->doc_offsets || (D > 0 && !test_groups->doc_group))
+        return fail(SPDP_E_ARG, "null test array");
+    if (test->doc_offsets[0] != 0 || test->doc_offsets[D] != N)
+        return fail(SPDP_E_ARG, "test doc_offsets must run from 0 to n_tokens");
+    std::vector<int32_t> gw((size_t)(N > 0 ? N : 1));
+    for (int32_t d = 0; d < D; ++d) {
+        const int64_t b0 = test->doc_offsets[d], b1 = test->doc_offsets[d + 1];
+        const int32_t g = test_groups->doc_group[d];
+        if (b1 < b0) return fail(SPDP_E_ARG, "test doc_offsets decrease");
+        if (g < 0 || g >= m.G) return fail(SPDP_E_ARG, "test doc_group out of [0, n_groups)");
+        for (int64_t i = b0; i < b1; ++i) {
+            const int32_t w = test->words[i];
+            if (w < 0 || w >= m.V) return fail(SPDP_E_ARG, "test word id out of [0, vocab)");
+            gw[(size_t)i] = g * m.V + w;
+        }
+    }
+    HIP_TRY(hipSetDevice(s->device));
+    int32_t *gw_d = nullptr, *grp_d = nullptr, *z_d = nullptr;
+    int64_t *off_d = nullptr;
+    double *ll_d = nullptr;
+    hipError_t e = hipMalloc(&gw_d, (size_t)(N > 0 ? N : 1) * 4);
+    if (e == hipSuccess) e = hipMalloc(&z_d, (size_t)(N > 0 ? N : 1) * 4);
+    if (e == hipSuccess) e = hipMalloc(&off_d, (size_t)(D + 1) * 8);
+    if (e == hipSuccess) e = hipMalloc(&grp_d, (size_t)(D > 0 ? D : 1) * 4);
+    if (e == hipSuccess) e = hipMalloc(&ll_d, (size_t)(D > 0 ? D : 1) * 8);
+    if (e == hipSuccess && N > 0)
+        e = hipMemcpyAsync(gw_d, gw.data(), (size_t)N * 4, hipMemcpyHostToDevice, s->st);
+    if (e == hipSuccess)
+        e = hipMemcpyAsync(off_d, test->doc_offsets, (size_t)(D + 1) * 8, hipMemcpyHostToDevice,
+                           s->st);
+    if (e == hipSuccess && D > 0)
+        e = hipMemcpyAsync(grp_d, test_groups->doc_group, (size_t)D * 4, hipMemcpyHostToDevice,
+                           s->st);
+    if (e == hipSuccess)
+        e = launch_foldin(m, s->b, D, gw_d, off_d, grp_d, n_sweeps, seed, z_d, ll_d, s->st);
+    std::vector<double> ll((size_t)(D > 0 ? D : 1), 0.0);
+    if (e == hipSuccess && D > 0)
+        e = hipMemcpyAsync(ll.data(), ll_d, (size_t)D * 8, hipMemcpyDeviceToHost, s->st);
+    if (e == hipSuccess && z_out && N > 0)
+        e = hipMemcpyAsync(z_out, z_d, (size_t)N * 4,
+                           where ? hipMemcpyDeviceToDevice : hipMemcpyDeviceToHost, s->st);
+    if (e == hipSuccess) e = hipStreamSynchronize(s->st);
+    hipFree(gw_d);
+    hipFree(z_d);
+    hipFree(off_d);
+    hipFree(grp_d);
+    hipFree(ll_d);
+    HIP_TRY(e);
+    double total = 0.0;  // documents in order
+    for (int32_t d = 0; d < D; ++d) total += ll[(size_t)d];
+    out2[0] = N > 0 ? exp(-total / (double)N) : NAN;
+    out2[1] = total;
+    return SPDP_OK;
+}
+
 int spdp_get_assignments(const spdp_state *s, int32_t *z, uint8_t *r, int where)
 {
     if (!s) return fail(SPDP_E_ARG, "state is NULL");

@@ -167,6 +167,16 @@ hipError_t launch_loglik(const Model &m, const DeviceBuffers &b, const int32_t *
                          hipStream_t st);
 int64_t loglik_partials_needed();
 
+hipError_t launch_theta(const Model &m, const DeviceBuffers &b, const int32_t *zr, double *theta,
+                        hipStream_t st);
+hipError_t launch_phi0(const Model &m, const DeviceBuffers &b, double *phi0, hipStream_t st);
+hipError_t launch_phig(const Model &m, const DeviceBuffers &b, int32_t g, double *phi,
+                       hipStream_t st);
+hipError_t launch_foldin(const Model &m, const DeviceBuffers &b, int32_t D_test,
+                         const int32_t *gw, const int64_t *doc_off, const int32_t *doc_group,
+                         int32_t n_sweeps, uint64_t seed, int32_t *z, double *ll_doc,
+                         hipStream_t st);
+
 // The sampler's per-lane topic count for K topics (4 at most per dwordx4).
 int sampler_kpl(int32_t K);
 int32_t padded_K(int32_t K);

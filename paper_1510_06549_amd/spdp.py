@@ -30,6 +30,7 @@ EXPORTS = (
     "spdp_create", "spdp_sweep", "spdp_counts", "spdp_totals", "spdp_loglik", "spdp_destroy",
     "spdp_get_assignments", "spdp_set_assignments", "spdp_debug_conditionals", "spdp_stats",
     "spdp_kernel_timing", "spdp_kernel_times", "spdp_info", "spdp_last_error",
+    "spdp_estimates", "spdp_heldout",
 )
 
 
@@ -91,6 +92,10 @@ def load_library() -> C.CDLL:
     L.spdp_info.restype = cint
     L.spdp_last_error.argtypes = []
     L.spdp_last_error.restype = C.c_char_p
+    L.spdp_estimates.argtypes = [vp, i32, i32, vp, vp, vp, cint]
+    L.spdp_estimates.restype = cint
+    L.spdp_heldout.argtypes = [vp, vp, vp, i32, u64, vp, vp, cint]
+    L.spdp_heldout.restype = cint
     return L
 
 
@@ -220,6 +225,27 @@ def spdp_info(h) -> dict:
     return {k: int(v) for k, v in zip(keys, out)}
 
 
+def spdp_estimates(h, g_begin, g_end, theta=None, phi0=None, phi=None):
+    where = _where(theta, phi0, phi)
+    _check(lib().spdp_estimates(h, int(g_begin), int(g_end), _buf(theta)[0], _buf(phi0)[0],
+                                _buf(phi)[0], where))
+
+
+def spdp_heldout(h, words, doc_offsets, doc_group, n_groups, vocab, n_sweeps, seed, z_out=None):
+    """(perplexity, sum of log p) of held-out documents; see include/spdp.h."""
+    words = np.ascontiguousarray(words, dtype=np.int32)
+    doc_offsets = np.ascontiguousarray(doc_offsets, dtype=np.int64)
+    doc_group = np.ascontiguousarray(doc_group, dtype=np.int32)
+    corpus = _Corpus(int(words.shape[0]), int(doc_group.shape[0]), int(vocab), words.ctypes.data,
+                     doc_offsets.ctypes.data, 0, None)
+    groups = _Groups(int(n_groups), doc_group.ctypes.data)
+    out = np.zeros(2, dtype=np.float64)
+    where = _where(z_out)
+    _check(lib().spdp_heldout(h, C.byref(corpus), C.byref(groups), int(n_sweeps),
+                              int(seed) & (2**64 - 1), out.ctypes.data, _buf(z_out)[0], where))
+    return float(out[0]), float(out[1])
+
+
 # ---------------------------------------------------------------------------
 # Convenience wrapper (host numpy in and out)
 # ---------------------------------------------------------------------------
@@ -293,3 +319,19 @@ class Sampler:
 
     def stats(self):
         return spdp_stats(self.h)
+
+    def estimates(self, g_begin=0, g_end=None):
+        """(theta [D, K], phi0 [V, K], phi [g, V, K]) in fp64."""
+        g_end = self.G if g_end is None else g_end
+        theta = np.empty((self.info["D"], self.K), dtype=np.float64)
+        phi0 = np.empty((self.V, self.K), dtype=np.float64)
+        phi = np.empty((g_end - g_begin, self.V, self.K), dtype=np.float64)
+        spdp_estimates(self.h, g_begin, g_end, theta, phi0, phi)
+        return theta, phi0, phi
+
+    def heldout(self, words, doc_offsets, doc_group, n_sweeps, seed):
+        """(perplexity, sum of log p, fold-in topics) of held-out documents."""
+        z = np.empty(len(words), dtype=np.int32)
+        ppl, ll = spdp_heldout(self.h, words, doc_offsets, doc_group, self.G, self.V, n_sweeps,
+                               seed, z)
+        return ppl, ll, z

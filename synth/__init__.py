@@ -143,3 +143,28 @@ def generate(w: Workload, seed: int = 0) -> Corpus:
         raise MemoryError("synth_fill failed")
     doc_group = (np.arange(D, dtype=np.int64) // w.docs_per_group).astype(np.int32)
     return Corpus(words, doc_off, doc_group, z, r, w.n_groups, w.vocab)
+
+
+def split_heldout(cp: Corpus, frac: float = 0.1):
+    """(train, test): the last floor(frac * docs) documents of every group held out,
+    as the thesis holds out 10% of each group for perplexity; both keep corpus
+    order, and the test corpus numbers its tokens from 0."""
+    test_mask = np.zeros(cp.n_docs, dtype=bool)
+    for g in range(cp.n_groups):
+        docs = np.flatnonzero(cp.doc_group == g)
+        n_out = int(np.floor(frac * docs.size))
+        if n_out:
+            test_mask[docs[-n_out:]] = True
+
+    def take(mask):
+        idx = np.flatnonzero(mask)
+        lens = (cp.doc_off[1:] - cp.doc_off[:-1])[idx]
+        off = np.zeros(idx.size + 1, dtype=np.int64)
+        np.cumsum(lens, out=off[1:])
+        tok = np.concatenate([np.arange(cp.doc_off[d], cp.doc_off[d + 1]) for d in idx]) \
+            if idx.size else np.zeros(0, dtype=np.int64)
+        return Corpus(cp.words[tok].astype(np.int32), off, cp.doc_group[idx].astype(np.int32),
+                      cp.z_true[tok].astype(np.int32), cp.r_true[tok].astype(np.uint8),
+                      cp.n_groups, cp.vocab)
+
+    return take(~test_mask), take(test_mask)

@@ -1,0 +1,184 @@
+"""GPU point estimates and held-out perplexity against the oracle.
+
+* spdp_estimates (theta, phi0, every group's phi) equals the oracle's
+  estimates of the same state to fp64 rounding.
+* spdp_heldout: on held-out documents (10% of every group, as the thesis
+  holds out), the fold-in topics equal the oracle's and the perplexity agrees
+  to 1e-9; edge cases: empty and long (> 64 token) test documents, K at lane
+  layout boundaries, no training tokens (perplexity = V exactly), invalid
+  test corpora.
+* The snapshot sweep against exact Gibbs: after the same number of sweeps the
+  held-out perplexity of the library's document-parallel chain is within 15%
+  of the oracle's sequential (exact collapsed Gibbs) chain, both far below the
+  random initial state's.
+"""
+import math
+
+import numpy as np
+import pytest
+
+import oracle
+import synth
+from paper_1510_06549_amd import spdp as sp
+from tests import parity
+
+pytestmark = pytest.mark.gpu
+
+
+def say(*a):
+    print(*a, flush=True)
+
+
+class W:
+    def __init__(self, K, alpha=0.1, a=0.5, b=10.0, gamma=0.01):
+        self.K, self.alpha, self.a, self.b, self.gamma = K, alpha, a, b, gamma
+
+
+def _pair(cp, wl, init_seed=0):
+    return parity.make_pair(cp, wl, init_seed)
+
+
+@pytest.mark.parametrize("widx,K", [(0, 10), (1, 50)])
+def test_estimates_match_oracle(widx, K):
+    say(f"estimates, workload {widx}, K = {K}")
+    cp = synth.generate(synth.workload(widx), 1)
+    wl = synth.workload(widx)
+    wl = W(K, wl.alpha, wl.a, wl.b, wl.gamma)
+    s, m = _pair(cp, wl)
+    for sw in range(3):
+        s.sweep(sw, 17)
+    z, r = s.assignments()
+    c = m.rebuild(z, r)
+    th_o, p0_o, pg_o = m.estimates(z, c)
+    th, p0, pg = s.estimates()
+    np.testing.assert_allclose(th, th_o, rtol=1e-13)
+    np.testing.assert_allclose(p0, p0_o.T, rtol=1e-13)
+    np.testing.assert_allclose(pg, pg_o.transpose(0, 2, 1), rtol=1e-12)
+    # a group sub-range
+    _, _, pg1 = s.estimates(1, 2)
+    np.testing.assert_array_equal(pg1, pg[1:2])
+    s.close()
+
+
+def _heldout_case(cp_train, cp_test, wl, sweeps_train, foldin_sweeps, seed):
+    s, m = _pair(cp_train, wl)
+    for sw in range(sweeps_train):
+        s.sweep(sw, 23)
+    z, r = s.assignments()
+    c = m.rebuild(z, r)
+    _, _, pg_o = m.estimates(z, c)
+    tot_o, zt_o, _ = m.heldout(pg_o, cp_test.words, cp_test.doc_off, cp_test.doc_group,
+                               foldin_sweeps, seed)
+    ppl, tot, zt = s.heldout(cp_test.words, cp_test.doc_off, cp_test.doc_group, foldin_sweeps,
+                             seed)
+    s.close()
+    return tot_o, zt_o, ppl, tot, zt
+
+
+@pytest.mark.parametrize("widx,K", [(0, 10), (1, 50), (2, 100)])
+def test_heldout_matches_oracle(widx, K):
+    say(f"held-out perplexity, workload {widx}, K = {K}")
+    w0 = synth.workload(widx)
+    cp = synth.generate(w0, 2)
+    tr, te = synth.split_heldout(cp, 0.1)
+    wl = W(K, w0.alpha, w0.a, w0.b, w0.gamma)
+    tot_o, zt_o, ppl, tot, zt = _heldout_case(tr, te, wl, 3, 10, 31)
+    same = float(np.mean(zt == zt_o)) if zt.size else 1.0
+    say(f"  test tokens {te.n_tokens}, fold-in topics equal {same:.6f}, ppl {ppl:.4f}")
+    assert same >= 0.9999
+    assert abs(tot - tot_o) <= 1e-9 * abs(tot_o)
+    assert abs(ppl - math.exp(-tot_o / te.n_tokens)) <= 1e-9 * ppl
+
+
+@pytest.mark.parametrize("K", [1, 2, 64, 65, 129, 513])
+def test_heldout_edge_documents(K):
+    say(f"held-out edge documents, K = {K}")
+    rng = np.random.default_rng(K)
+    V = 40
+    train = [(d % 3, list(rng.integers(0, V, size=int(rng.integers(1, 90))))) for d in range(60)]
+    test = [(0, []), (1, list(rng.integers(0, V, size=1))), (2, list(rng.integers(0, V, size=64))),
+            (0, list(rng.integers(0, V, size=65))), (1, list(rng.integers(0, V, size=200))),
+            (2, [])]
+
+    def corpus(docs):
+        words = np.array([w for _, d in docs for w in d], np.int32)
+        off = np.cumsum([0] + [len(d) for _, d in docs]).astype(np.int64)
+        grp = np.array([g for g, _ in docs], np.int32)
+        return synth.Corpus(words, off, grp, np.zeros_like(words), np.zeros(len(words), np.uint8),
+                            3, V)
+
+    tot_o, zt_o, ppl, tot, zt = _heldout_case(corpus(train), corpus(test), W(K, 0.3, 0.6, 4.0,
+                                                                              0.05), 2, 6, 5)
+    np.testing.assert_array_equal(zt, zt_o)
+    assert abs(tot - tot_o) <= 1e-9 * abs(tot_o)
+
+
+def test_heldout_without_training_tokens():
+    say("perplexity without training tokens")
+    V, K = 13, 7
+    train = synth.Corpus(np.zeros(0, np.int32), np.zeros(3, np.int64), np.array([0, 1], np.int32),
+                         np.zeros(0, np.int32), np.zeros(0, np.uint8), 2, V)
+    s = sp.Sampler(train.words, train.doc_off, train.doc_group, 2, V, K, 0.2, 0.5, 3.0, 0.1)
+    rng = np.random.default_rng(3)
+    lens = [5, 0, 70]
+    words = rng.integers(0, V, size=sum(lens)).astype(np.int32)
+    off = np.cumsum([0] + lens).astype(np.int64)
+    ppl, tot, _ = s.heldout(words, off, np.array([1, 0, 1], np.int32), 4, 9)
+    assert abs(ppl - V) <= 1e-12 * V
+    s.close()
+
+
+def test_heldout_rejects_bad_test_corpora():
+    say("held-out argument checks")
+    cp = synth.generate(synth.workload(0), 0)
+    s = sp.Sampler(cp.words, cp.doc_off, cp.doc_group, cp.n_groups, cp.vocab, 5, 0.1, 0.5, 10.0,
+                   0.01)
+    good_w = np.array([1, 2, 3], np.int32)
+    good_o = np.array([0, 3], np.int64)
+    good_g = np.array([0], np.int32)
+    bad = [
+        (np.array([1, 2, cp.vocab], np.int32), good_o, good_g),   # word out of range
+        (good_w, good_o, np.array([cp.n_groups], np.int32)),     # group out of range
+        (good_w, np.array([0, 2], np.int64), good_g),            # offsets do not end at N
+        (good_w, np.array([1, 3], np.int64), good_g),            # offsets do not start at 0
+    ]
+    for wv, off, grp in bad:
+        with pytest.raises(sp.SpdpError) as e:
+            sp.spdp_heldout(s.h, wv, off, grp, cp.n_groups, cp.vocab, 2, 1)
+        assert e.value.code == sp.SPDP_E_ARG
+    with pytest.raises(sp.SpdpError):
+        sp.spdp_heldout(s.h, good_w, good_o, good_g, cp.n_groups, cp.vocab + 1, 2, 1)
+    ppl, _ = sp.spdp_heldout(s.h, good_w, good_o, good_g, cp.n_groups, cp.vocab, 2, 1)
+    assert ppl > 1.0
+    s.close()
+
+
+@pytest.mark.parametrize("widx,sweeps", [(0, 150), (1, 60)])
+def test_snapshot_chain_perplexity_tracks_exact_gibbs(widx, sweeps):
+    """Document-parallel snapshot sweeps (library) against exact sequential
+    collapsed Gibbs (oracle), same corpus, same number of sweeps: both leave
+    the random initial state far behind, and the snapshot chain's held-out
+    perplexity stays within 15% of exact Gibbs (the approximation's cost on
+    these small corpora, where one sweep moves a large share of the counts)."""
+    say(f"snapshot sweep vs exact Gibbs: held-out perplexity, workload {widx}")
+    w0 = synth.workload(widx)
+    cp = synth.generate(w0, 4)
+    tr, te = synth.split_heldout(cp, 0.1)
+    wl = W(w0.K, w0.alpha, w0.a, w0.b, w0.gamma)
+    s, m = _pair(tr, wl)
+    z, r, c = m.initial_state(0)
+    for sw in range(sweeps):
+        s.sweep(sw, 41)
+        m.sweep(c, z, r, sw, 41, mode="sequential")
+    ppl_gpu, _, _ = s.heldout(te.words, te.doc_off, te.doc_group, 20, 7)
+    _, _, pg = m.estimates(z, c)
+    tot_o, _, _ = m.heldout(pg, te.words, te.doc_off, te.doc_group, 20, 7)
+    ppl_seq = math.exp(-tot_o / te.n_tokens)
+    # the perplexity of the initial (random) state, for scale
+    s0, _ = _pair(tr, wl)
+    ppl_0, _, _ = s0.heldout(te.words, te.doc_off, te.doc_group, 20, 7)
+    s0.close()
+    s.close()
+    say(f"  perplexity: initial {ppl_0:.1f}, snapshot chain {ppl_gpu:.1f}, exact Gibbs {ppl_seq:.1f}")
+    assert ppl_gpu < 0.9 * ppl_0 and ppl_seq < 0.9 * ppl_0
+    assert abs(ppl_gpu - ppl_seq) <= 0.15 * ppl_seq
