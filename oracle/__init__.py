@@ -2,8 +2,9 @@
 
 TEST INFRASTRUCTURE ONLY: imported by the tests, the smoke check and the CPU
 baseline leg of the benchmark, never by the product library.  It shares no code
-with the HIP path.  The arithmetic lives in ``oracle.c``; this module only
-marshals numpy arrays.
+with the HIP path.  The sampler's arithmetic lives in ``oracle.c``; this module
+only marshals numpy arrays.  ``hellinger.py`` (numpy) compares two topic
+models.
 
 Model: Li (2012), arXiv:1510.06549, chapter "Shared Topic Modelling Using
 Shadow Poisson Dirichlet Process" with identity transformation matrices:
@@ -311,3 +312,6 @@ class Counts:
 
 def num_threads() -> int:
     return int(lib().or_num_threads())
+
+
+from .hellinger import align_topics, hellinger  # noqa: E402  (topic-model comparison)

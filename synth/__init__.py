@@ -58,6 +58,8 @@ def _L():
         L.synth_fill.argtypes = [C.c_void_p, C.c_uint64, C.c_void_p, C.c_void_p, C.c_void_p,
                                  C.c_void_p]
         L.synth_fill.restype = C.c_int
+        L.synth_phi0.argtypes = [C.c_void_p, C.c_uint64, C.c_void_p]
+        L.synth_phi0.restype = C.c_int
         _lib = L
     return _lib
 
@@ -143,6 +145,17 @@ def generate(w: Workload, seed: int = 0) -> Corpus:
         raise MemoryError("synth_fill failed")
     doc_group = (np.arange(D, dtype=np.int64) // w.docs_per_group).astype(np.int32)
     return Corpus(words, doc_off, doc_group, z, r, w.n_groups, w.vocab)
+
+
+def true_phi0(w: Workload, seed: int = 0) -> np.ndarray:
+    """The generating shadow base phi0 [K, V] of ``generate(w, seed)``: the law
+    from which a new table of topic k draws its word."""
+    p = _Params(w.n_groups, w.docs_per_group, w.vocab, w.K, w.doc_len_mean, w.zipf_s,
+                w.alpha, w.a, w.b)
+    out = np.empty((w.K, w.vocab), dtype=np.float64)
+    if _L().synth_phi0(C.byref(p), seed, out.ctypes.data) != 0:
+        raise MemoryError("synth_phi0 failed")
+    return out
 
 
 def split_heldout(cp: Corpus, frac: float = 0.1):

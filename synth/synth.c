@@ -214,26 +214,18 @@ static slot_t *wmap_get(wmap_t *m, int32_t key)
 /* doc_off must hold the CSR offsets implied by the phase-1 lengths.         */
 /* Scratch: about 4 N + 4 K V bytes.                                         */
 /* ------------------------------------------------------------------------ */
-int synth_fill(const synth_params *p, uint64_t seed, const int64_t *doc_off, int32_t *words,
-               int32_t *z, uint8_t *rr)
+/* shadow base: Zipf CDF over ranks (cdf [V]), one word permutation per topic
+ * (perm [K][V]: the word of rank i in topic k) */
+static void base_law(const synth_params *p, uint64_t seed, double *cdf, int32_t *perm)
 {
-    const int64_t G = p->n_groups, K = p->K, V = p->vocab;
-    const int64_t D = G * p->docs_per_group;
-    const int64_t N = doc_off[D];
-
-    /* shadow base: Zipf CDF over ranks, one permutation per topic */
-    double *cdf = (double *)malloc(sizeof(double) * (size_t)V);
-    int32_t *perm = (int32_t *)malloc(sizeof(int32_t) * (size_t)(K * V));
-    if (!cdf || !perm) return -1;
-    {
-        double acc = 0.0;
-        for (int64_t i = 0; i < V; ++i) {
-            acc += pow((double)(i + 1), -p->zipf_s);
-            cdf[i] = acc;
-        }
-        for (int64_t i = 0; i < V; ++i) cdf[i] /= acc;
-        cdf[V - 1] = 1.0;
+    const int64_t K = p->K, V = p->vocab;
+    double acc = 0.0;
+    for (int64_t i = 0; i < V; ++i) {
+        acc += pow((double)(i + 1), -p->zipf_s);
+        cdf[i] = acc;
     }
+    for (int64_t i = 0; i < V; ++i) cdf[i] /= acc;
+    cdf[V - 1] = 1.0;
 #pragma omp parallel for schedule(static)
     for (int64_t k = 0; k < K; ++k) {
         rng_t r;
@@ -245,6 +237,37 @@ int synth_fill(const synth_params *p, uint64_t seed, const int64_t *doc_off, int
             int32_t tmp = pk[i]; pk[i] = pk[j]; pk[j] = tmp;
         }
     }
+}
+
+/* The generating shadow base phi0 [K][V] of the corpus drawn with (p, seed):
+ * the probability with which a new table of topic k serves word w, i.e. the
+ * CDF step of w's rank (the law new tables draw from in synth_fill). */
+int synth_phi0(const synth_params *p, uint64_t seed, double *phi0)
+{
+    const int64_t K = p->K, V = p->vocab;
+    double *cdf = (double *)malloc(sizeof(double) * (size_t)V);
+    int32_t *perm = (int32_t *)malloc(sizeof(int32_t) * (size_t)(K * V));
+    if (!cdf || !perm) { free(cdf); free(perm); return -1; }
+    base_law(p, seed, cdf, perm);
+    for (int64_t k = 0; k < K; ++k)
+        for (int64_t i = 0; i < V; ++i)
+            phi0[k * V + perm[k * V + i]] = cdf[i] - (i > 0 ? cdf[i - 1] : 0.0);
+    free(cdf);
+    free(perm);
+    return 0;
+}
+
+int synth_fill(const synth_params *p, uint64_t seed, const int64_t *doc_off, int32_t *words,
+               int32_t *z, uint8_t *rr)
+{
+    const int64_t G = p->n_groups, K = p->K, V = p->vocab;
+    const int64_t D = G * p->docs_per_group;
+    const int64_t N = doc_off[D];
+
+    double *cdf = (double *)malloc(sizeof(double) * (size_t)V);
+    int32_t *perm = (int32_t *)malloc(sizeof(int32_t) * (size_t)(K * V));
+    if (!cdf || !perm) return -1;
+    base_law(p, seed, cdf, perm);
 
     /* topics: theta_d ~ Dir(alpha), z ~ theta_d */
 #pragma omp parallel

@@ -50,3 +50,28 @@ def test_restaurant_table_counts_match_pyp_expectation():
     mask = n > 0
     ratio = t[mask].sum() / exp_t[mask].sum()
     assert abs(ratio - 1.0) < 0.05, ratio
+
+
+def test_true_shadow_base_is_the_law_of_new_tables():
+    # Words served at new tables (r = 1) are draws from phi0 of their topic;
+    # pooled over topics, the rank of such a word in its topic's law follows
+    # the Zipf(s) pmf.  Chi-square over the first 30 ranks and a tail bucket.
+    wl = synth.workload(1)
+    cp = synth.generate(wl, 5)
+    phi0 = synth.true_phi0(wl, 5)
+    assert phi0.shape == (wl.K, wl.vocab)
+    np.testing.assert_allclose(phi0.sum(1), 1.0, rtol=1e-12)
+    rank = np.empty_like(phi0, dtype=np.int64)
+    for k in range(wl.K):
+        rank[k, np.argsort(-phi0[k], kind="stable")] = np.arange(wl.vocab)
+    sel = cp.r_true == 1
+    rk = rank[cp.z_true[sel], cp.words[sel]]
+    zipf = np.arange(1, wl.vocab + 1, dtype=np.float64) ** -wl.zipf_s
+    zipf /= zipf.sum()
+    n = rk.size
+    obs = np.append(np.bincount(rk, minlength=wl.vocab)[:30], (rk >= 30).sum())
+    exp = np.append(zipf[:30], zipf[30:].sum()) * n
+    chi2 = float(((obs - exp) ** 2 / exp).sum())
+    assert chi2 < 70.0, chi2  # 30 dof: p ~ 1e-4
+    # the law is the generator's for this seed only
+    assert not np.array_equal(np.argmax(phi0, 1), np.argmax(synth.true_phi0(wl, 6), 1))
