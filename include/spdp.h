@@ -170,6 +170,37 @@ int spdp_heldout(spdp_state *s, const spdp_corpus *test, const spdp_groups *test
                  int32_t n_sweeps, uint64_t seed, double *out2, int32_t *z_out, int where);
 
 /*
+ * Hellinger distances between the topics of two models (chapter
+ * "Experiments", subsection "Hellinger Distance"):
+ *   h[i][j] = sqrt(max(0, 1 - sum_v sqrt(p[v][i]) sqrt(q[v][j]))),
+ * which is (1/sqrt 2) || sqrt(p_i) - sqrt(q_j) ||_2 for distributions.
+ * p [n_outcomes][kp] and q [n_outcomes][kq] hold one distribution per column
+ * (topics contiguous, the layout spdp_estimates writes phi0 and phi in);
+ * entries must be >= 0 (a negative entry gives NaN).  p = NULL takes the
+ * state's shadow-base estimate phi0 (then kp = K, n_outcomes = V).  h
+ * [kp][kq] fp64.  `where` applies to p, q and h alike.  The contraction runs
+ * on the fp64 matrix cores; it allocates slices * kp * kq doubles of device
+ * scratch (at most 2048 slices, fewer as kp * kq grows) plus device copies of
+ * host inputs.  Uses the state's device and stream only; the state is not
+ * changed.  Synchronises.
+ * Errors: E_ARG (NULL q or h, negative size, kp or kq above SPDP_MAX_K, p NULL
+ * with kp != K or n_outcomes != V), E_HIP.
+ */
+int spdp_hellinger(spdp_state *s, const double *p, int32_t kp, const double *q, int32_t kq,
+                   int32_t n_outcomes, double *h, int where);
+
+/*
+ * Topic alignment for comparing two models ("re-ordered to align" in the
+ * Hellinger comparison): the one-to-one matching of the kp rows of h
+ * [kp][kq] (kp <= kq; e.g. distances from spdp_hellinger) to columns that
+ * minimises the summed entries.  match [kp] int32 receives the column of each
+ * row, *total the minimum sum.  Host arrays only; runs on the host
+ * (Hungarian method with potentials, O(kp^2 kq)); needs no state and no GPU.
+ * Errors: E_ARG (NULL pointer, kp < 0 or kp > kq, an entry not finite).
+ */
+int spdp_align_topics(const double *h, int32_t kp, int32_t kq, int32_t *match, double *total);
+
+/*
  * Checkpoint: export z [N] int32 and r [N] uint8 (either may be NULL).
  * Synchronises.  Errors: E_ARG, E_HIP.
  */

@@ -537,6 +537,68 @@ int spdp_heldout(spdp_state *s, const spdp_corpus *test, const spdp_groups *test
     return SPDP_OK;
 }
 
+int spdp_hellinger(spdp_state *s, const double *p, int32_t kp, const double *q, int32_t kq,
+                   int32_t n_outcomes, double *h, int where)
+{
+    if (!s || !q || !h) return fail(SPDP_E_ARG, "null argument");
+    const Model &m = s->m;
+    if (where != 0 && where != 1) return fail(SPDP_E_ARG, "where must be 0 or 1");
+    if (kp < 0 || kq < 0 || n_outcomes < 0) return fail(SPDP_E_ARG, "negative size");
+    if (kp > SPDP_MAX_K || kq > SPDP_MAX_K)
+        return fail(SPDP_E_ARG, "topic counts must be at most %d", SPDP_MAX_K);
+    if (!p && (kp != m.K || n_outcomes != m.V))
+        return fail(SPDP_E_ARG, "with p NULL (the state's phi0), kp must be K and n_outcomes V");
+    HIP_TRY(hipSetDevice(s->device));
+    const int64_t V = n_outcomes, np = V * kp, nq = V * kq, nh = (int64_t)kp * kq;
+    const HellingerPlan plan = hellinger_plan(kp, kq, V);
+    std::vector<void *> tmp;
+    hipError_t e = hipSuccess;
+    auto dalloc = [&](int64_t n) -> double * {
+        void *x = nullptr;
+        if (e == hipSuccess) e = hipMalloc(&x, (size_t)(n > 0 ? n : 1) * sizeof(double));
+        if (e != hipSuccess) return nullptr;
+        tmp.push_back(x);
+        return (double *)x;
+    };
+    auto upload = [&](const double *src, int64_t n) -> const double * {
+        double *x = dalloc(n);
+        if (e == hipSuccess && n > 0)
+            e = hipMemcpyAsync(x, src, (size_t)n * sizeof(double), hipMemcpyHostToDevice, s->st);
+        return x;
+    };
+    const double *Pd = p, *Qd = q;
+    double *Hd = h;
+    if (!p) {
+        double *x = dalloc(np);
+        if (e == hipSuccess) e = launch_phi0(m, s->b, x, s->st);
+        Pd = x;
+    } else if (!where) {
+        Pd = upload(p, np);
+    }
+    if (!where) {
+        Qd = upload(q, nq);
+        Hd = dalloc(nh);
+    }
+    double *part = dalloc((int64_t)plan.slices * nh);
+    if (e == hipSuccess) e = launch_hellinger(plan, Pd, kp, Qd, kq, V, part, Hd, s->st);
+    if (e == hipSuccess && !where && nh > 0)
+        e = hipMemcpyAsync(h, Hd, (size_t)nh * sizeof(double), hipMemcpyDeviceToHost, s->st);
+    if (e == hipSuccess) e = hipStreamSynchronize(s->st);
+    for (void *x : tmp) hipFree(x);
+    HIP_TRY(e);
+    return SPDP_OK;
+}
+
+int spdp_align_topics(const double *h, int32_t kp, int32_t kq, int32_t *match, double *total)
+{
+    if (!total || (kp > 0 && (!h || !match))) return fail(SPDP_E_ARG, "null argument");
+    if (kp < 0 || kq < kp) return fail(SPDP_E_ARG, "need 0 <= kp <= kq");
+    for (int64_t i = 0; i < (int64_t)kp * kq; ++i)
+        if (!std::isfinite(h[i])) return fail(SPDP_E_ARG, "distance matrix entry is not finite");
+    *total = kp > 0 ? align_topics_host(h, kp, kq, match) : 0.0;
+    return SPDP_OK;
+}
+
 int spdp_get_assignments(const spdp_state *s, int32_t *z, uint8_t *r, int where)
 {
     if (!s) return fail(SPDP_E_ARG, "state is NULL");

@@ -177,6 +177,22 @@ hipError_t launch_foldin(const Model &m, const DeviceBuffers &b, int32_t D_test,
                          int32_t n_sweeps, uint64_t seed, int32_t *z, double *ll_doc,
                          hipStream_t st);
 
+// Hellinger distances between the topics of two models (P [V][kp], Q [V][kq],
+// topics contiguous): the launch shape and the partial-sum buffer it needs
+// (slices * kp * kq doubles).
+struct HellingerPlan {
+    int64_t slice = 0;   // outcomes per slice (a multiple of the LDS stage)
+    int32_t slices = 1;  // outcome slices (grid y)
+    int32_t tiles_j = 1; // 64-wide tiles along kq
+    int64_t tiles = 1;   // output tiles (grid x)
+};
+HellingerPlan hellinger_plan(int32_t kp, int32_t kq, int64_t V);
+hipError_t launch_hellinger(const HellingerPlan &p, const double *P, int32_t kp, const double *Q,
+                            int32_t kq, int64_t V, double *part, double *h, hipStream_t st);
+// least-total-cost matching of the rows of c [kp][kq] (kp <= kq, finite):
+// match[i] = column of row i; returns the total cost (host code)
+double align_topics_host(const double *c, int32_t kp, int32_t kq, int32_t *match);
+
 // The sampler's per-lane topic count for K topics (4 at most per dwordx4).
 int sampler_kpl(int32_t K);
 int32_t padded_K(int32_t K);

@@ -30,7 +30,7 @@ EXPORTS = (
     "spdp_create", "spdp_sweep", "spdp_counts", "spdp_totals", "spdp_loglik", "spdp_destroy",
     "spdp_get_assignments", "spdp_set_assignments", "spdp_debug_conditionals", "spdp_stats",
     "spdp_kernel_timing", "spdp_kernel_times", "spdp_info", "spdp_last_error",
-    "spdp_estimates", "spdp_heldout",
+    "spdp_estimates", "spdp_heldout", "spdp_hellinger", "spdp_align_topics",
 )
 
 
@@ -96,6 +96,10 @@ def load_library() -> C.CDLL:
     L.spdp_estimates.restype = cint
     L.spdp_heldout.argtypes = [vp, vp, vp, i32, u64, vp, vp, cint]
     L.spdp_heldout.restype = cint
+    L.spdp_hellinger.argtypes = [vp, vp, i32, vp, i32, i32, vp, cint]
+    L.spdp_hellinger.restype = cint
+    L.spdp_align_topics.argtypes = [vp, i32, i32, vp, vp]
+    L.spdp_align_topics.restype = cint
     return L
 
 
@@ -246,6 +250,30 @@ def spdp_heldout(h, words, doc_offsets, doc_group, n_groups, vocab, n_sweeps, se
     return float(out[0]), float(out[1])
 
 
+def spdp_hellinger(h, p, q, out):
+    """Hellinger distances out [kp, kq] between the columns of p [V, kp] (None:
+    the state's phi0) and q [V, kq]; see include/spdp.h."""
+    where = _where(p, q, out)
+    V, kq = q.shape
+    kp = out.shape[0]
+    if out.shape != (kp, kq) or (p is not None and p.shape != (V, kp)):
+        raise ValueError("p [V, kp], q [V, kq] and out [kp, kq] do not agree")
+    _check(lib().spdp_hellinger(h, _buf(p)[0], int(kp), _buf(q)[0], int(kq), int(V),
+                                _buf(out)[0], where))
+    return out
+
+
+def spdp_align_topics(dist):
+    """(match [kp] int32, total) of the least-total matching of rows to columns."""
+    dist = np.ascontiguousarray(dist, dtype=np.float64)
+    kp, kq = dist.shape
+    match = np.zeros(kp, dtype=np.int32)
+    total = C.c_double()
+    _check(lib().spdp_align_topics(dist.ctypes.data, int(kp), int(kq), match.ctypes.data,
+                                   C.byref(total)))
+    return match, float(total.value)
+
+
 # ---------------------------------------------------------------------------
 # Convenience wrapper (host numpy in and out)
 # ---------------------------------------------------------------------------
@@ -328,6 +356,16 @@ class Sampler:
         phi = np.empty((g_end - g_begin, self.V, self.K), dtype=np.float64)
         spdp_estimates(self.h, g_begin, g_end, theta, phi0, phi)
         return theta, phi0, phi
+
+    def hellinger(self, q, p=None):
+        """Hellinger distances [kp, kq] between the columns of p [V, kp] (default:
+        this state's phi0) and q [V, kq], fp64 host arrays."""
+        q = np.ascontiguousarray(q, dtype=np.float64)
+        if p is not None:
+            p = np.ascontiguousarray(p, dtype=np.float64)
+        kp = self.K if p is None else p.shape[1]
+        out = np.empty((kp, q.shape[1]), dtype=np.float64)
+        return spdp_hellinger(self.h, p, q, out)
 
     def heldout(self, words, doc_offsets, doc_group, n_sweeps, seed):
         """(perplexity, sum of log p, fold-in topics) of held-out documents."""
