@@ -110,6 +110,26 @@ def lib():
         L.or_estimates.restype = None
         L.or_heldout.argtypes = [vp, vp, i32, vp, vp, vp, i32, u64, vp, vp]
         L.or_heldout.restype = dbl
+        L.or_head_source.argtypes = [vp, vp, i32, i32]
+        L.or_head_source.restype = i32
+        L.or_rebuild_assoc.argtypes = [vp, vp, vp, vp, vp, vp]
+        L.or_rebuild_assoc.restype = None
+        L.or_repair_assoc.argtypes = [vp, vp, vp, vp, vp, vp]
+        L.or_repair_assoc.restype = i64
+        L.or_token_weights_assoc.argtypes = [vp, vp, vp, vp, i32, i32, i32, i32, i32, vp]
+        L.or_token_weights_assoc.restype = C.c_int
+        L.or_sample_docs_assoc.argtypes = [vp, vp, vp, vp, vp, vp, u32, u64, i32, i32, vp, vp,
+                                           vp, i64, i64]
+        L.or_sample_docs_assoc.restype = i64
+        L.or_sweep_assoc.argtypes = [vp, vp, vp, vp, vp, vp, u32, u64, C.c_int, vp]
+        L.or_sweep_assoc.restype = C.c_int
+        L.or_loglik_assoc.argtypes = [vp, vp, vp, vp, vp, vp]
+        L.or_loglik_assoc.restype = dbl
+        L.or_estimates_assoc.argtypes = [vp, vp, vp, vp, vp, vp, vp]
+        L.or_estimates_assoc.restype = None
+        L.or_chain_histogram_assoc.argtypes = [vp, vp, vp, vp, vp, vp, u32, i64, u64, C.c_int,
+                                               vp, i64]
+        L.or_chain_histogram_assoc.restype = C.c_int
         _lib = L
     return _lib
 
@@ -284,6 +304,114 @@ class Model:
         total = lib().or_heldout(self.ref, _p(phig), D, _p(words), _p(doc_off), _p(doc_group),
                                  int(n_sweeps), int(seed) & (2**64 - 1), _p(z), _p(ll_doc))
         return float(total), z, ll_doc
+
+
+class _Assoc(C.Structure):
+    _fields_ = [
+        ("S", C.c_int32),
+        ("row_off", C.c_void_p),
+        ("src", C.c_void_p),
+        ("p", C.c_void_p),
+    ]
+
+
+class AssocModel(Model):
+    """The model with word associations (non-identity P^g): every head carries
+    the slot s of its source in its row's list, and the shadow-base counts
+    Bkw[k, v] are keyed by source.  `row_off` [G V + 1] int64, `src` [nnz]
+    int32 and `p` [nnz] float64 list, for each row (g, w) in order, the
+    sources v with p_{g,w,v} > 0."""
+
+    def __init__(self, words, doc_off, doc_group, n_groups, K, vocab, alpha, a, b, gamma,
+                 row_off, src, p, ncap: int | None = None):
+        super().__init__(words, doc_off, doc_group, n_groups, K, vocab, alpha, a, b, gamma, ncap)
+        self.row_off = np.ascontiguousarray(row_off, dtype=np.int64)
+        self.src = np.ascontiguousarray(src, dtype=np.int32)
+        self.p = np.ascontiguousarray(p, dtype=np.float64)
+        assert self.row_off.shape == (self.G * self.V + 1,) and self.row_off[0] == 0
+        assert self.row_off[-1] == self.src.shape[0] == self.p.shape[0]
+        lens = np.diff(self.row_off)
+        assert lens.min() >= 1, "every row needs a source"
+        self.S = int(lens.max())
+        self._a = _Assoc(self.S, _p(self.row_off).value, _p(self.src).value, _p(self.p).value)
+
+    @property
+    def aref(self):
+        return C.byref(self._a)
+
+    def head_source(self, g, w) -> int:
+        return int(lib().or_head_source(self.ref, self.aref, int(g), int(w)))
+
+    def rebuild(self, z, r, s, counts: "Counts | None" = None) -> "Counts":
+        c = counts if counts is not None else self.new_counts()
+        lib().or_rebuild_assoc(self.ref, self.aref, _p(z), _p(r), _p(s), c.ref)
+        return c
+
+    def repair(self, z, r, s, counts: "Counts") -> int:
+        return int(lib().or_repair_assoc(self.ref, self.aref, _p(z), _p(r), _p(s), counts.ref))
+
+    def initial_state(self, init_seed: int):
+        """Philox-uniform topics, r = 0, s = 0, rebuild, repair."""
+        z, r = self.init(init_seed)
+        s = np.zeros(self.N, dtype=np.uint8)
+        c = self.rebuild(z, r, s)
+        self.repair(z, r, s, c)
+        return z, r, s, c
+
+    def token_weights(self, counts, crow, g, w, k0, r0, s0):
+        """K (S + 1) weights (None if the sole-head point mass applies)."""
+        out = np.zeros(self.K * (self.S + 1), dtype=np.float64)
+        crow = np.ascontiguousarray(crow, dtype=np.int32)
+        skip = lib().or_token_weights_assoc(self.ref, self.aref, counts.ref, _p(crow), int(g),
+                                            int(w), int(k0), int(r0), int(s0), _p(out))
+        return None if skip else out
+
+    def sample_docs(self, counts, z, r, s, sweep, seed, d_begin=0, d_end=None, trace=None):
+        if d_end is None:
+            d_end = self.D
+        if trace is None:
+            return int(lib().or_sample_docs_assoc(self.ref, self.aref, counts.ref, _p(z), _p(r),
+                                                  _p(s), sweep, seed, d_begin, d_end, None, None,
+                                                  None, 0, 0))
+        tb, te = trace
+        T = te - tb
+        tw = np.zeros((T, self.K * (self.S + 1)), dtype=np.float64)
+        tu = np.full(T, np.nan, dtype=np.float64)
+        ts = np.zeros(T, dtype=np.uint8)
+        ch = lib().or_sample_docs_assoc(self.ref, self.aref, counts.ref, _p(z), _p(r), _p(s),
+                                        sweep, seed, d_begin, d_end, _p(tw), _p(tu), _p(ts), tb,
+                                        te)
+        return int(ch), tw, tu, ts
+
+    def sweep(self, counts, z, r, s, sweep, seed, mode: str = "snapshot"):
+        stats = np.zeros(2, dtype=np.int64)
+        rc = lib().or_sweep_assoc(self.ref, self.aref, counts.ref, _p(z), _p(r), _p(s), sweep,
+                                  seed, 0 if mode == "snapshot" else 1, _p(stats))
+        if rc != 0:
+            raise ValueError(mode)
+        return int(stats[0]), int(stats[1])
+
+    def chain_histogram(self, counts, z, r, s, first_sweep, n_sweeps, seed, mode="sequential"):
+        n_bins = (self.K * (self.S + 1)) ** self.N
+        hist = np.zeros(n_bins, dtype=np.int64)
+        rc = lib().or_chain_histogram_assoc(self.ref, self.aref, counts.ref, _p(z), _p(r), _p(s),
+                                            first_sweep, n_sweeps, seed,
+                                            0 if mode == "snapshot" else 1, _p(hist), n_bins)
+        if rc != 0:
+            raise RuntimeError(f"or_chain_histogram_assoc failed ({rc})")
+        return hist
+
+    def loglik(self, z, r, s, counts: "Counts") -> float:
+        return float(lib().or_loglik_assoc(self.ref, self.aref, _p(z), _p(r), _p(s), counts.ref))
+
+    def estimates(self, z, counts: "Counts"):
+        theta = np.zeros((self.D, self.K), dtype=np.float64)
+        phi0 = np.zeros((self.K, self.V), dtype=np.float64)
+        phig = np.zeros((self.G, self.K, self.V), dtype=np.float64)
+        lib().or_estimates_assoc(self.ref, self.aref,
+                                 _p(np.ascontiguousarray(z, dtype=np.int32)), counts.ref,
+                                 _p(theta), _p(phi0), _p(phig))
+        return theta, phi0, phig
 
 
 class Counts:

@@ -640,3 +640,341 @@ double or_heldout(const or_model *m, const double *phig, int32_t d_test, const i
     if (!z_out) free(zz);
     return total;
 }
+
+/* ======================================================================== */
+/* Word associations: non-identity transformation matrices P^i.            */
+/*                                                                          */
+/* The full model of the SPDP chapter: group i's topic k is a Pitman-Yor     */
+/* process around P^i phi0_k, so a new table first takes a source word v     */
+/* from the shadow base and then serves word w with probability p_{i,w,v}    */
+/* (column v of P^i is a distribution over w).  Each table head carries its  */
+/* source (the thesis's v_{ikwt}); q_{ikwv} counts the tables of (i, k, w)   */
+/* with source v, and the shadow base counts tables by SOURCE:               */
+/*   Bkw[k][v] = sum_i sum_w q_{ikwv},   Bk[k] = sum_v Bkw[k][v] = sum T_gk.  */
+/* Eq. SPDP-joint-prob-with-v and the blocked-Gibbs joint add the factor     */
+/* prod over heads of p_{i,w,v(head)}; Eq. SPDP-sampling-w-z-r1 gains        */
+/* p_{i,w,v} and (gamma_v + sum q_{.k.v}) in place of (gamma + B_kw).        */
+/*                                                                          */
+/* P^i is sparse: row (g, w) lists its sources v with p_{g,w,v} > 0          */
+/* (at most S of them).  A head's source is stored as its index s within     */
+/* its row's list.  Readings (listed in the design notes):                   */
+/*   - outcomes of one token, per topic k, in the order (k, r=1, s) for       */
+/*     s = 0..S-1, then (k, r=0): j = k (S + 1) + s and j = k (S + 1) + S;    */
+/*     list slots s >= S_w of a shorter row have weight 0.  With S = 1 and    */
+/*     v = w this is the identity order j = 2k + 1 - r;                       */
+/*   - a token with r = 0 stores s = 0;                                       */
+/*   - repair promotes the smallest-index token of a cell with customers but  */
+/*     no table and gives it the row's most probable source (the first one    */
+/*     on ties);                                                              */
+/*   - initialisation as with P = I (z from Philox, r = 0, s = 0), then       */
+/*     rebuild and repair.                                                    */
+/* ======================================================================== */
+typedef struct {
+    int32_t S;              /* longest source list                          */
+    const int64_t *row_off; /* [G V + 1] CSR offsets of the rows (g, w)       */
+    const int32_t *src;     /* [nnz] source word v of each entry             */
+    const double *p;        /* [nnz] p_{g,w,v}                               */
+} or_assoc;
+
+static inline int64_t arow(const or_model *m, int64_t g, int64_t w) { return g * m->vocab + w; }
+
+/* index of the row's most probable source (first on ties) */
+int32_t or_head_source(const or_model *m, const or_assoc *A, int32_t g, int32_t w)
+{
+    const int64_t q = arow(m, g, w), beg = A->row_off[q], end = A->row_off[q + 1];
+    int32_t best = 0;
+    for (int64_t e = beg + 1; e < end; ++e)
+        if (A->p[e] > A->p[beg + best]) best = (int32_t)(e - beg);
+    return best;
+}
+
+static inline int32_t source_of(const or_model *m, const or_assoc *A, int64_t g, int64_t w,
+                                int32_t s)
+{
+    return A->src[A->row_off[arow(m, g, w)] + s];
+}
+
+void or_rebuild_assoc(const or_model *m, const or_assoc *A, const int32_t *z, const uint8_t *r,
+                      const uint8_t *s, or_counts *c)
+{
+    const int64_t G = m->n_groups, K = m->K, V = m->vocab;
+    memset(c->n, 0, sizeof(int32_t) * (size_t)(G * K * V));
+    memset(c->t, 0, sizeof(int32_t) * (size_t)(G * K * V));
+    memset(c->Ngk, 0, sizeof(int32_t) * (size_t)(G * K));
+    memset(c->Tgk, 0, sizeof(int32_t) * (size_t)(G * K));
+    memset(c->Bkw, 0, sizeof(int32_t) * (size_t)(K * V));
+    memset(c->Bk, 0, sizeof(int32_t) * (size_t)K);
+    for (int32_t d = 0; d < m->n_docs; ++d) {
+        const int64_t g = m->doc_group[d];
+        for (int64_t i = m->doc_off[d]; i < m->doc_off[d + 1]; ++i) {
+            const int64_t k = z[i], w = m->words[i];
+            c->n[(g * K + k) * V + w] += 1;
+            c->Ngk[g * K + k] += 1;
+            if (r[i]) {
+                c->t[(g * K + k) * V + w] += 1;
+                c->Tgk[g * K + k] += 1;
+                c->Bkw[k * V + source_of(m, A, g, w, s[i])] += 1;
+                c->Bk[k] += 1;
+            }
+        }
+    }
+}
+
+int64_t or_repair_assoc(const or_model *m, const or_assoc *A, const int32_t *z, uint8_t *r,
+                        uint8_t *s, or_counts *c)
+{
+    const int64_t K = m->K, V = m->vocab;
+    int64_t promoted = 0;
+    for (int32_t d = 0; d < m->n_docs; ++d) {
+        const int64_t g = m->doc_group[d];
+        for (int64_t i = m->doc_off[d]; i < m->doc_off[d + 1]; ++i) {
+            const int64_t k = z[i], w = m->words[i];
+            if (r[i] == 0 && c->t[(g * K + k) * V + w] == 0) {
+                const int32_t hs = or_head_source(m, A, (int32_t)g, (int32_t)w);
+                r[i] = 1;
+                s[i] = (uint8_t)hs;
+                c->t[(g * K + k) * V + w] += 1;
+                c->Tgk[g * K + k] += 1;
+                c->Bkw[k * V + source_of(m, A, g, w, hs)] += 1;
+                c->Bk[k] += 1;
+                ++promoted;
+            }
+        }
+    }
+    return promoted;
+}
+
+/* The K (S + 1) unnormalised conditionals of one token (Eq. SPDP-sampling-  */
+/* w-z-r0 and Eq. SPDP-sampling-w-z-r1 with p_{i,w,v}), on the counts `c`    */
+/* with the token's own contribution removed (its customer, and if it is a   */
+/* head its table and its source's base count), and the document row `crow` */
+/* (which still includes the token): w[k (S+1) + s] = (k, r=1, source slot   */
+/* s) and w[k (S+1) + S] = (k, r=0).                                          */
+/* The only head of a cell that keeps other customers must stay that cell's  */
+/* head (every other topic or r has joint probability zero), but its source  */
+/* is free: then only its own topic's head slots are non-zero, in proportion */
+/* to the joint, p_{g,w,v} (gamma + Bkw[k0][v] without the token's source).  */
+/* Always returns 0 (no point mass: some slot is always positive).          */
+int or_token_weights_assoc(const or_model *m, const or_assoc *A, const or_counts *c,
+                           const int32_t *crow, int32_t g, int32_t wd, int32_t k0, int32_t r0,
+                           int32_t s0, double *w)
+{
+    const int64_t K = m->K, V = m->vocab, S = A->S;
+    const int64_t cell0 = ((int64_t)g * K + k0) * V + wd;
+    const int64_t q = arow(m, g, wd), beg = A->row_off[q], nsrc = A->row_off[q + 1] - beg;
+    const int32_t v0 = A->src[beg + s0];
+    if (r0 == 1 && c->t[cell0] == 1 && c->n[cell0] > 1) {
+        for (int64_t j = 0; j < K * (S + 1); ++j) w[j] = 0.0;
+        for (int64_t sl = 0; sl < nsrc; ++sl) {
+            const int32_t v = A->src[beg + sl];
+            w[k0 * (S + 1) + sl] =
+                A->p[beg + sl] * (m->gam + (double)(c->Bkw[(int64_t)k0 * V + v] - (v == v0)));
+        }
+        return 0;
+    }
+    const double alpha = m->alpha, a = m->a, b = m->b, gam = m->gam;
+    for (int64_t k = 0; k < K; ++k) {
+        const int del = (k == k0);
+        const int64_t cell = ((int64_t)g * K + k) * V + wd;
+        const int64_t nw = c->n[cell] - del;
+        const int64_t tw = c->t[cell] - del * r0;
+        const int64_t Nk = c->Ngk[g * K + k] - del;
+        const int64_t Tk = c->Tgk[g * K + k] - del * r0;
+        const int64_t Bt = c->Bk[k] - del * r0;
+        const double ck = (double)(crow[k] - del);
+        double q0, q1;
+        if (nw == 0) {
+            q0 = 0.0;
+            q1 = 1.0;
+        } else {
+            const double ls = log_stirling(m, nw, tw);
+            q0 = (double)(nw - tw + 1) / (double)(nw + 1) * exp(log_stirling(m, nw + 1, tw) - ls);
+            q1 = (double)(tw + 1) / (double)(nw + 1) * exp(log_stirling(m, nw + 1, tw + 1) - ls);
+        }
+        const double doc = alpha + ck;
+        double *wk = w + k * (S + 1);
+        for (int64_t sl = 0; sl < S; ++sl) {
+            if (sl >= nsrc) { wk[sl] = 0.0; continue; }
+            const int32_t v = A->src[beg + sl];
+            const int64_t Bv = c->Bkw[k * V + v] - ((del && r0 && v == v0) ? 1 : 0);
+            wk[sl] = A->p[beg + sl] * doc * (b + a * (double)Tk) / (b + (double)Nk) *
+                     (gam + (double)Bv) / ((double)V * gam + (double)Bt) * q1;
+        }
+        wk[S] = doc / (b + (double)Nk) * q0;
+    }
+    return 0;
+}
+
+/* Sampling step of one sweep over documents [d_begin, d_end) against the    */
+/* snapshot `c` (read only); as or_sample_docs, with the source slot s.       */
+/* Trace: K (S + 1) weights per token.                                        */
+int64_t or_sample_docs_assoc(const or_model *m, const or_assoc *A, const or_counts *c,
+                             int32_t *z, uint8_t *r, uint8_t *s, uint32_t sweep, uint64_t seed,
+                             int32_t d_begin, int32_t d_end, double *tr_w, double *tr_u,
+                             uint8_t *tr_skip, int64_t tr_begin, int64_t tr_end)
+{
+    const int64_t K = m->K, S1 = A->S + 1, nout = K * S1;
+    int64_t changed = 0;
+#pragma omp parallel reduction(+ : changed)
+    {
+        int32_t *crow = (int32_t *)malloc(sizeof(int32_t) * (size_t)K);
+        double *w = (double *)malloc(sizeof(double) * (size_t)nout);
+#pragma omp for schedule(dynamic, 16)
+        for (int32_t d = d_begin; d < d_end; ++d) {
+            const int32_t g = m->doc_group[d];
+            memset(crow, 0, sizeof(int32_t) * (size_t)K);
+            for (int64_t i = m->doc_off[d]; i < m->doc_off[d + 1]; ++i) crow[z[i]] += 1;
+            for (int64_t i = m->doc_off[d]; i < m->doc_off[d + 1]; ++i) {
+                const int32_t k0 = z[i], r0 = r[i], s0 = s[i];
+                const int skip =
+                    or_token_weights_assoc(m, A, c, crow, g, m->words[i], k0, r0, s0, w);
+                const int tr = (tr_w != NULL && i >= tr_begin && i < tr_end);
+                if (tr) tr_skip[i - tr_begin] = (uint8_t)skip;
+                if (skip) continue;
+                const double u = or_uniform(seed, i, sweep);
+                if (tr) {
+                    memcpy(tr_w + (i - tr_begin) * nout, w, sizeof(double) * (size_t)nout);
+                    tr_u[i - tr_begin] = u;
+                }
+                const int j = draw_outcome(w, nout, u);
+                const int32_t k1 = (int32_t)(j / S1), sl = (int32_t)(j % S1);
+                const int32_t r1 = sl < A->S ? 1 : 0, s1 = r1 ? sl : 0;
+                crow[k0] -= 1;
+                crow[k1] += 1;
+                if (k1 != k0 || r1 != r0 || s1 != s0) ++changed;
+                z[i] = k1;
+                r[i] = (uint8_t)r1;
+                s[i] = (uint8_t)s1;
+            }
+        }
+        free(crow);
+        free(w);
+    }
+    return changed;
+}
+
+static void apply_token_assoc(const or_model *m, const or_assoc *A, or_counts *c, int32_t g,
+                              int32_t wd, int32_t k, int32_t rr, int32_t sl, int sgn)
+{
+    const int64_t K = m->K, V = m->vocab;
+    const int64_t cell = ((int64_t)g * K + k) * V + wd;
+    c->n[cell] += sgn;
+    c->Ngk[(int64_t)g * K + k] += sgn;
+    if (rr) {
+        c->t[cell] += sgn;
+        c->Tgk[(int64_t)g * K + k] += sgn;
+        c->Bkw[(int64_t)k * V + source_of(m, A, g, wd, sl)] += sgn;
+        c->Bk[k] += sgn;
+    }
+}
+
+/* One sweep: mode 0 snapshot-parallel (sampling, then rebuild and repair),  */
+/* mode 1 sequential collapsed Gibbs (Algorithm SPDP-Full-Gibbs with stored  */
+/* r and source: live counts after every token).                             */
+int or_sweep_assoc(const or_model *m, const or_assoc *A, or_counts *c, int32_t *z, uint8_t *r,
+                   uint8_t *s, uint32_t sweep, uint64_t seed, int mode, int64_t *out_stats)
+{
+    int64_t changed = 0, promoted = 0;
+    const int64_t K = m->K, S1 = A->S + 1, nout = K * S1;
+    if (mode == 0) {
+        changed = or_sample_docs_assoc(m, A, c, z, r, s, sweep, seed, 0, m->n_docs, NULL, NULL,
+                                       NULL, 0, 0);
+        or_rebuild_assoc(m, A, z, r, s, c);
+        promoted = or_repair_assoc(m, A, z, r, s, c);
+    } else if (mode == 1) {
+        int32_t *crow = (int32_t *)malloc(sizeof(int32_t) * (size_t)K);
+        double *w = (double *)malloc(sizeof(double) * (size_t)nout);
+        for (int32_t d = 0; d < m->n_docs; ++d) {
+            const int32_t g = m->doc_group[d];
+            memset(crow, 0, sizeof(int32_t) * (size_t)K);
+            for (int64_t i = m->doc_off[d]; i < m->doc_off[d + 1]; ++i) crow[z[i]] += 1;
+            for (int64_t i = m->doc_off[d]; i < m->doc_off[d + 1]; ++i) {
+                const int32_t k0 = z[i], r0 = r[i], s0 = s[i], wd = m->words[i];
+                if (or_token_weights_assoc(m, A, c, crow, g, wd, k0, r0, s0, w)) continue;
+                const int j = draw_outcome(w, nout, or_uniform(seed, i, sweep));
+                const int32_t k1 = (int32_t)(j / S1), sl = (int32_t)(j % S1);
+                const int32_t r1 = sl < A->S ? 1 : 0, s1 = r1 ? sl : 0;
+                apply_token_assoc(m, A, c, g, wd, k0, r0, s0, -1);
+                apply_token_assoc(m, A, c, g, wd, k1, r1, s1, +1);
+                crow[k0] -= 1;
+                crow[k1] += 1;
+                if (k1 != k0 || r1 != r0 || s1 != s0) ++changed;
+                z[i] = k1;
+                r[i] = (uint8_t)r1;
+                s[i] = (uint8_t)s1;
+            }
+        }
+        free(crow);
+        free(w);
+    } else {
+        return -1;
+    }
+    if (out_stats) { out_stats[0] = changed; out_stats[1] = promoted; }
+    return 0;
+}
+
+/* Joint log p(W, Z, V, R): the P = I joint evaluated on counts whose shadow */
+/* base is keyed by source (or_rebuild_assoc), times the association factor  */
+/* prod_{g,w,v} p_{g,w,v}^{sum_k q_{gkwv}} = prod over heads of p of the     */
+/* head's source.                                                            */
+double or_loglik_assoc(const or_model *m, const or_assoc *A, const int32_t *z, const uint8_t *r,
+                       const uint8_t *s, const or_counts *c)
+{
+    double ll = or_loglik(m, z, r, c);
+    double lp = 0.0;
+    for (int32_t d = 0; d < m->n_docs; ++d) {
+        const int64_t g = m->doc_group[d];
+        for (int64_t i = m->doc_off[d]; i < m->doc_off[d + 1]; ++i)
+            if (r[i]) lp += log(A->p[A->row_off[arow(m, g, m->words[i])] + s[i]]);
+    }
+    return ll + lp;
+}
+
+/* Estimates with associations: theta as before; phi0[k][v] over sources;    */
+/* the group estimate takes the base of its Pitman-Yor process, P^g phi0_k:  */
+/*   phig[g][k][w] = (n - a t + (b + a T_gk) sum_v p_{g,w,v} phi0[k][v]) / (b + N_gk). */
+void or_estimates_assoc(const or_model *m, const or_assoc *A, const int32_t *z,
+                        const or_counts *c, double *theta, double *phi0, double *phig)
+{
+    const int64_t G = m->n_groups, K = m->K, V = m->vocab;
+    double *p0 = (double *)malloc(sizeof(double) * (size_t)(K * V > 0 ? K * V : 1));
+    or_estimates(m, z, c, theta, p0, NULL);
+    if (phi0) memcpy(phi0, p0, sizeof(double) * (size_t)(K * V));
+    if (phig) {
+        for (int64_t g = 0; g < G; ++g)
+            for (int64_t k = 0; k < K; ++k) {
+                const double N = (double)c->Ngk[g * K + k], T = (double)c->Tgk[g * K + k];
+                for (int64_t w = 0; w < V; ++w) {
+                    const int64_t cell = (g * K + k) * V + w, q = arow(m, g, w);
+                    double base = 0.0;
+                    for (int64_t e = A->row_off[q]; e < A->row_off[q + 1]; ++e)
+                        base += A->p[e] * p0[k * V + A->src[e]];
+                    phig[cell] = ((double)c->n[cell] - m->a * (double)c->t[cell] +
+                                  (m->b + m->a * T) * base) /
+                                 (m->b + N);
+                }
+            }
+    }
+    free(p0);
+}
+
+/* Chain histogram with associations: a state is encoded per token with the  */
+/* digit (S + 1) z + (r ? s : S) in base K (S + 1) (least significant first). */
+int or_chain_histogram_assoc(const or_model *m, const or_assoc *A, or_counts *c, int32_t *z,
+                             uint8_t *r, uint8_t *s, uint32_t first_sweep, int64_t n_sweeps,
+                             uint64_t seed, int mode, int64_t *hist, int64_t n_bins)
+{
+    const int64_t S1 = A->S + 1, base = (int64_t)m->K * S1;
+    for (int64_t sw = 0; sw < n_sweeps; ++sw) {
+        if (or_sweep_assoc(m, A, c, z, r, s, first_sweep + (uint32_t)sw, seed, mode, NULL) != 0)
+            return -1;
+        int64_t code = 0, mul = 1;
+        for (int64_t i = 0; i < m->n_tokens; ++i) {
+            code += (S1 * (int64_t)z[i] + (r[i] ? s[i] : A->S)) * mul;
+            mul *= base;
+        }
+        if (code < 0 || code >= n_bins) return -2;
+        hist[code] += 1;
+    }
+    return 0;
+}

@@ -158,6 +158,46 @@ def true_phi0(w: Workload, seed: int = 0) -> np.ndarray:
     return out
 
 
+def associations(n_groups: int, vocab: int, S: int, eps: float, seed: int = 0):
+    """Sparse word-association matrices P^g, one per group (the transformation
+    matrices of the model with word associations): P^g = (1 - eps) I +
+    eps / (S - 1) sum_{j < S-1} Pi_{g,j}, with Pi a seeded random permutation
+    matrix (Pi[w][v] = 1 iff w = pi(v)), so every row and every column sums to
+    one and row w lists at most S sources: w itself, then pi_j^{-1}(w) for
+    j = 0, 1, ... (a repeated source is merged into its first entry).  S = 1
+    gives the identity.  Returns CSR arrays over the rows (g, w) in order:
+    (row_off [G V + 1] int64, src [nnz] int32, p [nnz] float64)."""
+    if S < 1 or not 0.0 <= eps < 1.0:
+        raise ValueError("need S >= 1 and 0 <= eps < 1")
+    rng = np.random.default_rng([seed, 0xA550C])
+    rows_src, rows_p, lens = [], [], []
+    w = np.arange(vocab)
+    for _ in range(n_groups):
+        cand = np.empty((vocab, S), dtype=np.int64)
+        val = np.empty((vocab, S), dtype=np.float64)
+        cand[:, 0], val[:, 0] = w, (1.0 - eps) if S > 1 else 1.0
+        for j in range(1, S):
+            perm = rng.permutation(vocab)
+            inv = np.empty(vocab, dtype=np.int64)
+            inv[perm] = w
+            cand[:, j], val[:, j] = inv, eps / (S - 1)
+        keep = np.ones((vocab, S), dtype=bool)
+        for j in range(1, S):
+            for i in range(j):
+                same = keep[:, j] & (cand[:, j] == cand[:, i]) & keep[:, i]
+                val[same, i] += val[same, j]
+                keep[same, j] = False
+        lens.append(keep.sum(1))
+        rows_src.append(cand[keep])
+        rows_p.append(val[keep])
+    lens = np.concatenate(lens) if n_groups else np.zeros(0, dtype=np.int64)
+    row_off = np.zeros(n_groups * vocab + 1, dtype=np.int64)
+    np.cumsum(lens, out=row_off[1:])
+    src = np.concatenate(rows_src).astype(np.int32) if n_groups else np.zeros(0, np.int32)
+    p = np.concatenate(rows_p) if n_groups else np.zeros(0, np.float64)
+    return row_off, src, p
+
+
 def split_heldout(cp: Corpus, frac: float = 0.1):
     """(train, test): the last floor(frac * docs) documents of every group held out,
     as the thesis holds out 10% of each group for perplexity; both keep corpus

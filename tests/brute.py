@@ -85,3 +85,44 @@ def p_W_given_Z(words, doc_off, doc_group, z, G, K, V, a, b, gamma):
 def log_p_WZ(words, doc_off, doc_group, z, G, K, V, alpha, a, b, gamma):
     return log_p_Z(doc_off, z, K, alpha) + math.log(
         p_W_given_Z(words, doc_off, doc_group, z, G, K, V, a, b, gamma))
+
+
+def p_W_given_Z_assoc(words, doc_off, doc_group, z, G, K, V, a, b, gamma, assoc):
+    """p(W | Z) of the model with word associations, by the same enumeration:
+    a new table of group g first draws its source v from the Polya urn of its
+    topic's shadow base (counts kept per source), then serves word w with
+    probability p_{g,w,v} (column v of P^g); every source choice of every
+    table is summed over.  `assoc[(g, w)]` maps source v -> p_{g,w,v}."""
+    rest = {}
+    for d in range(len(doc_off) - 1):
+        g = doc_group[d]
+        for i in range(doc_off[d], doc_off[d + 1]):
+            rest.setdefault((g, z[i]), []).append(i)
+    keys = sorted(rest)
+    per_rest = [_seatings([words[i] for i in rest[key]]) for key in keys]
+    total = 0.0
+    for combo in itertools.product(*per_rest):
+        p_seat = 1.0
+        tables = []  # (g, k, w) of every new table, in order
+        for key, seat in zip(keys, combo):
+            g, k = key
+            sizes = []
+            for c_idx, (i, tb) in enumerate(zip(rest[key], seat)):
+                if tb == len(sizes):
+                    p_seat *= (b + a * len(sizes)) / (b + c_idx)
+                    tables.append((g, k, words[i]))
+                    sizes.append(1)
+                else:
+                    p_seat *= (sizes[tb] - a) / (b + c_idx)
+                    sizes[tb] += 1
+        choices = [sorted(assoc[(g, w)].items()) for g, _, w in tables]
+        for pick in itertools.product(*choices):
+            p = p_seat
+            B = {}
+            Bk = [0] * K
+            for (g, k, w), (v, pv) in zip(tables, pick):
+                p *= (gamma + B.get((k, v), 0)) / (V * gamma + Bk[k]) * pv
+                B[(k, v)] = B.get((k, v), 0) + 1
+                Bk[k] += 1
+            total += p
+    return total
