@@ -48,11 +48,12 @@ def dense_bytes_per_token(K: int) -> int:
 def recorded_traffic(workload: str):
     """HBM bytes per k_sample launch measured with rocprofv3 counters, if they
     were taken on the current sampler source (profiles/traffic_*.txt holds
-    the figure with the SHA-256 of sample.hip at the time), else None."""
+    the figure with the SHA-256 of sample.hip followed by sampler_common.hpp
+    at the time), else None."""
     import hashlib
 
     path = os.path.join(ROOT, "profiles", f"traffic_k_sample_{workload}.txt")
-    src = os.path.join(ROOT, "paper_1510_06549_amd", "csrc", "sample.hip")
+    csrc = os.path.join(ROOT, "paper_1510_06549_amd", "csrc")
     if not os.path.exists(path):
         return None
     kv = {}
@@ -60,7 +61,10 @@ def recorded_traffic(workload: str):
         if ":" in line and not line.startswith("#"):
             k, v = line.split(":", 1)
             kv[k.strip()] = v.strip()
-    sha = hashlib.sha256(open(src, "rb").read()).hexdigest()
+    h = hashlib.sha256()
+    for name in ("sample.hip", "sampler_common.hpp"):
+        h.update(open(os.path.join(csrc, name), "rb").read())
+    sha = h.hexdigest()
     if kv.get("sample_hip_sha256") != sha or "bytes_per_launch" not in kv:
         return None
     return float(kv["bytes_per_launch"])

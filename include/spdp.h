@@ -53,6 +53,7 @@ extern "C" {
 #define SPDP_E_STATE (-5) /* an invariant of the count state is violated         */
 
 #define SPDP_MAX_K 1024
+#define SPDP_MAX_SOURCES 8 /* longest source list of a word association row */
 
 typedef struct spdp_state spdp_state; /* opaque */
 
@@ -74,6 +75,24 @@ typedef struct {
 } spdp_groups;
 
 /*
+ * Word associations: the transformation matrices P^g of the full SPDP model
+ * (chapter "Shared Topic Modelling Using Shadow Poisson Dirichlet Process":
+ * group g's topic k is a Pitman-Yor process around P^g phi0_k, so a new table
+ * takes a source word v from the shadow base and serves word w with
+ * probability p_{g,w,v}; Eq. SPDP-joint-prob-with-v).  P^g is given sparse, by
+ * rows: row q = g V + w lists the sources v with p_{g,w,v} > 0 in entries
+ * [row_off[q], row_off[q + 1]).  Column v of P^g is meant to be a
+ * distribution over words (the sampler does not need it; the group estimate
+ * then sums to one).
+ */
+typedef struct {
+    int32_t max_sources;        /* S: the longest row, 1 <= S <= SPDP_MAX_SOURCES   */
+    const int64_t *row_off;     /* host [G V + 1], [0] = 0, every row non-empty       */
+    const int32_t *src;         /* host [nnz] source words, 0 <= v < V, distinct per row */
+    const double *p;            /* host [nnz] p_{g,w,v}, finite and > 0               */
+} spdp_assoc;
+
+/*
  * Create a sampler state: validate, upload the corpus, tabulate the
  * generalised Stirling numbers S^n_{t,a} (recurrence of the PYP joint,
  * Corollary 17 passage) in fp64 log space for every n the corpus can reach,
@@ -92,6 +111,22 @@ int spdp_create(const spdp_corpus *corpus, const spdp_groups *groups, int32_t K,
                 double a, double b, double gamma, spdp_state **out);
 
 /*
+ * The same for the model with word associations (`assoc`, copied at the
+ * call).  Each table head then carries a source word, stored as its slot s in
+ * its row's list (0 <= s < the row's length), and the shadow-base counts are
+ * keyed by source: B[v][k] counts the heads of topic k whose source is v.
+ * Initialisation and repair give a new head its row's most probable source
+ * (the first on ties).  Every entry point below works on such a state, with
+ * the differences stated there.  Errors: as spdp_create, and E_ARG for a bad
+ * association list (an empty or over-long row, a source out of range or
+ * repeated in its row, p not finite and > 0, max_sources not the longest
+ * row).
+ */
+int spdp_create_assoc(const spdp_corpus *corpus, const spdp_groups *groups,
+                      const spdp_assoc *assoc, int32_t K, double alpha, double a, double b,
+                      double gamma, spdp_state **out);
+
+/*
  * One Gibbs sweep (asynchronous on the state's stream): every token's (z, r)
  * is resampled from the 2K outcomes of Eq. SPDP-sampling-w-z-r0/-r1, with the
  * shared counts of the sweep start and the live row of its own document;
@@ -101,6 +136,14 @@ int spdp_create(const spdp_corpus *corpus, const spdp_groups *groups, int32_t K,
  * only head of a cell with other customers keeps its state.  Counts are then
  * updated exactly and every cell left with customers but no table gets its
  * smallest-index token as head.  Errors: E_ARG, E_HIP.
+ * With word associations a token has K (S + 1) outcomes, per topic k the head
+ * outcomes (k, r = 1, slot s) for s = 0 .. S - 1, then (k, r = 0):
+ *   j = k (S + 1) + s is (k, 1, s),  j = k (S + 1) + S is (k, 0),
+ * with W(k, 1, s) = p_{g,w,v_s} times the plain r = 1 weight evaluated on the
+ * shadow-base count of source v_s (Eq. SPDP-sampling-w-z-r1 with p_{i,w,v});
+ * slots past a row's length weigh 0.  The only head of a cell with other
+ * customers keeps its topic and r but redraws its source, in proportion to
+ * p_{g,w,v} (gamma + B'[v][k]).
  */
 int spdp_sweep(spdp_state *s, uint32_t sweep, uint64_t seed);
 
@@ -114,7 +157,8 @@ int spdp_counts(const spdp_state *s, int32_t g_begin, int32_t g_end, int32_t *n_
 
 /*
  * Export the totals: customers N[g][k] = sum_w n, tables T[g][k] = sum_w t,
- * shadow-base table counts B[w][k] = sum_g t and B[k] = sum_w B[w][k].
+ * shadow-base table counts B[w][k] = sum_g t and B[k] = sum_w B[w][k] (with
+ * word associations B[v][k] counts the heads of topic k whose source is v).
  * Any pointer may be NULL.  Synchronises.  Errors: E_ARG, E_HIP.
  */
 int spdp_totals(const spdp_state *s, int32_t *N_gk, int32_t *T_gk, int32_t *B_wk, int32_t *B_k,
@@ -125,7 +169,9 @@ int spdp_totals(const spdp_state *s, int32_t *N_gk, int32_t *T_gk, int32_t *B_wk
  * collapsed joint of the thesis's blocked-Gibbs derivation with P = I):
  * document Dirichlet-multinomial terms, per-restaurant (b|a)_T / (b)_N,
  * per-cell S^n_{t,a} / C(n, t), and the shadow-base Dirichlet-multinomial of
- * each topic.  Deterministic reduction order.  Synchronises.
+ * each topic; with word associations the base counts are keyed by source and
+ * the sum over table heads of log p_{g,w,v} of the head's source is added.
+ * Deterministic reduction order.  Synchronises.
  * Errors: E_ARG, E_HIP, E_STATE (a cell with t > n or t = 0 < n).
  */
 int spdp_loglik(spdp_state *s, double *out);
@@ -142,7 +188,9 @@ void spdp_destroy(spdp_state *s);
  *   phi   [g_end - g_begin][V][K]
  *                  phi[g][w][k] = (n - a t + (b + a T_gk) phi0[w][k]) / (b + N_gk)
  * (the base weight b + a T is the Pitman-Yor seating rule's; the printed
- * a T does not normalise).  Any pointer may be NULL; the group range applies
+ * a T does not normalise).  With word associations phi0 is over source words
+ * and the group's base is P^g phi0: phi0[w][k] above is replaced by
+ * sum_v p_{g,w,v} phi0[v][k].  Any pointer may be NULL; the group range applies
  * to phi only.  `where` as for spdp_counts.  Synchronises.
  * Errors: E_ARG (bad range), E_HIP.
  */
@@ -214,12 +262,28 @@ int spdp_get_assignments(const spdp_state *s, int32_t *z, uint8_t *r, int where)
 int spdp_set_assignments(spdp_state *s, const int32_t *z, const uint8_t *r, int where);
 
 /*
+ * Word associations: export the source slot of every token's table ([N]
+ * uint8, 0 for r = 0), or resume from (z, r, slot) (as spdp_set_assignments;
+ * a head's slot must index a source of its row, r = 0 tokens store slot 0).
+ * spdp_set_assignments on such a state gives every head slot 0.  *S receives
+ * the longest source list (0 for a state without associations).
+ * Synchronise.  Errors: E_ARG (null pointer, a state without associations for
+ * the resume, a value out of range), E_HIP.
+ */
+int spdp_get_slots(const spdp_state *s, uint8_t *slot, int where);
+int spdp_set_assignments_assoc(spdp_state *s, const int32_t *z, const uint8_t *r,
+                               const uint8_t *slot, int where);
+int spdp_max_sources(const spdp_state *s, int32_t *S);
+
+/*
  * Test hook: run the sampling step of sweep (sweep, seed) on the current state
  * WITHOUT committing it, and export, for tokens i in [tok_begin, tok_end), the
  * fp32 unnormalised weights of all 2K outcomes (w_out, [(tok_end - tok_begin)
  * * 2K], outcome order as in spdp_sweep), the uniform (u_out, -1 for a token
  * kept by the sole-head rule) and the sampled packed outcome (zr_out, value
- * 2 z + r, may be NULL).  With w_out and u_out both NULL no trace is kept and
+ * 2 z + r, may be NULL).  With word associations w_out holds K (S + 1)
+ * weights per token, every token draws (no -1), and zr_out holds
+ * s << 16 | 2 z + r.  With w_out and u_out both NULL no trace is kept and
  * any token range may be requested (the sampled state before the count update
  * and repair).  Uses the same kernel as spdp_sweep.  Synchronises.
  * Errors: E_ARG, E_NOMEM, E_HIP.

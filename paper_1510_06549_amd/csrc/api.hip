@@ -1,5 +1,6 @@
 // api.hip -- the extern "C" boundary (declared in include/spdp.h): argument
 // validation, device memory, error mapping and the order of kernel launches.
+#include <algorithm>
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
@@ -124,8 +125,13 @@ int rebuild_state(spdp_state *s)
     const Model &m = s->m;
     DeviceBuffers &b = s->b;
     int32_t *zr = b.zr[s->cur];
-    HIP_TRY(launch_rows(m, b, zr, s->st));
-    HIP_TRY(launch_base(m, b, s->st));
+    if (m.Sp > 0) {
+        HIP_TRY(launch_rows_assoc(m, b, zr, s->st));
+        HIP_TRY(launch_base16(m, b, s->st));
+    } else {
+        HIP_TRY(launch_rows(m, b, zr, s->st));
+        HIP_TRY(launch_base(m, b, s->st));
+    }
     HIP_TRY(launch_totals(m, b, zr, s->st));
     if (m.N > 0)
         HIP_TRY(hipMemcpyAsync(b.zr[1 - s->cur], zr, (size_t)m.N * sizeof(int32_t),
@@ -139,6 +145,82 @@ int check_device_flags(spdp_state *s, int32_t *host_err)
     return sync(s);
 }
 
+// Word associations: validate the source lists of the G V rows and build the
+// padded device records (Sp slots per row; a padding slot repeats the row's
+// first source with p = 0), the fp64 p and the repair's head slot per row.
+int check_assoc(const spdp_assoc *A, int32_t G, int32_t V)
+{
+    if (A->max_sources < 1 || A->max_sources > SPDP_MAX_SOURCES)
+        return fail(SPDP_E_ARG, "max_sources must be in [1, %d]", SPDP_MAX_SOURCES);
+    if (!A->row_off || !A->src || !A->p) return fail(SPDP_E_ARG, "null association array");
+    const int64_t rows = (int64_t)G * V;
+    if (A->row_off[0] != 0) return fail(SPDP_E_ARG, "association row_off must start at 0");
+    int32_t longest = 0;
+    for (int64_t q = 0; q < rows; ++q) {
+        const int64_t b0 = A->row_off[q], b1 = A->row_off[q + 1];
+        if (b1 <= b0) return fail(SPDP_E_ARG, "association row %lld has no source", (long long)q);
+        if (b1 - b0 > A->max_sources)
+            return fail(SPDP_E_ARG, "association row %lld lists more than max_sources sources",
+                        (long long)q);
+        longest = std::max<int32_t>(longest, (int32_t)(b1 - b0));
+        for (int64_t e = b0; e < b1; ++e) {
+            if (A->src[e] < 0 || A->src[e] >= V)
+                return fail(SPDP_E_ARG, "association source out of [0, vocab) in row %lld",
+                            (long long)q);
+            if (!(A->p[e] > 0.0) || !std::isfinite(A->p[e]))
+                return fail(SPDP_E_ARG, "association p must be finite and > 0 (row %lld)",
+                            (long long)q);
+            for (int64_t f = b0; f < e; ++f)
+                if (A->src[f] == A->src[e])
+                    return fail(SPDP_E_ARG, "association row %lld repeats source %d",
+                                (long long)q, A->src[e]);
+        }
+    }
+    if (longest != A->max_sources)
+        return fail(SPDP_E_ARG, "max_sources (%d) is not the longest row (%d)", A->max_sources,
+                    longest);
+    return SPDP_OK;
+}
+
+int upload_assoc(spdp_state *s, const spdp_assoc *A)
+{
+    Model &m = s->m;
+    DeviceBuffers &B = s->b;
+    m.S = A->max_sources;
+    m.Sp = m.S <= 1 ? 1 : (m.S <= 2 ? 2 : (m.S <= 4 ? 4 : 8));
+    const int64_t rows = (int64_t)m.G * m.V;
+    std::vector<int32_t> rec((size_t)(rows * 2 * m.Sp));
+    std::vector<double> p64((size_t)(rows * m.Sp), 0.0);
+    std::vector<uint8_t> hs((size_t)rows);
+    for (int64_t q = 0; q < rows; ++q) {
+        const int64_t b0 = A->row_off[q], n = A->row_off[q + 1] - b0;
+        int32_t *r = rec.data() + q * 2 * m.Sp;
+        int32_t best = 0;
+        for (int32_t sl = 0; sl < m.Sp; ++sl) {
+            const bool real = sl < n;
+            const float pf = real ? (float)A->p[b0 + sl] : 0.0f;
+            r[sl] = A->src[b0 + (real ? sl : 0)];
+            std::memcpy(&r[m.Sp + sl], &pf, sizeof pf);
+            p64[(size_t)(q * m.Sp + sl)] = real ? A->p[b0 + sl] : 0.0;
+            if (real && A->p[b0 + sl] > A->p[b0 + best]) best = sl;
+        }
+        hs[(size_t)q] = (uint8_t)best;
+    }
+    int rc;
+    if ((rc = dev_alloc(s, &B.srcrec, rows * 2 * m.Sp, "association records")) != SPDP_OK) return rc;
+    if ((rc = dev_alloc(s, &B.p64, rows * m.Sp, "association p")) != SPDP_OK) return rc;
+    if ((rc = dev_alloc(s, &B.head_slot, rows, "head slots")) != SPDP_OK) return rc;
+    HIP_TRY(hipMemcpyAsync(B.srcrec, rec.data(), rec.size() * sizeof(int32_t),
+                           hipMemcpyHostToDevice, s->st));
+    HIP_TRY(hipMemcpyAsync(B.p64, p64.data(), p64.size() * sizeof(double), hipMemcpyHostToDevice,
+                           s->st));
+    HIP_TRY(hipMemcpyAsync(B.head_slot, hs.data(), hs.size(), hipMemcpyHostToDevice, s->st));
+    return sync(s);  // the host vectors go out of scope
+}
+
+int create_state(const spdp_corpus *corpus, const spdp_groups *groups, const spdp_assoc *assoc,
+                 int32_t K, double alpha, double a, double b, double gamma, spdp_state **out);
+
 }  // namespace
 
 extern "C" {
@@ -149,6 +231,25 @@ int spdp_create(const spdp_corpus *corpus, const spdp_groups *groups, int32_t K,
                 double a, double b, double gamma, spdp_state **out)
 {
     g_last_error.clear();
+    return create_state(corpus, groups, nullptr, K, alpha, a, b, gamma, out);
+}
+
+int spdp_create_assoc(const spdp_corpus *corpus, const spdp_groups *groups,
+                      const spdp_assoc *assoc, int32_t K, double alpha, double a, double b,
+                      double gamma, spdp_state **out)
+{
+    g_last_error.clear();
+    if (!assoc) return fail(SPDP_E_ARG, "assoc is NULL");
+    return create_state(corpus, groups, assoc, K, alpha, a, b, gamma, out);
+}
+
+}  // extern "C"
+
+namespace {
+
+int create_state(const spdp_corpus *corpus, const spdp_groups *groups, const spdp_assoc *assoc,
+                 int32_t K, double alpha, double a, double b, double gamma, spdp_state **out)
+{
     if (!out) return fail(SPDP_E_ARG, "out is NULL");
     *out = nullptr;
     if (!corpus || !groups) return fail(SPDP_E_ARG, "corpus or groups is NULL");
@@ -170,6 +271,10 @@ int spdp_create(const spdp_corpus *corpus, const spdp_groups *groups, int32_t K,
     if (off[0] != 0 || off[D] != N) return fail(SPDP_E_ARG, "doc_offsets must start at 0 and end at N");
     for (int32_t d = 0; d < D; ++d)
         if (off[d + 1] < off[d]) return fail(SPDP_E_ARG, "doc_offsets not nondecreasing at %d", d);
+    if (assoc) {
+        const int rca = check_assoc(assoc, G, V);
+        if (rca != SPDP_OK) return rca;
+    }
 
     spdp_state *s = new (std::nothrow) spdp_state();
     if (!s) return fail(SPDP_E_NOMEM, "host allocation failed");
@@ -282,6 +387,9 @@ int spdp_create(const spdp_corpus *corpus, const spdp_groups *groups, int32_t K,
         TRY_HIP(e);
     }
 
+    // word associations
+    if (assoc) TRY(upload_assoc(s, assoc));
+
     // Stirling cache
     const int64_t n_logS = tri_index(m.ncap + 1, 0);  // rows 0..ncap
     const int64_t n_Q = tri_index(m.ncap, 0);         // rows 0..ncap-1
@@ -323,6 +431,9 @@ int spdp_create(const spdp_corpus *corpus, const spdp_groups *groups, int32_t K,
         x.gamma = gamma;
         x.K = K;
         x.ncap = m.ncap;
+        x.srcrec = B.srcrec;
+        x.p64 = B.p64;
+        x.Sp = m.Sp;
         TRY_HIP(hipMemcpyAsync(B.exact, &x, sizeof x, hipMemcpyHostToDevice, s->st));
         TRY_HIP(hipStreamSynchronize(s->st));
     }
@@ -338,6 +449,10 @@ int spdp_create(const spdp_corpus *corpus, const spdp_groups *groups, int32_t K,
     return SPDP_OK;
 }
 
+}  // namespace
+
+extern "C" {
+
 void spdp_destroy(spdp_state *s) { free_state(s); }
 
 int spdp_sweep(spdp_state *s, uint32_t sweep, uint64_t seed)
@@ -349,12 +464,26 @@ int spdp_sweep(spdp_state *s, uint32_t sweep, uint64_t seed)
     int32_t *zr_old = b.zr[s->cur], *zr_new = b.zr[1 - s->cur];
     int rc;
     if ((rc = timed(s, 3, [&] { return launch_factors(m, b, s->st); })) != SPDP_OK) return rc;
-    if ((rc = timed(s, 0, [&] {
-             return launch_sample(m, b, zr_old, zr_new, sweep, seed, nullptr, nullptr, 0, 0, s->st);
-         })) != SPDP_OK)
-        return rc;
-    if ((rc = timed(s, 1, [&] { return launch_rows(m, b, zr_new, s->st); })) != SPDP_OK) return rc;
-    if ((rc = timed(s, 2, [&] { return launch_base(m, b, s->st); })) != SPDP_OK) return rc;
+    if (m.Sp > 0) {
+        // word associations: source-keyed shadow base, rebuilt by the row pass
+        if ((rc = timed(s, 0, [&] {
+                 return launch_sample_assoc(m, b, zr_old, zr_new, sweep, seed, nullptr, nullptr,
+                                            0, 0, s->st);
+             })) != SPDP_OK)
+            return rc;
+        if ((rc = timed(s, 1, [&] { return launch_rows_assoc(m, b, zr_new, s->st); })) != SPDP_OK)
+            return rc;
+        if ((rc = timed(s, 2, [&] { return launch_base16(m, b, s->st); })) != SPDP_OK) return rc;
+    } else {
+        if ((rc = timed(s, 0, [&] {
+                 return launch_sample(m, b, zr_old, zr_new, sweep, seed, nullptr, nullptr, 0, 0,
+                                      s->st);
+             })) != SPDP_OK)
+            return rc;
+        if ((rc = timed(s, 1, [&] { return launch_rows(m, b, zr_new, s->st); })) != SPDP_OK)
+            return rc;
+        if ((rc = timed(s, 2, [&] { return launch_base(m, b, s->st); })) != SPDP_OK) return rc;
+    }
     if ((rc = timed(s, 3, [&] { return launch_totals(m, b, zr_new, s->st); })) != SPDP_OK) return rc;
     s->cur = 1 - s->cur;
     return SPDP_OK;
@@ -624,44 +753,105 @@ int spdp_get_assignments(const spdp_state *s, int32_t *z, uint8_t *r, int where)
     return SPDP_OK;
 }
 
-int spdp_set_assignments(spdp_state *s, const int32_t *z, const uint8_t *r, int where)
+}  // extern "C"
+
+namespace {
+
+// Replace the state by (z, r[, s]) and rebuild; slots only with associations.
+int set_state(spdp_state *s, const int32_t *z, const uint8_t *r, const uint8_t *sl, int where)
 {
-    if (!s || !z || !r) return fail(SPDP_E_ARG, "null argument");
     if (where != 0 && where != 1) return fail(SPDP_E_ARG, "where must be 0 or 1");
     HIP_TRY(hipSetDevice(s->device));
     const Model &m = s->m;
     if (m.N > 0) {
         const int32_t *zd = z;
-        const uint8_t *rd = r;
+        const uint8_t *rd = r, *sd = sl;
         int32_t *zt = nullptr;
-        uint8_t *rt = nullptr;
+        uint8_t *rt = nullptr, *st8 = nullptr;
+        auto release = [&]() {
+            if (zt) hipFree(zt);
+            if (rt) hipFree(rt);
+            if (st8) hipFree(st8);
+        };
         if (where == 0) {
-            HIP_TRY(hipMalloc(&zt, (size_t)m.N * sizeof(int32_t)));
-            hipError_t e = hipMalloc(&rt, (size_t)m.N);
+            hipError_t e = hipMalloc(&zt, (size_t)m.N * sizeof(int32_t));
+            if (e == hipSuccess) e = hipMalloc(&rt, (size_t)m.N);
+            if (e == hipSuccess && sl) e = hipMalloc(&st8, (size_t)m.N);
             if (e == hipSuccess)
                 e = hipMemcpyAsync(zt, z, (size_t)m.N * 4, hipMemcpyHostToDevice, s->st);
             if (e == hipSuccess) e = hipMemcpyAsync(rt, r, (size_t)m.N, hipMemcpyHostToDevice, s->st);
+            if (e == hipSuccess && sl)
+                e = hipMemcpyAsync(st8, sl, (size_t)m.N, hipMemcpyHostToDevice, s->st);
             if (e != hipSuccess) {
-                hipFree(zt);
-                if (rt) hipFree(rt);
+                release();
                 HIP_TRY(e);
             }
             zd = zt;
             rd = rt;
+            sd = st8;
         }
         HIP_TRY(launch_fill_i32(s->b.err, 2, 0, s->st));
-        hipError_t e = launch_pack_zr(m, zd, rd, s->b.zr[s->cur], s->b.err, s->st);
+        hipError_t e = m.Sp > 0 ? launch_pack_zrs(m, s->b, zd, rd, sd, s->b.zr[s->cur], s->b.err, s->st)
+                                : launch_pack_zr(m, zd, rd, s->b.zr[s->cur], s->b.err, s->st);
         int32_t herr[2] = {0, 0};
         if (e == hipSuccess) e = hipMemcpyAsync(herr, s->b.err, sizeof herr, hipMemcpyDeviceToHost, s->st);
         if (e == hipSuccess) e = hipStreamSynchronize(s->st);
-        if (zt) hipFree(zt);
-        if (rt) hipFree(rt);
+        release();
         HIP_TRY(e);
-        if (herr[0] & 4) return fail(SPDP_E_ARG, "z out of [0, K) or r not in {0, 1}");
+        if (herr[0] & 4)
+            return fail(SPDP_E_ARG, m.Sp > 0 ? "z out of [0, K), r not in {0, 1}, or a head's "
+                                               "slot is not a source of its row"
+                                             : "z out of [0, K) or r not in {0, 1}");
     }
     int rc = rebuild_state(s);
     if (rc != SPDP_OK) return rc;
     return sync(s);
+}
+
+}  // namespace
+
+extern "C" {
+
+int spdp_set_assignments(spdp_state *s, const int32_t *z, const uint8_t *r, int where)
+{
+    if (!s || !z || !r) return fail(SPDP_E_ARG, "null argument");
+    return set_state(s, z, r, nullptr, where);
+}
+
+int spdp_set_assignments_assoc(spdp_state *s, const int32_t *z, const uint8_t *r,
+                               const uint8_t *slot, int where)
+{
+    if (!s || !z || !r || !slot) return fail(SPDP_E_ARG, "null argument");
+    if (s->m.Sp == 0) return fail(SPDP_E_ARG, "the state has no word associations");
+    return set_state(s, z, r, slot, where);
+}
+
+int spdp_get_slots(const spdp_state *s, uint8_t *slot, int where)
+{
+    if (!s || !slot) return fail(SPDP_E_ARG, "null argument");
+    if (where != 0 && where != 1) return fail(SPDP_E_ARG, "where must be 0 or 1");
+    HIP_TRY(hipSetDevice(s->device));
+    const Model &m = s->m;
+    if (m.N == 0) return SPDP_OK;
+    if (where == 1) {
+        HIP_TRY(launch_unpack_slot(m, s->b.zr[s->cur], slot, s->st));
+        return sync(s);
+    }
+    uint8_t *sd = nullptr;
+    HIP_TRY(hipMalloc(&sd, (size_t)m.N));
+    hipError_t e = launch_unpack_slot(m, s->b.zr[s->cur], sd, s->st);
+    if (e == hipSuccess) e = hipMemcpyAsync(slot, sd, (size_t)m.N, hipMemcpyDeviceToHost, s->st);
+    if (e == hipSuccess) e = hipStreamSynchronize(s->st);
+    hipFree(sd);
+    HIP_TRY(e);
+    return SPDP_OK;
+}
+
+int spdp_max_sources(const spdp_state *s, int32_t *S)
+{
+    if (!s || !S) return fail(SPDP_E_ARG, "null argument");
+    *S = s->m.S;
+    return SPDP_OK;
 }
 
 int spdp_debug_conditionals(spdp_state *s, uint32_t sweep, uint64_t seed, int64_t tok_begin,
@@ -677,6 +867,8 @@ int spdp_debug_conditionals(spdp_state *s, uint32_t sweep, uint64_t seed, int64_
     DeviceBuffers &b = s->b;
     const int64_t T = tok_end - tok_begin;
     if (T == 0) return SPDP_OK;
+    // outcomes per token: 2K, or K (S + 1) with word associations
+    const int64_t nout = m.Sp > 0 ? (int64_t)m.K * (m.S + 1) : 2 * (int64_t)m.K;
     if (!b.zr_dbg) {
         void *p = nullptr;
         if (hipMalloc(&p, (size_t)m.N * sizeof(int32_t)) != hipSuccess) {
@@ -693,7 +885,7 @@ int spdp_debug_conditionals(spdp_state *s, uint32_t sweep, uint64_t seed, int64_
         b.tr_u = nullptr;
         b.tr_cap = 0;
         void *p = nullptr;
-        if (hipMalloc(&p, (size_t)T * 2 * m.K * sizeof(float)) != hipSuccess) {
+        if (hipMalloc(&p, (size_t)(T * nout) * sizeof(float)) != hipSuccess) {
             (void)hipGetLastError();
             return fail(SPDP_E_NOMEM, "trace buffer");
         }
@@ -706,15 +898,19 @@ int spdp_debug_conditionals(spdp_state *s, uint32_t sweep, uint64_t seed, int64_
         b.tr_cap = T;
     }
     if (trace) {
-        HIP_TRY(launch_fill_i32((int32_t *)b.tr_w, T * 2 * m.K, 0, s->st));
+        HIP_TRY(launch_fill_i32((int32_t *)b.tr_w, T * nout, 0, s->st));
         HIP_TRY(launch_fill_i32((int32_t *)b.tr_u, T, 0, s->st));
     }
     int32_t *zr_old = b.zr[s->cur], *zr_tmp = b.zr_dbg;
     HIP_TRY(launch_factors(m, b, s->st));
-    HIP_TRY(launch_sample(m, b, zr_old, zr_tmp, sweep, seed, trace ? b.tr_w : nullptr,
-                          trace ? b.tr_u : nullptr, tok_begin, tok_end, s->st));
+    if (m.Sp > 0)
+        HIP_TRY(launch_sample_assoc(m, b, zr_old, zr_tmp, sweep, seed, trace ? b.tr_w : nullptr,
+                                    trace ? b.tr_u : nullptr, tok_begin, tok_end, s->st));
+    else
+        HIP_TRY(launch_sample(m, b, zr_old, zr_tmp, sweep, seed, trace ? b.tr_w : nullptr,
+                              trace ? b.tr_u : nullptr, tok_begin, tok_end, s->st));
     const hipMemcpyKind kind = where ? hipMemcpyDeviceToDevice : hipMemcpyDeviceToHost;
-    if (w_out) HIP_TRY(hipMemcpyAsync(w_out, b.tr_w, (size_t)T * 2 * m.K * 4, kind, s->st));
+    if (w_out) HIP_TRY(hipMemcpyAsync(w_out, b.tr_w, (size_t)(T * nout) * 4, kind, s->st));
     if (u_out) HIP_TRY(hipMemcpyAsync(u_out, b.tr_u, (size_t)T * 4, kind, s->st));
     if (zr_out) HIP_TRY(hipMemcpyAsync(zr_out, zr_tmp + tok_begin, (size_t)T * 4, kind, s->st));
     return sync(s);

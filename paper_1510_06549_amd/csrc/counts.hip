@@ -15,6 +15,10 @@
 //   k_base      shadow-base table counts B[w][k] = sum_g t[g][w][k], and the
 //               16-bit copy the sampler reads (with a flag raised when a count
 //               does not fit, in which case the sampler reads B itself)
+//   k_rows_assoc / k_base16
+//               the same with word associations: shadow-base counts keyed by
+//               each head's source word, and a promoted head takes its row's
+//               most probable source
 //   k_unpack    export of n and t as separate int32 arrays
 #include <hipcub/hipcub.hpp>
 
@@ -91,6 +95,84 @@ __global__ void __launch_bounds__(64) k_rows(int32_t Kp, const int32_t *__restri
     }
     for (int o = 32; o > 0; o >>= 1) rep += __shfl_xor(rep, o);
     if (lane == 0) rep_part[q] = rep;
+}
+
+// Word associations: the same per-row rebuild, where a promoted head takes
+// the row's most probable source (head_slot[q]) and every head adds one to
+// the shadow-base count of its source, B[src][k] (zeroed before; integer
+// atomics, so the result does not depend on their order).
+__global__ void __launch_bounds__(64) k_rows_assoc(int32_t Kp, int32_t Sp,
+                                                   const int32_t *__restrict__ row_off,
+                                                   const int32_t *__restrict__ perm,
+                                                   const int32_t *__restrict__ srcrec,
+                                                   const uint8_t *__restrict__ head_slot,
+                                                   int32_t *__restrict__ zr,
+                                                   int32_t *__restrict__ nt,
+                                                   int32_t *__restrict__ B,
+                                                   uint32_t *__restrict__ rep_part)
+{
+    __shared__ int32_t h[SPDP_MAX_K];
+    __shared__ int32_t first[SPDP_MAX_K];
+    const int64_t q = blockIdx.x;
+    const int32_t lane = threadIdx.x;
+    const int32_t rs = row_off[q], re = row_off[q + 1];
+    const int32_t *__restrict__ src = srcrec + q * 2 * Sp;
+    uint32_t rep = 0;
+    if (rs < re) {
+        for (int32_t k = lane; k < Kp; k += 64) h[k] = 0;
+        __syncthreads();
+        for (int32_t j = rs + lane; j < re; j += 64) {
+            const int32_t v = zr[perm[j]];
+            const int32_t k = zr_topic(v);
+            atomicAdd(&h[k], 1 + ((v & 1) << 16));
+            if (v & 1) atomicAdd(&B[(int64_t)src[zr_slot(v)] * Kp + k], 1);
+        }
+        __syncthreads();
+        int broken = 0;
+        for (int32_t k = lane; k < Kp; k += 64) {
+            const int32_t x = h[k];
+            const bool br = (x != 0) && ((x >> 16) == 0);
+            first[k] = br ? INT_MAX : -1;
+            broken |= br;
+        }
+        if (__syncthreads_or(broken)) {
+            for (int32_t j = rs + lane; j < re; j += 64) {
+                const int32_t k = zr_topic(zr[perm[j]]);
+                if (first[k] >= 0) atomicMin(&first[k], j);
+            }
+            __syncthreads();
+            const int32_t hs = head_slot[q];
+            for (int32_t k = lane; k < Kp; k += 64) {
+                const int32_t j = first[k];
+                if (j >= 0 && j != INT_MAX) {
+                    const int32_t tok = perm[j];
+                    zr[tok] = zr_pack(k, 1, hs);
+                    h[k] += 1 << 16;
+                    atomicAdd(&B[(int64_t)src[hs] * Kp + k], 1);
+                    ++rep;
+                }
+            }
+            __syncthreads();
+        }
+        int32_t *__restrict__ row = nt + q * Kp;
+        for (int32_t k = lane; k < Kp; k += 64) row[k] = h[k];
+    }
+    for (int o = 32; o > 0; o >>= 1) rep += __shfl_xor(rep, o);
+    if (lane == 0) rep_part[q] = rep;
+}
+
+// B16 = min(B, 65535), *wide = 1 if any B > 65535 (B already built)
+__global__ void k_base16(int64_t cells, const int32_t *__restrict__ B,
+                         uint16_t *__restrict__ B16, int32_t *__restrict__ wide)
+{
+    const int64_t j = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    bool over = false;
+    if (j < cells) {
+        const int32_t s = B[j];
+        over = s > 0xFFFF;
+        B16[j] = (uint16_t)(over ? 0xFFFF : s);
+    }
+    if (__any(over) && (threadIdx.x & 63) == 0) atomicOr(wide, 1);
 }
 
 // B[w][k] = sum_g t[g][w][k];  B16 = min(B, 65535), *wide = 1 if any B > 65535
@@ -242,6 +324,26 @@ hipError_t launch_base(const Model &m, const DeviceBuffers &b, hipStream_t st)
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(k_base, dim3((unsigned)blocks_for(cells, kBlock)), dim3(kBlock), 0, st, m.G,
                        m.V, m.Kp, b.nt, b.B, b.B16, b.wide);
+    return hipGetLastError();
+}
+
+hipError_t launch_rows_assoc(const Model &m, const DeviceBuffers &b, int32_t *zr, hipStream_t st)
+{
+    const int64_t rows = (int64_t)m.G * m.V;
+    hipError_t e = launch_fill_i32(b.B, (int64_t)m.V * m.Kp, 0, st);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(k_rows_assoc, dim3((unsigned)rows), dim3(64), 0, st, m.Kp, m.Sp, b.row_off,
+                       b.perm, b.srcrec, b.head_slot, zr, b.nt, b.B, b.rep_part);
+    return hipGetLastError();
+}
+
+hipError_t launch_base16(const Model &m, const DeviceBuffers &b, hipStream_t st)
+{
+    const int64_t cells = (int64_t)m.V * m.Kp;
+    hipError_t e = launch_fill_i32(b.wide, 1, 0, st);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(k_base16, dim3((unsigned)blocks_for(cells, kBlock)), dim3(kBlock), 0, st,
+                       cells, b.B, b.B16, b.wide);
     return hipGetLastError();
 }
 

@@ -20,6 +20,10 @@
 //   log p(w_d) = sum_n log sum_k phi[g][w_n][k] theta_d[k]
 // with theta_d from the final counts.  All in fp64.  One wavefront per test
 // document; the estimates are computed from the count rows on the fly.
+//
+// With word associations (non-identity P^g) phi0 is over source words and the
+// base of group g's Pitman-Yor process is P^g phi0_k:
+//   phi[g][w][k] = (n - a t + (b + a T_gk) sum_v p_{g,w,v} phi0[v][k]) / (b + N_gk).
 #include "spdp_internal.hpp"
 
 namespace spdp {
@@ -47,7 +51,7 @@ __global__ void __launch_bounds__(64) k_theta(int32_t D, int32_t K, double alpha
     for (int32_t k = threadIdx.x; k < K; k += 64) c[k] = 0;
     __syncthreads();
     const int64_t beg = doc_off[d], end = doc_off[d + 1];
-    for (int64_t i = beg + threadIdx.x; i < end; i += 64) atomicAdd(&c[zr[i] >> 1], 1);
+    for (int64_t i = beg + threadIdx.x; i < end; i += 64) atomicAdd(&c[zr_topic(zr[i])], 1);
     __syncthreads();
     const double inv = 1.0 / ((double)(end - beg) + (double)K * alpha);
     double *row = theta + (int64_t)d * K;
@@ -82,6 +86,31 @@ __global__ void k_phig(int32_t g, int32_t V, int32_t K, int32_t Kp, double a, do
     phi[j] = (n - a * t + (b + a * T) * p0) / (b + N);
 }
 
+// phi of group g as [V][K] with word associations: the base term sums phi0
+// over the sources of row (g, w) (padding slots have p = 0)
+__global__ void k_phig_assoc(int32_t g, int32_t V, int32_t K, int32_t Kp, int32_t Sp, double a,
+                             double b, double gamma, double Vgamma,
+                             const int32_t *__restrict__ nt, const int32_t *__restrict__ B,
+                             const int32_t *__restrict__ Ngk, const int32_t *__restrict__ Tgk,
+                             const int32_t *__restrict__ Bk, const int32_t *__restrict__ srcrec,
+                             const double *__restrict__ p64, double *__restrict__ phi)
+{
+    const int64_t j = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (j >= (int64_t)V * K) return;
+    const int64_t w = j / K, k = j % K;
+    const int64_t q = (int64_t)g * V + w;
+    const int32_t x = nt[q * Kp + k];
+    const double n = (double)(x & kCountMax), t = (double)(x >> kCountBits);
+    const double N = (double)Ngk[(int64_t)g * Kp + k], T = (double)Tgk[(int64_t)g * Kp + k];
+    const double den = Vgamma + (double)Bk[k];
+    double base = 0.0;
+    for (int32_t s = 0; s < Sp; ++s) {
+        const double pv = p64[q * Sp + s];
+        if (pv > 0.0) base += pv * ((gamma + (double)B[(int64_t)srcrec[q * 2 * Sp + s] * Kp + k]) / den);
+    }
+    phi[j] = (n - a * t + (b + a * T) * base) / (b + N);
+}
+
 struct FoldArgs {
     const int32_t *gw;        // [Nt] row index g V + w of each test token
     const int64_t *doc_off;   // [Dt + 1]
@@ -89,8 +118,10 @@ struct FoldArgs {
     int32_t *z;               // [Nt] fold-in topics
     double *ll_doc;           // [Dt] log p(w_d)
     const int32_t *nt, *B, *Ngk, *Tgk, *Bk;
+    const int32_t *srcrec;    // word associations (Sp > 0): source records
+    const double *p64;        //   and fp64 p of each row
     uint64_t seed;
-    int32_t D, V, K, Kp, n_sweeps;
+    int32_t D, V, K, Kp, n_sweeps, Sp;
     double alpha, a, b, gamma, Vgamma;
 };
 
@@ -101,7 +132,9 @@ __device__ __forceinline__ double wave_sum(double x)
     return x;
 }
 
-// This lane's KPL values of the group estimate for row q (topics kbase..).
+// This lane's KPL values of the group estimate for row q (topics kbase..);
+// with word associations the base weight gamma + B sums over the row's
+// sources, p-weighted.
 template <int KPL>
 __device__ __forceinline__ void phi_row(const FoldArgs &A, int64_t q, int32_t w, int32_t kbase,
                                         const double *inv, const double *base, double (&ph)[KPL])
@@ -113,7 +146,19 @@ __device__ __forceinline__ void phi_row(const FoldArgs &A, int64_t q, int32_t w,
         if (k < A.K) {
             const int32_t x = A.nt[q * A.Kp + k];
             const double n = (double)(x & kCountMax), t = (double)(x >> kCountBits);
-            ph[j] = (n - A.a * t) * inv[k] + (A.gamma + (double)A.B[(int64_t)w * A.Kp + k]) * base[k];
+            double bw;
+            if (A.Sp == 0) {
+                bw = A.gamma + (double)A.B[(int64_t)w * A.Kp + k];
+            } else {
+                bw = 0.0;
+                for (int32_t s = 0; s < A.Sp; ++s) {
+                    const double pv = A.p64[q * A.Sp + s];
+                    if (pv > 0.0)
+                        bw += pv * (A.gamma +
+                                    (double)A.B[(int64_t)A.srcrec[q * 2 * A.Sp + s] * A.Kp + k]);
+                }
+            }
+            ph[j] = (n - A.a * t) * inv[k] + bw * base[k];
         }
     }
 }
@@ -262,9 +307,14 @@ hipError_t launch_phig(const Model &m, const DeviceBuffers &b, int32_t g, double
                        hipStream_t st)
 {
     const int64_t n = (int64_t)m.V * m.K;
-    hipLaunchKernelGGL(k_phig, dim3((unsigned)blocks_for(n, kBlock)), dim3(kBlock), 0, st, g, m.V,
-                       m.K, m.Kp, m.a, m.b, m.gamma, (double)m.V * m.gamma, b.nt, b.B, b.Ngk,
-                       b.Tgk, b.Bk, phi);
+    if (m.Sp > 0)
+        hipLaunchKernelGGL(k_phig_assoc, dim3((unsigned)blocks_for(n, kBlock)), dim3(kBlock), 0,
+                           st, g, m.V, m.K, m.Kp, m.Sp, m.a, m.b, m.gamma, (double)m.V * m.gamma,
+                           b.nt, b.B, b.Ngk, b.Tgk, b.Bk, b.srcrec, b.p64, phi);
+    else
+        hipLaunchKernelGGL(k_phig, dim3((unsigned)blocks_for(n, kBlock)), dim3(kBlock), 0, st, g,
+                           m.V, m.K, m.Kp, m.a, m.b, m.gamma, (double)m.V * m.gamma, b.nt, b.B,
+                           b.Ngk, b.Tgk, b.Bk, phi);
     return hipGetLastError();
 }
 
@@ -285,6 +335,9 @@ hipError_t launch_foldin(const Model &m, const DeviceBuffers &b, int32_t D_test,
     A.Ngk = b.Ngk;
     A.Tgk = b.Tgk;
     A.Bk = b.Bk;
+    A.srcrec = b.srcrec;
+    A.p64 = b.p64;
+    A.Sp = m.Sp;
     A.seed = seed;
     A.D = D_test;
     A.V = m.V;

@@ -9,6 +9,10 @@
 //   PYP       sum_{g,k} log (b|a)_{T_gk} - log (b)_{N_gk}
 //   documents sum_d lgamma(K alpha) - lgamma(K alpha + L_d)
 //                   + sum_k lgamma(alpha + n_dk) - lgamma(alpha)
+// With word associations (non-identity P^g) the base counts B_wk are keyed by
+// each head's source word, and the joint gains the association factor of the
+// thesis's joint with the v variables: one p_{g,w,v} per table head,
+//   heads     sum_{i: r_i = 1} log p_{g(i), w_i, v_i}.
 // A cell with t > n or t = 0 < n (zero probability) sets err[0].
 #include "spdp_internal.hpp"
 
@@ -21,6 +25,7 @@ constexpr int kCellBlocks = 2048;
 constexpr int kBaseBlocks = 512;
 constexpr int kPypBlocks = 64;
 constexpr int kDocBlocks = 2048;  // one document per wave and iteration
+constexpr int kHeadBlocks = 1024; // word associations only
 
 __device__ double block_sum(double v)
 {
@@ -126,7 +131,7 @@ __global__ void __launch_bounds__(kLBlock) k_ll_docs(int32_t D, int32_t K, doubl
         for (int32_t k = lane; k < K; k += 64) hist[k] = 0;
         __threadfence_block();
         __builtin_amdgcn_wave_barrier();
-        for (int64_t i = beg + lane; i < end; i += 64) atomicAdd(&hist[zr[i] >> 1], 1);
+        for (int64_t i = beg + lane; i < end; i += 64) atomicAdd(&hist[zr_topic(zr[i])], 1);
         __threadfence_block();
         __builtin_amdgcn_wave_barrier();
         for (int32_t k = lane; k < K; k += 64) {
@@ -136,6 +141,23 @@ __global__ void __launch_bounds__(kLBlock) k_ll_docs(int32_t D, int32_t K, doubl
         if (lane == 0) acc += lgKa - lgamma((double)K * alpha + (double)(end - beg));
         __threadfence_block();
         __builtin_amdgcn_wave_barrier();
+    }
+    const double s = block_sum(acc);
+    if (threadIdx.x == 0) partial[blockIdx.x] = s;
+}
+
+// sum over table heads of log p of the head's source (word associations)
+__global__ void __launch_bounds__(kLBlock) k_ll_heads(int64_t N, int32_t Sp,
+                                                      const int32_t *__restrict__ gw,
+                                                      const int32_t *__restrict__ zr,
+                                                      const double *__restrict__ p64,
+                                                      double *__restrict__ partial)
+{
+    double acc = 0.0;
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < N; i += stride) {
+        const int32_t v = zr[i];
+        if (v & 1) acc += log(p64[(int64_t)gw[i] * Sp + zr_slot(v)]);
     }
     const double s = block_sum(acc);
     if (threadIdx.x == 0) partial[blockIdx.x] = s;
@@ -152,7 +174,10 @@ __global__ void __launch_bounds__(kLBlock) k_ll_final(int64_t n, const double *_
 
 }  // namespace
 
-int64_t loglik_partials_needed() { return kCellBlocks + kBaseBlocks + kPypBlocks + kDocBlocks; }
+int64_t loglik_partials_needed()
+{
+    return kCellBlocks + kBaseBlocks + kPypBlocks + kDocBlocks + kHeadBlocks;
+}
 
 hipError_t launch_loglik(const Model &m, const DeviceBuffers &b, const int32_t *zr,
                          hipStream_t st)
@@ -169,8 +194,14 @@ hipError_t launch_loglik(const Model &m, const DeviceBuffers &b, const int32_t *
     p += kPypBlocks;
     hipLaunchKernelGGL(k_ll_docs, dim3(kDocBlocks), dim3(kLBlock), 0, st, m.D, m.K, m.alpha,
                        b.doc_off, zr, p);
-    hipLaunchKernelGGL(k_ll_final, dim3(1), dim3(kLBlock), 0, st, loglik_partials_needed(),
-                       b.partial, b.scalar);
+    p += kDocBlocks;
+    int64_t np = p - b.partial;
+    if (m.Sp > 0) {
+        hipLaunchKernelGGL(k_ll_heads, dim3(kHeadBlocks), dim3(kLBlock), 0, st, m.N, m.Sp, b.gw,
+                           zr, b.p64, p);
+        np += kHeadBlocks;
+    }
+    hipLaunchKernelGGL(k_ll_final, dim3(1), dim3(kLBlock), 0, st, np, b.partial, b.scalar);
     return hipGetLastError();
 }
 

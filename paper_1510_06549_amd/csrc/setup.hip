@@ -172,13 +172,42 @@ __global__ void k_pack_zr(int64_t N, int32_t K, const int32_t *__restrict__ z,
     zr[i] = zr_pack(zi, ri);
 }
 
+// Word associations: (z, r, s) -> zr; a head's slot must hold a source of its
+// row (p > 0), a token with r = 0 stores slot 0.
+__global__ void k_pack_zrs(int64_t N, int32_t K, int32_t Sp, const int32_t *__restrict__ gw,
+                           const double *__restrict__ p64, const int32_t *__restrict__ z,
+                           const uint8_t *__restrict__ r, const uint8_t *__restrict__ s,
+                           int32_t *__restrict__ zr, int32_t *__restrict__ bad)
+{
+    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= N) return;
+    int32_t zi = z[i];
+    int32_t ri = r[i];
+    int32_t si = s ? (int32_t)s[i] : 0;
+    if (ri == 0) si = 0;
+    if (zi < 0 || zi >= K || ri > 1 || si >= Sp || !(p64[(int64_t)gw[i] * Sp + si] > 0.0)) {
+        atomicOr(bad, 4);
+        zi = 0;
+        ri = 0;
+        si = 0;
+    }
+    zr[i] = zr_pack(zi, ri, si);
+}
+
+__global__ void k_unpack_slot(int64_t N, const int32_t *__restrict__ zr, uint8_t *__restrict__ s)
+{
+    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= N) return;
+    s[i] = (uint8_t)zr_slot(zr[i]);
+}
+
 __global__ void k_unpack_zr(int64_t N, const int32_t *__restrict__ zr, int32_t *__restrict__ z,
                             uint8_t *__restrict__ r)
 {
     const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (i >= N) return;
     const int32_t v = zr[i];
-    if (z) z[i] = v >> 1;
+    if (z) z[i] = zr_topic(v);
     if (r) r[i] = (uint8_t)(v & 1);
 }
 
@@ -202,7 +231,7 @@ __global__ void __launch_bounds__(1024) k_totals_lds(int64_t N, int32_t Kp, int3
     for (int64_t i = beg + threadIdx.x; i < end; i += blockDim.x) {
         const int32_t v = zr[i];
         const int32_t g = (int32_t)fastdiv((uint32_t)gw[i], divV);
-        atomicAdd(&h[g * Kp + (v >> 1)], 1u + ((uint32_t)(v & 1) << 16));
+        atomicAdd(&h[g * Kp + zr_topic(v)], 1u + ((uint32_t)(v & 1) << 16));
     }
     __syncthreads();
     for (int j = threadIdx.x; j < bins; j += blockDim.x) {
@@ -222,8 +251,8 @@ __global__ void k_totals_global(int64_t N, int32_t Kp, FastDiv divV,
     if (i >= N) return;
     const int32_t v = zr[i];
     const int32_t g = (int32_t)fastdiv((uint32_t)gw[i], divV);
-    atomicAdd(Ngk + g * Kp + (v >> 1), 1);
-    if (v & 1) atomicAdd(Tgk + g * Kp + (v >> 1), 1);
+    atomicAdd(Ngk + g * Kp + zr_topic(v), 1);
+    if (v & 1) atomicAdd(Tgk + g * Kp + zr_topic(v), 1);
 }
 
 __global__ void k_topic_tables(int32_t G, int32_t Kp, const int32_t *__restrict__ Tgk,
@@ -332,6 +361,24 @@ hipError_t launch_pack_zr(const Model &m, const int32_t *z, const uint8_t *r, in
     if (m.N <= 0) return hipSuccess;
     hipLaunchKernelGGL(k_pack_zr, dim3((unsigned)blocks_for(m.N, kBlock)), dim3(kBlock), 0, st, m.N,
                        m.K, z, r, zr, bad);
+    return hipGetLastError();
+}
+
+hipError_t launch_pack_zrs(const Model &m, const DeviceBuffers &b, const int32_t *z,
+                           const uint8_t *r, const uint8_t *s, int32_t *zr, int32_t *bad,
+                           hipStream_t st)
+{
+    if (m.N <= 0) return hipSuccess;
+    hipLaunchKernelGGL(k_pack_zrs, dim3((unsigned)blocks_for(m.N, kBlock)), dim3(kBlock), 0, st,
+                       m.N, m.K, m.Sp, b.gw, b.p64, z, r, s, zr, bad);
+    return hipGetLastError();
+}
+
+hipError_t launch_unpack_slot(const Model &m, const int32_t *zr, uint8_t *s, hipStream_t st)
+{
+    if (m.N <= 0) return hipSuccess;
+    hipLaunchKernelGGL(k_unpack_slot, dim3((unsigned)blocks_for(m.N, kBlock)), dim3(kBlock), 0, st,
+                       m.N, zr, s);
     return hipGetLastError();
 }
 

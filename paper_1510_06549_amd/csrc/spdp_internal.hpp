@@ -61,8 +61,17 @@ __host__ __device__ __forceinline__ uint32_t fastdiv(uint32_t n, FastDiv f)
     return (uint32_t)(((uint64_t)n * f.m) >> f.s);
 }
 
-// Packed per-token state: zr = 2 z + r.
+// Packed per-token state: zr = 2 z + r, plus (model with word associations)
+// the slot s of a head's source word in bits 16..18: zr = s << 16 | 2 z + r.
+// A token with r = 0 has s = 0, and the plain model has s = 0 throughout.
+constexpr int32_t kSlotShift = 16;
 __host__ __device__ __forceinline__ int32_t zr_pack(int32_t z, int32_t r) { return 2 * z + r; }
+__host__ __device__ __forceinline__ int32_t zr_pack(int32_t z, int32_t r, int32_t s)
+{
+    return (s << kSlotShift) | (2 * z + r);
+}
+__host__ __device__ __forceinline__ int32_t zr_topic(int32_t v) { return (v & 0xFFFF) >> 1; }
+__host__ __device__ __forceinline__ int32_t zr_slot(int32_t v) { return v >> kSlotShift; }
 
 // Index of (n, t) in a lower-triangular table with row n at n (n + 1) / 2.
 __host__ __device__ __forceinline__ int64_t tri_index(int64_t n, int64_t t)
@@ -85,6 +94,9 @@ struct Model {
     double alpha, a, b, gamma;
     int32_t ncap;  // largest per-(g, w) token count: every n' < ncap in a sweep
     FastDiv divV;  // q -> g
+    // word associations (0 for the plain model, P = I): S = longest source
+    // list, Sp = S rounded up to 1, 2, 4 or 8 (the slot count of the records)
+    int32_t S = 0, Sp = 0;
 };
 
 // Inputs of the sampler's rare fp64 re-decision path, kept in device memory
@@ -94,6 +106,10 @@ struct ExactCtx {
     const double *logS;
     double a, b, Vgamma, alpha, gamma;
     int32_t K, ncap;
+    // word associations: source records and fp64 p of each row (Sp slots)
+    const int32_t *srcrec;
+    const double *p64;
+    int32_t Sp;
 };
 
 struct DeviceBuffers {
@@ -130,6 +146,13 @@ struct DeviceBuffers {
     float *tr_w = nullptr;
     float *tr_u = nullptr;
     int64_t tr_cap = 0;
+    // word associations (allocated only for that model): per row q = g V + w,
+    // the Sp source words followed by their p in fp32 (a padding slot repeats
+    // the first source with p = 0), the same p in fp64, and the slot a head
+    // promoted by the repair takes (the most probable source, first on ties)
+    int32_t *srcrec = nullptr;    // [G V][2 Sp]
+    double *p64 = nullptr;        // [G V][Sp]
+    uint8_t *head_slot = nullptr; // [G V]
 };
 
 // ---------------------------------------------------------------------------
@@ -152,6 +175,15 @@ hipError_t build_row_index(const Model &m, DeviceBuffers &b, const int32_t *gw_c
                            hipStream_t st);
 hipError_t launch_rows(const Model &m, const DeviceBuffers &b, int32_t *zr, hipStream_t st);
 hipError_t launch_base(const Model &m, const DeviceBuffers &b, hipStream_t st);
+// word associations: count rows with the repair, and the shadow-base counts
+// keyed by source (B zeroed, then one increment per head), then B16 and the
+// width flag from B
+hipError_t launch_rows_assoc(const Model &m, const DeviceBuffers &b, int32_t *zr, hipStream_t st);
+hipError_t launch_base16(const Model &m, const DeviceBuffers &b, hipStream_t st);
+hipError_t launch_pack_zrs(const Model &m, const DeviceBuffers &b, const int32_t *z,
+                           const uint8_t *r, const uint8_t *s, int32_t *zr, int32_t *bad,
+                           hipStream_t st);
+hipError_t launch_unpack_slot(const Model &m, const int32_t *zr, uint8_t *s, hipStream_t st);
 hipError_t launch_unpack_counts(const Model &m, const DeviceBuffers &b, int32_t g,
                                 int32_t *n_out, int32_t *t_out, hipStream_t st);
 hipError_t launch_stat_sums(const Model &m, const DeviceBuffers &b, const int32_t *zr_now,
@@ -163,6 +195,9 @@ hipError_t launch_factors(const Model &m, const DeviceBuffers &b, hipStream_t st
 hipError_t launch_sample(const Model &m, const DeviceBuffers &b, const int32_t *zr_old,
                          int32_t *zr_new, uint32_t sweep, uint64_t seed, float *tr_w,
                          float *tr_u, int64_t tr_begin, int64_t tr_end, hipStream_t st);
+hipError_t launch_sample_assoc(const Model &m, const DeviceBuffers &b, const int32_t *zr_old,
+                               int32_t *zr_new, uint32_t sweep, uint64_t seed, float *tr_w,
+                               float *tr_u, int64_t tr_begin, int64_t tr_end, hipStream_t st);
 hipError_t launch_loglik(const Model &m, const DeviceBuffers &b, const int32_t *zr,
                          hipStream_t st);
 int64_t loglik_partials_needed();

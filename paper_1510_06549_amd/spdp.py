@@ -22,6 +22,7 @@ SPDP_E_HIP = -3
 SPDP_E_RANGE = -4
 SPDP_E_STATE = -5
 SPDP_MAX_K = 1024
+SPDP_MAX_SOURCES = 8
 SPDP_NKERNELS = 4
 KERNEL_CLASSES = ("sample", "rebuild", "base", "totals")
 
@@ -31,6 +32,7 @@ EXPORTS = (
     "spdp_get_assignments", "spdp_set_assignments", "spdp_debug_conditionals", "spdp_stats",
     "spdp_kernel_timing", "spdp_kernel_times", "spdp_info", "spdp_last_error",
     "spdp_estimates", "spdp_heldout", "spdp_hellinger", "spdp_align_topics",
+    "spdp_create_assoc", "spdp_get_slots", "spdp_set_assignments_assoc", "spdp_max_sources",
 )
 
 
@@ -54,6 +56,15 @@ class _Corpus(C.Structure):
 
 class _Groups(C.Structure):
     _fields_ = [("n_groups", C.c_int32), ("doc_group", C.c_void_p)]
+
+
+class _Assoc(C.Structure):
+    _fields_ = [
+        ("max_sources", C.c_int32),
+        ("row_off", C.c_void_p),
+        ("src", C.c_void_p),
+        ("p", C.c_void_p),
+    ]
 
 
 def load_library() -> C.CDLL:
@@ -100,6 +111,14 @@ def load_library() -> C.CDLL:
     L.spdp_hellinger.restype = cint
     L.spdp_align_topics.argtypes = [vp, i32, i32, vp, vp]
     L.spdp_align_topics.restype = cint
+    L.spdp_create_assoc.argtypes = [vp, vp, vp, i32, dbl, dbl, dbl, dbl, C.POINTER(vp)]
+    L.spdp_create_assoc.restype = cint
+    L.spdp_get_slots.argtypes = [vp, vp, cint]
+    L.spdp_get_slots.restype = cint
+    L.spdp_set_assignments_assoc.argtypes = [vp, vp, vp, vp, cint]
+    L.spdp_set_assignments_assoc.restype = cint
+    L.spdp_max_sources.argtypes = [vp, C.POINTER(i32)]
+    L.spdp_max_sources.restype = cint
     return L
 
 
@@ -157,6 +176,49 @@ def spdp_create(words, doc_offsets, doc_group, n_groups, vocab, K, alpha, a, b, 
     _check(lib().spdp_create(C.byref(corpus), C.byref(groups), int(K), float(alpha), float(a),
                              float(b), float(gamma), C.byref(h)))
     return h
+
+
+def spdp_create_assoc(words, doc_offsets, doc_group, n_groups, vocab, K, alpha, a, b, gamma,
+                      row_off, src, p, max_sources=None, init_seed=0, hip_stream=None):
+    """State of the model with word associations: row q = g V + w of P^g lists
+    its sources src[row_off[q]:row_off[q+1]] with probabilities p (see
+    include/spdp.h)."""
+    words = np.ascontiguousarray(words, dtype=np.int32)
+    doc_offsets = np.ascontiguousarray(doc_offsets, dtype=np.int64)
+    doc_group = np.ascontiguousarray(doc_group, dtype=np.int32)
+    row_off = np.ascontiguousarray(row_off, dtype=np.int64)
+    src = np.ascontiguousarray(src, dtype=np.int32)
+    p = np.ascontiguousarray(p, dtype=np.float64)
+    if max_sources is None:
+        max_sources = int(np.diff(row_off).max()) if row_off.size > 1 else 0
+    corpus = _Corpus(int(words.shape[0]), int(doc_group.shape[0]), int(vocab), words.ctypes.data,
+                     doc_offsets.ctypes.data, int(init_seed) & (2**64 - 1),
+                     None if hip_stream is None else int(hip_stream))
+    groups = _Groups(int(n_groups), doc_group.ctypes.data)
+    assoc = _Assoc(int(max_sources), row_off.ctypes.data, src.ctypes.data, p.ctypes.data)
+    h = C.c_void_p()
+    _check(lib().spdp_create_assoc(C.byref(corpus), C.byref(groups), C.byref(assoc), int(K),
+                                   float(alpha), float(a), float(b), float(gamma), C.byref(h)))
+    return h
+
+
+def spdp_get_slots(h, slot_out):
+    _check(lib().spdp_get_slots(h, _buf(slot_out)[0], _where(slot_out)))
+
+
+def spdp_set_assignments_assoc(h, z, r, slot):
+    if isinstance(z, np.ndarray):
+        z = np.ascontiguousarray(z, dtype=np.int32)
+        r = np.ascontiguousarray(r, dtype=np.uint8)
+        slot = np.ascontiguousarray(slot, dtype=np.uint8)
+    where = _where(z, r, slot)
+    _check(lib().spdp_set_assignments_assoc(h, _buf(z)[0], _buf(r)[0], _buf(slot)[0], where))
+
+
+def spdp_max_sources(h) -> int:
+    S = C.c_int32()
+    _check(lib().spdp_max_sources(h, C.byref(S)))
+    return int(S.value)
 
 
 def spdp_sweep(h, sweep: int, seed: int):
@@ -281,12 +343,20 @@ class Sampler:
     """Owns one library state; thin host-side helpers around the entry points."""
 
     def __init__(self, words, doc_offsets, doc_group, n_groups, vocab, K, alpha, a, b, gamma,
-                 init_seed=0, hip_stream=None):
-        self.h = spdp_create(words, doc_offsets, doc_group, n_groups, vocab, K, alpha, a, b, gamma,
-                             init_seed, hip_stream)
+                 init_seed=0, hip_stream=None, assoc=None):
+        """assoc: None (P = I) or (row_off, src, p) of the word associations."""
+        if assoc is None:
+            self.h = spdp_create(words, doc_offsets, doc_group, n_groups, vocab, K, alpha, a, b,
+                                 gamma, init_seed, hip_stream)
+        else:
+            row_off, src, p = assoc
+            self.h = spdp_create_assoc(words, doc_offsets, doc_group, n_groups, vocab, K, alpha,
+                                       a, b, gamma, row_off, src, p, init_seed=init_seed,
+                                       hip_stream=hip_stream)
         self.info = spdp_info(self.h)
         self.N, self.G, self.V, self.K = (self.info["N"], self.info["G"], self.info["V"],
                                           self.info["K"])
+        self.S = spdp_max_sources(self.h)
 
     def close(self):
         if self.h:
@@ -308,8 +378,17 @@ class Sampler:
         spdp_get_assignments(self.h, z, r)
         return z, r
 
-    def set_assignments(self, z, r):
-        spdp_set_assignments(self.h, z, r)
+    def set_assignments(self, z, r, slot=None):
+        if slot is None:
+            spdp_set_assignments(self.h, z, r)
+        else:
+            spdp_set_assignments_assoc(self.h, z, r, slot)
+
+    def slots(self):
+        """Source slot of each token's table (word associations; 0 for r = 0)."""
+        s = np.empty(self.N, dtype=np.uint8)
+        spdp_get_slots(self.h, s)
+        return s
 
     def counts(self, g_begin=0, g_end=None):
         """n, t as [g][w][k] int32 arrays."""
@@ -332,7 +411,8 @@ class Sampler:
 
     def conditionals(self, sweep, seed, tok_begin, tok_end):
         T = tok_end - tok_begin
-        w = np.zeros((T, 2 * self.K), dtype=np.float32)
+        per_topic = 2 if self.S == 0 else self.S + 1
+        w = np.zeros((T, per_topic * self.K), dtype=np.float32)
         u = np.zeros(T, dtype=np.float32)
         zr = np.zeros(T, dtype=np.int32)
         spdp_debug_conditionals(self.h, sweep, seed, tok_begin, tok_end, w, u, zr)

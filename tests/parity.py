@@ -11,6 +11,8 @@ The comparison protocol, per sweep, from one identical state:
         normalised CDF boundary between the two outcomes;
   (iv)  after update and repair the library's state and counts equal the
         oracle's rebuild and repair of the library's sampled (z, r).
+With word associations the state is (z, r, source slot), the outcomes per
+token are K (S + 1) and every token draws (the sole head redraws its source).
 """
 from __future__ import annotations
 
@@ -26,13 +28,31 @@ U_TOL = 1e-5
 MATCH_FRAC = 0.9999
 
 
-def make_pair(cp, wl, init_seed=0, K=None):
+def make_pair(cp, wl, init_seed=0, K=None, assoc=None):
+    """Library state and oracle model of one corpus; assoc = (row_off, src, p)
+    for the model with word associations."""
     K = wl.K if K is None else K
     s = sp.Sampler(cp.words, cp.doc_off, cp.doc_group, cp.n_groups, cp.vocab, K, wl.alpha, wl.a,
-                   wl.b, wl.gamma, init_seed=init_seed)
-    m = oracle.Model(cp.words, cp.doc_off, cp.doc_group, cp.n_groups, K, cp.vocab, wl.alpha, wl.a,
-                     wl.b, wl.gamma)
+                   wl.b, wl.gamma, init_seed=init_seed, assoc=assoc)
+    args = (cp.words, cp.doc_off, cp.doc_group, cp.n_groups, K, cp.vocab, wl.alpha, wl.a, wl.b,
+            wl.gamma)
+    m = oracle.Model(*args) if assoc is None else oracle.AssocModel(*args, *assoc)
     return s, m
+
+
+def _is_assoc(m) -> bool:
+    return isinstance(m, oracle.AssocModel)
+
+
+def state_of(s: sp.Sampler, m):
+    """The library's current state as the oracle takes it: (z, r) or (z, r, slot)."""
+    z, r = s.assignments()
+    return (z, r, s.slots()) if _is_assoc(m) else (z, r)
+
+
+def unpack(zr):
+    """Packed sampled outcomes -> (z, r, slot)."""
+    return (zr & 0xFFFF) >> 1, (zr & 1).astype(np.uint8), (zr >> 16).astype(np.uint8)
 
 
 def assert_counts_equal(s: sp.Sampler, c: oracle.Counts):
@@ -66,14 +86,25 @@ def _chunks(m, chunk_tokens):
         d = d_end
 
 
+def _outcome(m, z, r, sl):
+    """Index of the outcome (z, r[, slot]) in the token's weight vector."""
+    if _is_assoc(m):
+        return (m.S + 1) * int(z) + (int(sl) if r else m.S)
+    return 2 * int(z) + (1 - int(r))
+
+
 def one_step(s: sp.Sampler, m: oracle.Model, sweep: int, seed: int, chunk_tokens=150_000):
     """Run one sweep on both sides from the library's current state and compare."""
-    z, r = s.assignments()
-    c = m.rebuild(z, r)
+    assoc = _is_assoc(m)
+    st = state_of(s, m)
+    c = m.rebuild(*st)
     assert_counts_equal(s, c)  # (i)
-    zo, ro = z.copy(), r.copy()
+    zo, ro = st[0].copy(), st[1].copy()
+    so = st[2].copy() if assoc else np.zeros(m.N, np.uint8)
+    ost = (zo, ro, so) if assoc else (zo, ro)
     zg_pre = np.empty(m.N, dtype=np.int32)
     rg_pre = np.empty(m.N, dtype=np.uint8)
+    sg_pre = np.zeros(m.N, dtype=np.uint8)
     n_mism = primary = checked = 0
     primary_gap = max_rel = 0.0
     for d0, d1, tb, te in _chunks(m, chunk_tokens):
@@ -82,13 +113,15 @@ def one_step(s: sp.Sampler, m: oracle.Model, sweep: int, seed: int, chunk_tokens
         # library: weights, uniforms and samples of the (uncommitted) sampling step
         w_g, u_g, zr_g = s.conditionals(sweep, seed, tb, te)
         # oracle: the same documents with a full trace
-        _, w_o, u_o, skip_o = m.sample_docs(c, zo, ro, sweep, seed, d0, d1, trace=(tb, te))
+        _, w_o, u_o, skip_o = m.sample_docs(c, *ost, sweep, seed, d0, d1, trace=(tb, te))
         skip_o = skip_o.astype(bool)
-        zg, rg = zr_g >> 1, (zr_g & 1).astype(np.uint8)
-        zg_pre[tb:te], rg_pre[tb:te] = zg, rg
+        zg, rg, sg = unpack(zr_g)
+        zg_pre[tb:te], rg_pre[tb:te], sg_pre[tb:te] = zg, rg, sg
+        if not assoc:
+            assert not sg.any(), "slot bits in a state without associations"
 
         # (iii) samples
-        same = (zg == zo[tb:te]) & (rg == ro[tb:te])
+        same = (zg == zo[tb:te]) & (rg == ro[tb:te]) & (sg == so[tb:te])
         mism = np.flatnonzero(~same)
         n_mism += len(mism)
         doc = np.repeat(np.arange(d0, d1), np.diff(m.doc_off[d0:d1 + 1])) - d0
@@ -98,8 +131,8 @@ def one_step(s: sp.Sampler, m: oracle.Model, sweep: int, seed: int, chunk_tokens
         for i in np.unique(first_bad[first_bad < np.iinfo(np.int64).max]):
             primary += 1
             assert not skip_o[i], f"token {tb + i}: oracle kept it (sole head), library moved it"
-            jg = 2 * int(zg[i]) + (1 - int(rg[i]))
-            jo = 2 * int(zo[tb + i]) + (1 - int(ro[tb + i]))
+            jg = _outcome(m, zg[i], rg[i], sg[i])
+            jo = _outcome(m, zo[tb + i], ro[tb + i], so[tb + i])
             cdf = np.cumsum(w_o[i])
             cdf /= cdf[-1]
             gap = abs(u_o[i] - cdf[min(jg, jo)])
@@ -125,11 +158,13 @@ def one_step(s: sp.Sampler, m: oracle.Model, sweep: int, seed: int, chunk_tokens
 
     # commit the library's sweep
     s.sweep(sweep, seed)
-    zs, rs = s.assignments()
+    st2 = state_of(s, m)
     # (iv) update + repair: oracle rebuild and repair of the library's samples
-    c2 = m.rebuild(zg_pre, rg_pre)
-    m.repair(zg_pre, rg_pre, c2)
-    assert np.array_equal(zs, zg_pre) and np.array_equal(rs, rg_pre), "post-repair state differs"
+    pre = (zg_pre, rg_pre, sg_pre) if assoc else (zg_pre, rg_pre)
+    c2 = m.rebuild(*pre)
+    m.repair(*pre, c2)
+    for a, b in zip(st2, pre):
+        assert np.array_equal(a, b), "post-repair state differs"
     assert_counts_equal(s, c2)
     changed, repaired = s.stats()
     return StepReport(m.N, n_mism, primary, primary_gap, max_rel, checked), changed, repaired

@@ -70,3 +70,38 @@ def test_null_state_is_an_argument_error():
     assert L.spdp_sweep(None, 0, 0) == sp.SPDP_E_ARG
     assert L.spdp_stats(None, None, None) == sp.SPDP_E_ARG
     L.spdp_destroy(None)  # NULL is ignored
+
+
+def test_invalid_associations_rejected_without_gpu():
+    from paper_1510_06549_amd import spdp as sp
+
+    words = np.array([0, 1, 2], np.int32)
+    off = np.array([0, 3], np.int64)
+    grp = np.array([0], np.int32)
+    V = 3
+
+    def create(row_off, src, p, S=None):
+        return sp.spdp_create_assoc(words, off, grp, 1, V, 2, 0.1, 0.5, 1.0, 0.1, row_off, src,
+                                    p, max_sources=S)
+
+    good = (np.array([0, 2, 3, 5]), np.array([0, 1, 1, 2, 0]), np.array([.5, .5, 1., .5, .5]))
+    cases = [
+        ((np.array([0, 2, 2, 4]), np.array([0, 1, 2, 0]), np.array([.5, .5, .5, .5])), None,
+         "no source"),
+        ((good[0], np.array([0, 1, 1, 2, 3]), good[2]), None, "out of [0, vocab)"),
+        ((good[0], np.array([0, 0, 1, 2, 0]), good[2]), None, "repeats source"),
+        ((good[0], good[1], np.array([.5, 0., 1., .5, .5])), None, "finite and > 0"),
+        ((good[0], good[1], np.array([.5, np.inf, 1., .5, .5])), None, "finite and > 0"),
+        (good, 3, "longest row"),
+        (good, 9, "max_sources must be in"),
+        ((np.array([0, 9, 10, 11]), np.arange(11) % 3, np.ones(11)), 9, "max_sources must be in"),
+    ]
+    for (ro, src, p), S, msg in cases:
+        with pytest.raises(sp.SpdpError) as e:
+            create(ro, src, p, S)
+        assert e.value.code == sp.SPDP_E_ARG, msg
+        assert msg in sp.spdp_last_error(), (msg, sp.spdp_last_error())
+    L = sp.lib()
+    assert L.spdp_create_assoc(None, None, None, 2, 0.1, 0.5, 1.0, 0.1, None) == sp.SPDP_E_ARG
+    assert L.spdp_get_slots(None, None, 0) == sp.SPDP_E_ARG
+    assert L.spdp_max_sources(None, None) == sp.SPDP_E_ARG
