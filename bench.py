@@ -9,6 +9,11 @@ duration) and the fp64 oracle timed on the host cores over a bounded sample
 of documents.
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME|IDX]
+                       [--assoc S [--assoc-eps E]]
+
+--assoc S runs the model with word associations instead (sparse
+transformation matrices with S sources per word, from synth.associations)
+and reports the same line for it.
 """
 from __future__ import annotations
 
@@ -38,6 +43,14 @@ def sample_bytes_per_token(K: int, wide: bool) -> int:
     or int32 once some count exceeds 65535), and the token stream (row index
     and state in, state out)."""
     return 4 * K + (4 if wide else 2) * K + 12
+
+
+def assoc_bytes_per_token(K: int, wide: bool, mean_sources: float, Sp: int) -> float:
+    """Bytes the association sampler must move per token: the packed count
+    row, one shadow-base row per source of the token's row (mean_sources on
+    average), the token stream (row index and state in, state out) and the
+    row's source record (Sp source words and Sp fp32 p)."""
+    return 4 * K + (4 if wide else 2) * K * mean_sources + 12 + 8 * Sp
 
 
 def dense_bytes_per_token(K: int) -> int:
@@ -70,31 +83,32 @@ def recorded_traffic(workload: str):
     return float(kv["bytes_per_launch"])
 
 
-def cpu_baseline(cp, wl, z, r, target_s: float):
+def cpu_baseline(cp, wl, state, target_s: float, assoc=None):
+    """The oracle's sampling step timed on the host cores over a bounded
+    sample of documents; state = (z, r) or (z, r, slot) with assoc."""
     import numpy as np
 
     import oracle
 
     t0 = time.time()
-    m = oracle.Model(cp.words, cp.doc_off, cp.doc_group, cp.n_groups, wl.K, wl.vocab, wl.alpha,
-                     wl.a, wl.b, wl.gamma)
-    c = m.rebuild(z, r)
+    args = (cp.words, cp.doc_off, cp.doc_group, cp.n_groups, wl.K, wl.vocab, wl.alpha, wl.a,
+            wl.b, wl.gamma)
+    m = oracle.Model(*args) if assoc is None else oracle.AssocModel(*args, *assoc)
+    c = m.rebuild(*state)
     log(f"[bench] oracle model + dense counts ready in {time.time() - t0:.1f}s")
     threads = oracle.num_threads()
     # calibrate on a few documents, then size the sample to about target_s
-    zs, rs = z.copy(), r.copy()
     d_cal = min(2048, m.D)
     t0 = time.perf_counter()
-    m.sample_docs(c, zs, rs, 0, 1, 0, d_cal)
+    m.sample_docs(c, *[x.copy() for x in state], 0, 1, 0, d_cal)
     dt = max(time.perf_counter() - t0, 1e-6)
     tok_cal = int(m.doc_off[d_cal])
     per_tok = dt / max(tok_cal, 1)
     want_tok = int(target_s / per_tok)
     d_s = int(np.searchsorted(m.doc_off, want_tok))
     d_s = max(d_cal, min(d_s, m.D))
-    zs, rs = z.copy(), r.copy()
     t0 = time.perf_counter()
-    m.sample_docs(c, zs, rs, 0, 1, 0, d_s)
+    m.sample_docs(c, *[x.copy() for x in state], 0, 1, 0, d_s)
     dt = time.perf_counter() - t0
     toks = int(m.doc_off[d_s])
     return {
@@ -119,6 +133,10 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="also run a plain device copy of this size (counter calibration)")
+    ap.add_argument("--assoc", type=int, default=0,
+                    help="sources per word of the word-association model (0: P = I)")
+    ap.add_argument("--assoc-eps", type=float, default=0.3,
+                    help="probability mass of the other sources of a word")
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -141,10 +159,18 @@ def main():
     log(f"[bench] workload {wl.name}: {cp.n_tokens} tokens, {cp.n_docs} docs, generated in "
         f"{time.time() - t0:.1f}s")
 
+    assoc = None
+    if args.assoc > 0:
+        t0 = time.time()
+        assoc = synth.associations(cp.n_groups, cp.vocab, args.assoc, args.assoc_eps, args.seed)
+        log(f"[bench] associations S={args.assoc} eps={args.assoc_eps}: {assoc[0][-1]} entries "
+            f"in {time.time() - t0:.1f}s")
+
     stream = torch.cuda.current_stream()
     t0 = time.time()
     s = sp.Sampler(cp.words, cp.doc_off, cp.doc_group, cp.n_groups, wl.vocab, wl.K, wl.alpha,
-                   wl.a, wl.b, wl.gamma, init_seed=args.seed, hip_stream=stream.cuda_stream)
+                   wl.a, wl.b, wl.gamma, init_seed=args.seed, hip_stream=stream.cuda_stream,
+                   assoc=assoc)
     torch.cuda.synchronize()
     info = s.info
     log(f"[bench] state created in {time.time() - t0:.1f}s: {info}")
@@ -186,12 +212,22 @@ def main():
     value = N * args.steps / elapsed
     ms_sample, n_sample = kt["sample"]
     avg_sample_s = ms_sample / 1000.0 / max(n_sample, 1)
-    alg = N * sample_bytes_per_token(wl.K, wide)
+    if assoc is None:
+        bpt = sample_bytes_per_token(wl.K, wide)
+        traffic = recorded_traffic(wl.name)
+    else:
+        # mean length of the source list of each token's row
+        lens = np.diff(assoc[0])
+        q = np.repeat(cp.doc_group, np.diff(cp.doc_off)).astype(np.int64) * cp.vocab + cp.words
+        mean_sources = float(lens[q].mean())
+        Sp = 1 if s.S <= 1 else (2 if s.S <= 2 else (4 if s.S <= 4 else 8))
+        bpt = assoc_bytes_per_token(wl.K, wide, mean_sources, Sp)
+        traffic = None
+    alg = N * bpt
     achieved = alg / avg_sample_s / 1e9
-    traffic = recorded_traffic(wl.name)
     roofline = {
         "bound": "hbm",
-        "kernel": "k_sample",
+        "kernel": "k_sample" if assoc is None else "k_sample_assoc",
         "achieved": round(achieved, 1),
         "peak": HBM_PEAK_GBS,
         "unit": "GB/s",
@@ -199,18 +235,22 @@ def main():
         "traffic": None if traffic is None else round(traffic / 1e9, 3),
         "traffic_unit": "GB per launch",
         "alg_bytes_per_launch_GB": round(alg / 1e9, 3),
-        "bytes_per_token": sample_bytes_per_token(wl.K, wide),
+        "bytes_per_token": round(bpt, 2),
         "shadow_base_bits": 32 if wide else 16,
-        "dense_int32_bytes_per_token": dense_bytes_per_token(wl.K),
-        "dense_int32_equiv_GBps": round(N * dense_bytes_per_token(wl.K) / avg_sample_s / 1e9, 1),
         "avg_launch_ms": round(avg_sample_s * 1000.0, 3),
     }
+    if assoc is None:
+        roofline["dense_int32_bytes_per_token"] = dense_bytes_per_token(wl.K)
+        roofline["dense_int32_equiv_GBps"] = round(
+            N * dense_bytes_per_token(wl.K) / avg_sample_s / 1e9, 1)
+    else:
+        roofline["mean_sources_per_token"] = round(mean_sources, 4)
 
     cpu = None
     if not args.no_cpu_baseline:
-        z, r = s.assignments()
+        state = s.assignments() + ((s.slots(),) if assoc is not None else ())
         s.close()
-        cpu = cpu_baseline(cp, wl, z, r, args.cpu_seconds)
+        cpu = cpu_baseline(cp, wl, state, args.cpu_seconds, assoc)
         log(f"[bench] cpu baseline {cpu}")
     else:
         s.close()
@@ -241,6 +281,10 @@ def main():
         "roofline": roofline,
         "cpu_baseline": cpu,
     }
+    if assoc is not None:
+        out["config"]["workload"] = f"{wl.name}-assoc{args.assoc}"
+        out["config"]["sources_per_word"] = args.assoc
+        out["config"]["assoc_eps"] = args.assoc_eps
     print(json.dumps(out), flush=True)
 
 
