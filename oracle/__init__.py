@@ -104,6 +104,12 @@ def lib():
         L.or_max_group_word_count.restype = i32
         L.or_chain_histogram.argtypes = [vp, vp, vp, vp, u32, i64, u64, C.c_int, vp, i64]
         L.or_chain_histogram.restype = C.c_int
+        L.or_interleaved_order.argtypes = [vp, vp]
+        L.or_interleaved_order.restype = None
+        L.or_sweep_ordered.argtypes = [vp, vp, vp, vp, u32, u64, vp, vp]
+        L.or_sweep_ordered.restype = C.c_int
+        L.or_chain_histogram_ordered.argtypes = [vp, vp, vp, vp, u32, i64, u64, vp, vp, i64]
+        L.or_chain_histogram_ordered.restype = C.c_int
         L.or_num_threads.argtypes = []
         L.or_num_threads.restype = C.c_int
         L.or_estimates.argtypes = [vp, vp, vp, vp, vp, vp]
@@ -255,20 +261,43 @@ class Model:
                                   _p(tw), _p(tu), _p(ts), tb, te)
         return int(ch), tw, tu, ts
 
-    def sweep(self, counts, z, r, sweep, seed, mode: str = "snapshot"):
+    def interleaved_order(self):
+        """Visiting order of the word order rearrangement: round robin over the
+        position inside the document, documents in index order."""
+        order = np.zeros(self.N, dtype=np.int32)
+        lib().or_interleaved_order(self.ref, _p(order))
+        return order
+
+    def sweep(self, counts, z, r, sweep, seed, mode: str = "snapshot", order=None):
+        """mode "snapshot", "sequential" (token index order) or "ordered"
+        (sequential in the visiting order `order`)."""
         stats = np.zeros(2, dtype=np.int64)
-        rc = lib().or_sweep(self.ref, counts.ref, _p(z), _p(r), sweep, seed,
-                            0 if mode == "snapshot" else 1, _p(stats))
+        if mode == "ordered":
+            order = np.ascontiguousarray(order, dtype=np.int32)
+            assert order.shape == (self.N,)
+            rc = lib().or_sweep_ordered(self.ref, counts.ref, _p(z), _p(r), sweep, seed,
+                                        _p(order), _p(stats))
+        else:
+            rc = lib().or_sweep(self.ref, counts.ref, _p(z), _p(r), sweep, seed,
+                                0 if mode == "snapshot" else 1, _p(stats))
         if rc != 0:
             raise ValueError(mode)
         return int(stats[0]), int(stats[1])
 
-    def chain_histogram(self, counts, z, r, first_sweep, n_sweeps, seed, mode="sequential"):
+    def chain_histogram(self, counts, z, r, first_sweep, n_sweeps, seed, mode="sequential",
+                        order=None):
         """Visit counts of encoded states over `n_sweeps` sweeps (tiny corpora only)."""
         n_bins = (2 * self.K) ** self.N
         hist = np.zeros(n_bins, dtype=np.int64)
-        rc = lib().or_chain_histogram(self.ref, counts.ref, _p(z), _p(r), first_sweep, n_sweeps,
-                                      seed, 0 if mode == "snapshot" else 1, _p(hist), n_bins)
+        if mode == "ordered":
+            order = np.ascontiguousarray(order, dtype=np.int32)
+            rc = lib().or_chain_histogram_ordered(self.ref, counts.ref, _p(z), _p(r),
+                                                  first_sweep, n_sweeps, seed, _p(order),
+                                                  _p(hist), n_bins)
+        else:
+            rc = lib().or_chain_histogram(self.ref, counts.ref, _p(z), _p(r), first_sweep,
+                                          n_sweeps, seed, 0 if mode == "snapshot" else 1,
+                                          _p(hist), n_bins)
         if rc != 0:
             raise RuntimeError(f"or_chain_histogram failed ({rc})")
         return hist

@@ -493,6 +493,91 @@ int or_num_threads(void)
 }
 
 /* ------------------------------------------------------------------------ */
+/* Word order rearrangement (thesis, subsection "Parallelism With Improved    */
+/* Accuracy: Word Order Rearrangement"): tokens are visited round robin over  */
+/* their position inside the document -- every document's first token, then  */
+/* every document's second token, and so on -- so that tokens taken up at     */
+/* about the same time come from different documents.  Documents are taken   */
+/* in index order at every position.  order [N] receives token indices.      */
+/* ------------------------------------------------------------------------ */
+void or_interleaved_order(const or_model *m, int32_t *order)
+{
+    int64_t longest = 0, out = 0;
+    for (int32_t d = 0; d < m->n_docs; ++d)
+        if (m->doc_off[d + 1] - m->doc_off[d] > longest) longest = m->doc_off[d + 1] - m->doc_off[d];
+    for (int64_t pos = 0; pos < longest; ++pos)
+        for (int32_t d = 0; d < m->n_docs; ++d)
+            if (m->doc_off[d] + pos < m->doc_off[d + 1]) order[out++] = (int32_t)(m->doc_off[d] + pos);
+}
+
+/* ------------------------------------------------------------------------ */
+/* Sequential collapsed Gibbs (Algorithm SPDP-Full-Gibbs with stored r, live */
+/* counts) visiting the tokens in a given order (a permutation of 0..N-1):   */
+/* the exact single-site sampler whose racy concurrent execution the        */
+/* thesis's asynchronous GPU kernel is.  Each document's topic counts stay   */
+/* live across the sweep.  The uniform of token i is that of or_sweep.       */
+/* ------------------------------------------------------------------------ */
+int or_sweep_ordered(const or_model *m, or_counts *c, int32_t *z, uint8_t *r, uint32_t sweep,
+                     uint64_t seed, const int32_t *order, int64_t *out_stats)
+{
+    const int64_t K = m->K, N = m->n_tokens;
+    int32_t *cdk = (int32_t *)calloc((size_t)(m->n_docs > 0 ? m->n_docs : 1) * (size_t)K,
+                                     sizeof(int32_t));
+    int32_t *tok_doc = (int32_t *)malloc(sizeof(int32_t) * (size_t)(N > 0 ? N : 1));
+    double *w = (double *)malloc(sizeof(double) * (size_t)(2 * K));
+    for (int32_t d = 0; d < m->n_docs; ++d)
+        for (int64_t i = m->doc_off[d]; i < m->doc_off[d + 1]; ++i) {
+            tok_doc[i] = d;
+            cdk[(int64_t)d * K + z[i]] += 1;
+        }
+    int64_t changed = 0;
+    int bad = 0;
+    for (int64_t p = 0; p < N; ++p) {
+        const int64_t i = order[p];
+        if (i < 0 || i >= N) { bad = 1; break; }
+        const int32_t d = tok_doc[i], g = m->doc_group[d];
+        int32_t *crow = cdk + (int64_t)d * K;
+        const int32_t k0 = z[i], r0 = r[i], wd = m->words[i];
+        if (or_token_weights(m, c, crow, g, wd, k0, r0, w)) continue;
+        const int j = draw_outcome(w, 2 * K, or_uniform(seed, i, sweep));
+        const int32_t k1 = j / 2, r1 = 1 - (j % 2);
+        apply_token(m, c, g, wd, k0, r0, -1);
+        apply_token(m, c, g, wd, k1, r1, +1);
+        crow[k0] -= 1;
+        crow[k1] += 1;
+        if (k1 != k0 || r1 != r0) ++changed;
+        z[i] = k1;
+        r[i] = (uint8_t)r1;
+    }
+    free(cdk);
+    free(tok_doc);
+    free(w);
+    if (bad) return -1;
+    if (out_stats) { out_stats[0] = changed; out_stats[1] = 0; }
+    return 0;
+}
+
+/* Chain histogram of the ordered sequential sweep (encoding as below). */
+int or_chain_histogram_ordered(const or_model *m, or_counts *c, int32_t *z, uint8_t *r,
+                               uint32_t first_sweep, int64_t n_sweeps, uint64_t seed,
+                               const int32_t *order, int64_t *hist, int64_t n_bins)
+{
+    const int64_t base = 2 * (int64_t)m->K;
+    for (int64_t s = 0; s < n_sweeps; ++s) {
+        if (or_sweep_ordered(m, c, z, r, first_sweep + (uint32_t)s, seed, order, NULL) != 0)
+            return -1;
+        int64_t code = 0, mul = 1;
+        for (int64_t i = 0; i < m->n_tokens; ++i) {
+            code += (2 * (int64_t)z[i] + 1 - r[i]) * mul;
+            mul *= base;
+        }
+        if (code < 0 || code >= n_bins) return -2;
+        hist[code] += 1;
+    }
+    return 0;
+}
+
+/* ------------------------------------------------------------------------ */
 /* Test helper: run `n_sweeps` sweeps (mode as in or_sweep, sweep index =    */
 /* first_sweep + s) and histogram the visited states.  A state is encoded in  */
 /* base 2K with digit (2 z_i + 1 - r_i) for token i (least significant first), */
