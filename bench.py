@@ -13,7 +13,9 @@ Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME|IDX]
 
 --assoc S runs the model with word associations instead (sparse
 transformation matrices with S sources per word, from synth.associations)
-and reports the same line for it.
+and reports the same line for it.  --async runs the thesis's asynchronous
+sweep (an ablation: live atomics, racy reads; --async-waves wavefronts, 0 for
+the library's default) instead of the snapshot sweep.
 """
 from __future__ import annotations
 
@@ -51,6 +53,14 @@ def assoc_bytes_per_token(K: int, wide: bool, mean_sources: float, Sp: int) -> f
     average), the token stream (row index and state in, state out) and the
     row's source record (Sp source words and Sp fp32 p)."""
     return 4 * K + (4 if wide else 2) * K * mean_sources + 12 + 8 * Sp
+
+
+def async_bytes_per_token(K: int) -> int:
+    """Bytes the asynchronous sweep's pass must move per token: the live
+    packed count row, shadow-base row (int32) and document row of the token
+    (the group's total rows stay in cache), the visiting order, row index,
+    document and state of the token, and its state written back."""
+    return 4 * K + 4 * K + 4 * K + 20
 
 
 def dense_bytes_per_token(K: int) -> int:
@@ -137,6 +147,12 @@ def main():
                     help="sources per word of the word-association model (0: P = I)")
     ap.add_argument("--assoc-eps", type=float, default=0.3,
                     help="probability mass of the other sources of a word")
+    ap.add_argument("--async", dest="async_sweep", action="store_true",
+                    help="time the asynchronous (racy) sweep instead of the snapshot sweep")
+    ap.add_argument("--async-waves", type=int, default=0,
+                    help="wavefronts of the asynchronous sweep (0: library default)")
+    ap.add_argument("--async-live-totals", action="store_true",
+                    help="asynchronous sweep with the sums N, T, B_k updated live")
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -185,9 +201,19 @@ def main():
         log(f"[bench] copy probe: {nbytes} bytes read + {nbytes} bytes written")
         del src, dst
 
+    if args.async_sweep and assoc is not None:
+        print("bench.py: the asynchronous sweep is built for P = I only", file=sys.stderr)
+        sys.exit(2)
+
+    def one_sweep(k):
+        if args.async_sweep:
+            s.sweep_async(k, seed, args.async_waves, args.async_live_totals)
+        else:
+            s.sweep(k, seed)
+
     seed = 1000 + args.seed
     for w in range(args.warmup):
-        s.sweep(w, seed)
+        one_sweep(w)
     torch.cuda.synchronize()
     log(f"[bench] {args.warmup} warm-up sweep(s) done")
     # width of the shadow-base rows the timed sweeps read (set by each rebuild)
@@ -197,7 +223,7 @@ def main():
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for k in range(args.steps):
-        s.sweep(args.warmup + k, seed)
+        one_sweep(args.warmup + k)
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
     kt = sp.spdp_kernel_times(s.h)
@@ -212,7 +238,10 @@ def main():
     value = N * args.steps / elapsed
     ms_sample, n_sample = kt["sample"]
     avg_sample_s = ms_sample / 1000.0 / max(n_sample, 1)
-    if assoc is None:
+    if args.async_sweep:
+        bpt = async_bytes_per_token(wl.K)
+        traffic = None
+    elif assoc is None:
         bpt = sample_bytes_per_token(wl.K, wide)
         traffic = recorded_traffic(wl.name)
     else:
@@ -227,7 +256,8 @@ def main():
     achieved = alg / avg_sample_s / 1e9
     roofline = {
         "bound": "hbm",
-        "kernel": "k_sample" if assoc is None else "k_sample_assoc",
+        "kernel": ("k_sample_async" if args.async_sweep
+                   else ("k_sample" if assoc is None else "k_sample_assoc")),
         "achieved": round(achieved, 1),
         "peak": HBM_PEAK_GBS,
         "unit": "GB/s",
@@ -239,7 +269,9 @@ def main():
         "shadow_base_bits": 32 if wide else 16,
         "avg_launch_ms": round(avg_sample_s * 1000.0, 3),
     }
-    if assoc is None:
+    if args.async_sweep:
+        pass
+    elif assoc is None:
         roofline["dense_int32_bytes_per_token"] = dense_bytes_per_token(wl.K)
         roofline["dense_int32_equiv_GBps"] = round(
             N * dense_bytes_per_token(wl.K) / avg_sample_s / 1e9, 1)
@@ -281,6 +313,10 @@ def main():
         "roofline": roofline,
         "cpu_baseline": cpu,
     }
+    if args.async_sweep:
+        out["config"]["workload"] = f"{wl.name}-async"
+        out["config"]["async_waves"] = args.async_waves
+        out["config"]["async_live_totals"] = bool(args.async_live_totals)
     if assoc is not None:
         out["config"]["workload"] = f"{wl.name}-assoc{args.assoc}"
         out["config"]["sources_per_word"] = args.assoc

@@ -148,6 +148,30 @@ int spdp_create_assoc(const spdp_corpus *corpus, const spdp_groups *groups,
 int spdp_sweep(spdp_state *s, uint32_t sweep, uint64_t seed);
 
 /*
+ * Ablation (not the library's sweep): one sweep of the thesis's asynchronous
+ * scheme (section "Parallel Word Sampling": each token reads the global
+ * counts as they are, removes itself and adds itself back with atomics, no
+ * locks; subsection "Word Order Rearrangement": tokens taken up round robin
+ * over the position inside the document, documents in index order at each
+ * position).  `waves` wavefronts take the tokens of the visiting order in
+ * turn (wave w: positions w, w + waves, ...); 0 takes the library's default
+ * (16 per compute unit).  The word, shadow-base and document counts are live;
+ * the sums N_gk, T_gk, B_k are live too if live_totals != 0, else held at
+ * their sweep-start values during the pass (the thesis lets them drift and
+ * corrects them regularly; live sums serialise on their few counters).  With
+ * waves = 1 and live_totals = 1 the sweep is exactly sequential collapsed
+ * Gibbs in the visiting order (same outcomes, uniforms and sole-head rule as
+ * spdp_sweep, counts live after every token); with more waves it is racy and
+ * its result depends on scheduling.  The counts are then regenerated exactly
+ * from the new state, with the repair of spdp_sweep.  The first call builds
+ * the visiting order and allocates 8 N + 4 D Kp bytes of device memory.
+ * Asynchronous on the state's stream.  Errors: E_ARG (NULL state, waves < 0,
+ * a state with word associations), E_NOMEM, E_HIP.
+ */
+int spdp_sweep_async(spdp_state *s, uint32_t sweep, uint64_t seed, int32_t waves,
+                     int32_t live_totals);
+
+/*
  * Export customer counts n and table counts t of groups [g_begin, g_end) as
  * [g_end - g_begin][V][K] int32 each (either pointer may be NULL to skip it).
  * Synchronises.  Errors: E_ARG, E_HIP.

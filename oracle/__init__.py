@@ -106,7 +106,7 @@ def lib():
         L.or_chain_histogram.restype = C.c_int
         L.or_interleaved_order.argtypes = [vp, vp]
         L.or_interleaved_order.restype = None
-        L.or_sweep_ordered.argtypes = [vp, vp, vp, vp, u32, u64, vp, vp]
+        L.or_sweep_ordered.argtypes = [vp, vp, vp, vp, u32, u64, vp, C.c_int, vp]
         L.or_sweep_ordered.restype = C.c_int
         L.or_chain_histogram_ordered.argtypes = [vp, vp, vp, vp, u32, i64, u64, vp, vp, i64]
         L.or_chain_histogram_ordered.restype = C.c_int
@@ -268,15 +268,17 @@ class Model:
         lib().or_interleaved_order(self.ref, _p(order))
         return order
 
-    def sweep(self, counts, z, r, sweep, seed, mode: str = "snapshot", order=None):
+    def sweep(self, counts, z, r, sweep, seed, mode: str = "snapshot", order=None,
+              stale_totals=False):
         """mode "snapshot", "sequential" (token index order) or "ordered"
-        (sequential in the visiting order `order`)."""
+        (sequential in the visiting order `order`; stale_totals holds the sums
+        N_gk, T_gk, B_k at their sweep-start values in the conditionals)."""
         stats = np.zeros(2, dtype=np.int64)
         if mode == "ordered":
             order = np.ascontiguousarray(order, dtype=np.int32)
             assert order.shape == (self.N,)
             rc = lib().or_sweep_ordered(self.ref, counts.ref, _p(z), _p(r), sweep, seed,
-                                        _p(order), _p(stats))
+                                        _p(order), 1 if stale_totals else 0, _p(stats))
         else:
             rc = lib().or_sweep(self.ref, counts.ref, _p(z), _p(r), sweep, seed,
                                 0 if mode == "snapshot" else 1, _p(stats))

@@ -516,11 +516,29 @@ void or_interleaved_order(const or_model *m, int32_t *order)
 /* the exact single-site sampler whose racy concurrent execution the        */
 /* thesis's asynchronous GPU kernel is.  Each document's topic counts stay   */
 /* live across the sweep.  The uniform of token i is that of or_sweep.       */
+/* stale_totals = 1: the auxiliary sums N_gk, T_gk and B_k enter the         */
+/* conditionals at their sweep-start values (the token's own contribution    */
+/* removed), while n, t, B_kw and the document counts stay live -- the       */
+/* thesis lets the sums drift during an iteration and corrects them          */
+/* regularly; this variant is not exact Gibbs (parity unpinned: only its     */
+/* invariants and its single-wave GPU counterpart check it).               */
 /* ------------------------------------------------------------------------ */
 int or_sweep_ordered(const or_model *m, or_counts *c, int32_t *z, uint8_t *r, uint32_t sweep,
-                     uint64_t seed, const int32_t *order, int64_t *out_stats)
+                     uint64_t seed, const int32_t *order, int stale_totals, int64_t *out_stats)
 {
-    const int64_t K = m->K, N = m->n_tokens;
+    const int64_t K = m->K, N = m->n_tokens, G = m->n_groups;
+    /* the counts the conditionals read: live, or live with frozen sums */
+    or_counts view = *c;
+    int32_t *frozen = NULL;
+    if (stale_totals) {
+        frozen = (int32_t *)malloc(sizeof(int32_t) * (size_t)(2 * G * K + K));
+        memcpy(frozen, c->Ngk, sizeof(int32_t) * (size_t)(G * K));
+        memcpy(frozen + G * K, c->Tgk, sizeof(int32_t) * (size_t)(G * K));
+        memcpy(frozen + 2 * G * K, c->Bk, sizeof(int32_t) * (size_t)K);
+        view.Ngk = frozen;
+        view.Tgk = frozen + G * K;
+        view.Bk = frozen + 2 * G * K;
+    }
     int32_t *cdk = (int32_t *)calloc((size_t)(m->n_docs > 0 ? m->n_docs : 1) * (size_t)K,
                                      sizeof(int32_t));
     int32_t *tok_doc = (int32_t *)malloc(sizeof(int32_t) * (size_t)(N > 0 ? N : 1));
@@ -538,7 +556,7 @@ int or_sweep_ordered(const or_model *m, or_counts *c, int32_t *z, uint8_t *r, ui
         const int32_t d = tok_doc[i], g = m->doc_group[d];
         int32_t *crow = cdk + (int64_t)d * K;
         const int32_t k0 = z[i], r0 = r[i], wd = m->words[i];
-        if (or_token_weights(m, c, crow, g, wd, k0, r0, w)) continue;
+        if (or_token_weights(m, &view, crow, g, wd, k0, r0, w)) continue;
         const int j = draw_outcome(w, 2 * K, or_uniform(seed, i, sweep));
         const int32_t k1 = j / 2, r1 = 1 - (j % 2);
         apply_token(m, c, g, wd, k0, r0, -1);
@@ -552,6 +570,7 @@ int or_sweep_ordered(const or_model *m, or_counts *c, int32_t *z, uint8_t *r, ui
     free(cdk);
     free(tok_doc);
     free(w);
+    free(frozen);
     if (bad) return -1;
     if (out_stats) { out_stats[0] = changed; out_stats[1] = 0; }
     return 0;
@@ -564,7 +583,7 @@ int or_chain_histogram_ordered(const or_model *m, or_counts *c, int32_t *z, uint
 {
     const int64_t base = 2 * (int64_t)m->K;
     for (int64_t s = 0; s < n_sweeps; ++s) {
-        if (or_sweep_ordered(m, c, z, r, first_sweep + (uint32_t)s, seed, order, NULL) != 0)
+        if (or_sweep_ordered(m, c, z, r, first_sweep + (uint32_t)s, seed, order, 0, NULL) != 0)
             return -1;
         int64_t code = 0, mul = 1;
         for (int64_t i = 0; i < m->n_tokens; ++i) {

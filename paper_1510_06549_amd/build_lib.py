@@ -8,7 +8,8 @@ import sys
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
-SOURCES = ["api.hip", "setup.hip", "counts.hip", "sample.hip", "sample_assoc.hip", "loglik.hip",
+SOURCES = ["api.hip", "setup.hip", "counts.hip", "sample.hip", "sample_assoc.hip", "sample_async.hip",
+           "loglik.hip",
            "estimate.hip",
            "hellinger.hip"]
 LIB = os.path.join(HERE, "libspdp.so")

@@ -489,6 +489,48 @@ int spdp_sweep(spdp_state *s, uint32_t sweep, uint64_t seed)
     return SPDP_OK;
 }
 
+int spdp_sweep_async(spdp_state *s, uint32_t sweep, uint64_t seed, int32_t waves,
+                     int32_t live_totals)
+{
+    if (!s) return fail(SPDP_E_ARG, "state is NULL");
+    const Model &m = s->m;
+    if (m.Sp > 0) return fail(SPDP_E_ARG, "the asynchronous sweep is built for P = I only");
+    if (waves < 0) return fail(SPDP_E_ARG, "waves must be >= 0");
+    HIP_TRY(hipSetDevice(s->device));
+    DeviceBuffers &b = s->b;
+    int rc;
+    if (!b.order) {
+        if ((rc = dev_alloc(s, &b.order, m.N, "visiting order")) != SPDP_OK) return rc;
+        if ((rc = dev_alloc(s, &b.tok_doc, m.N, "token documents")) != SPDP_OK) return rc;
+        if ((rc = dev_alloc(s, &b.cdk, (int64_t)m.D * m.Kp, "document counts")) != SPDP_OK)
+            return rc;
+        HIP_TRY(build_visit_order(m, b, s->st));
+    }
+    if (waves == 0) {
+        int cus = 0;
+        HIP_TRY(hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, s->device));
+        waves = 16 * (cus > 0 ? cus : 1);
+    }
+    // the pass updates the state in place, in the other buffer, so that the
+    // statistics compare it with the state before the sweep
+    int32_t *zr_old = b.zr[s->cur], *zr_new = b.zr[1 - s->cur];
+    if (m.N > 0)
+        HIP_TRY(hipMemcpyAsync(zr_new, zr_old, (size_t)m.N * sizeof(int32_t),
+                               hipMemcpyDeviceToDevice, s->st));
+    if ((rc = timed(s, 3, [&] { return launch_doc_counts(m, b, zr_new, b.cdk, s->st); })) != SPDP_OK)
+        return rc;
+    if ((rc = timed(s, 0, [&] {
+             return launch_sample_async(m, b, b.order, b.tok_doc, b.cdk, zr_new, sweep, seed,
+                                        waves, live_totals != 0, s->st);
+         })) != SPDP_OK)
+        return rc;
+    if ((rc = timed(s, 1, [&] { return launch_rows(m, b, zr_new, s->st); })) != SPDP_OK) return rc;
+    if ((rc = timed(s, 2, [&] { return launch_base(m, b, s->st); })) != SPDP_OK) return rc;
+    if ((rc = timed(s, 3, [&] { return launch_totals(m, b, zr_new, s->st); })) != SPDP_OK) return rc;
+    s->cur = 1 - s->cur;
+    return SPDP_OK;
+}
+
 int spdp_counts(const spdp_state *s, int32_t g_begin, int32_t g_end, int32_t *n_gwk,
                 int32_t *t_gwk, int where)
 {

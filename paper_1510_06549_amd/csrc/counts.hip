@@ -309,6 +309,50 @@ hipError_t build_row_index(const Model &m, DeviceBuffers &b, const int32_t *gw_c
     return e != hipSuccess ? e : e2;
 }
 
+// Visiting order of the asynchronous sweep: tokens stably sorted by their
+// position inside the document, so at each position the documents come in
+// index order (the word order rearrangement).  Fills b.order and b.tok_doc.
+hipError_t build_visit_order(const Model &m, DeviceBuffers &b, hipStream_t st)
+{
+    if (m.N <= 0) return hipSuccess;
+    int32_t *pos = nullptr, *keys_out = nullptr, *vals_in = nullptr;
+    void *temp = nullptr;
+    hipError_t e = hipMalloc(&pos, (size_t)m.N * 4);
+    if (e == hipSuccess) e = hipMalloc(&keys_out, (size_t)m.N * 4);
+    if (e == hipSuccess) e = hipMalloc(&vals_in, (size_t)m.N * 4);
+    if (e == hipSuccess) e = launch_tok_doc(m, b.doc_off, b.tok_doc, pos, st);
+    if (e == hipSuccess) {
+        hipLaunchKernelGGL(k_iota, dim3((unsigned)blocks_for(m.N, kBlock)), dim3(kBlock), 0, st,
+                           vals_in, m.N);
+        e = hipGetLastError();
+    }
+    // the longest document bounds the keys
+    int32_t *mx = nullptr;
+    int32_t longest = 0;
+    if (e == hipSuccess) e = hipMalloc(&mx, 4);
+    if (e == hipSuccess) e = launch_fill_i32(mx, 1, 0, st);
+    if (e == hipSuccess) e = launch_max_i32(pos, m.N, mx, st);
+    if (e == hipSuccess) e = hipMemcpyAsync(&longest, mx, 4, hipMemcpyDeviceToHost, st);
+    if (e == hipSuccess) e = hipStreamSynchronize(st);
+    int end_bit = 1;
+    while ((1ll << end_bit) <= longest) ++end_bit;
+    size_t bytes = 0;
+    if (e == hipSuccess)
+        e = hipcub::DeviceRadixSort::SortPairs(nullptr, bytes, pos, keys_out, vals_in, b.order,
+                                               (int)m.N, 0, end_bit, st);
+    if (e == hipSuccess) e = hipMalloc(&temp, bytes > 0 ? bytes : 1);
+    if (e == hipSuccess)
+        e = hipcub::DeviceRadixSort::SortPairs(temp, bytes, pos, keys_out, vals_in, b.order,
+                                               (int)m.N, 0, end_bit, st);
+    hipError_t e2 = hipStreamSynchronize(st);
+    hipFree(pos);
+    hipFree(keys_out);
+    hipFree(vals_in);
+    hipFree(mx);
+    hipFree(temp);
+    return e != hipSuccess ? e : e2;
+}
+
 hipError_t launch_rows(const Model &m, const DeviceBuffers &b, int32_t *zr, hipStream_t st)
 {
     const int64_t rows = (int64_t)m.G * m.V;

@@ -153,6 +153,11 @@ struct DeviceBuffers {
     int32_t *srcrec = nullptr;    // [G V][2 Sp]
     double *p64 = nullptr;        // [G V][Sp]
     uint8_t *head_slot = nullptr; // [G V]
+    // asynchronous sweep (allocated on its first use): visiting order of the
+    // word order rearrangement, document of each token, live document counts
+    int32_t *order = nullptr;     // [N]
+    int32_t *tok_doc = nullptr;   // [N]
+    int32_t *cdk = nullptr;       // [D][Kp]
 };
 
 // ---------------------------------------------------------------------------
@@ -200,6 +205,17 @@ hipError_t launch_sample_assoc(const Model &m, const DeviceBuffers &b, const int
                                float *tr_u, int64_t tr_begin, int64_t tr_end, hipStream_t st);
 hipError_t launch_loglik(const Model &m, const DeviceBuffers &b, const int32_t *zr,
                          hipStream_t st);
+// asynchronous sweep: token -> document and position, the visiting order
+// (stable sort of tokens by position inside the document), document counts,
+// the sampling pass with live atomics (waves wavefronts)
+hipError_t launch_tok_doc(const Model &m, const int64_t *doc_off, int32_t *tok_doc, int32_t *pos,
+                          hipStream_t st);
+hipError_t build_visit_order(const Model &m, DeviceBuffers &b, hipStream_t st);
+hipError_t launch_doc_counts(const Model &m, const DeviceBuffers &b, const int32_t *zr,
+                             int32_t *cdk, hipStream_t st);
+hipError_t launch_sample_async(const Model &m, const DeviceBuffers &b, const int32_t *order,
+                               const int32_t *tok_doc, int32_t *cdk, int32_t *zr, uint32_t sweep,
+                               uint64_t seed, int32_t waves, bool live_totals, hipStream_t st);
 int64_t loglik_partials_needed();
 
 hipError_t launch_theta(const Model &m, const DeviceBuffers &b, const int32_t *zr, double *theta,

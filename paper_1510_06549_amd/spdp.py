@@ -33,6 +33,7 @@ EXPORTS = (
     "spdp_kernel_timing", "spdp_kernel_times", "spdp_info", "spdp_last_error",
     "spdp_estimates", "spdp_heldout", "spdp_hellinger", "spdp_align_topics",
     "spdp_create_assoc", "spdp_get_slots", "spdp_set_assignments_assoc", "spdp_max_sources",
+    "spdp_sweep_async",
 )
 
 
@@ -119,6 +120,8 @@ def load_library() -> C.CDLL:
     L.spdp_set_assignments_assoc.restype = cint
     L.spdp_max_sources.argtypes = [vp, C.POINTER(i32)]
     L.spdp_max_sources.restype = cint
+    L.spdp_sweep_async.argtypes = [vp, u32, u64, i32, i32]
+    L.spdp_sweep_async.restype = cint
     return L
 
 
@@ -223,6 +226,11 @@ def spdp_max_sources(h) -> int:
 
 def spdp_sweep(h, sweep: int, seed: int):
     _check(lib().spdp_sweep(h, int(sweep) & 0xFFFFFFFF, int(seed) & (2**64 - 1)))
+
+
+def spdp_sweep_async(h, sweep: int, seed: int, waves: int = 0, live_totals: bool = False):
+    _check(lib().spdp_sweep_async(h, int(sweep) & 0xFFFFFFFF, int(seed) & (2**64 - 1),
+                                  int(waves), 1 if live_totals else 0))
 
 
 def spdp_counts(h, g_begin, g_end, n_out=None, t_out=None):
@@ -371,6 +379,10 @@ class Sampler:
 
     def sweep(self, sweep, seed):
         spdp_sweep(self.h, sweep, seed)
+
+    def sweep_async(self, sweep, seed, waves=0, live_totals=False):
+        """The thesis's asynchronous sweep (an ablation; see include/spdp.h)."""
+        spdp_sweep_async(self.h, sweep, seed, waves, live_totals)
 
     def assignments(self):
         z = np.empty(self.N, dtype=np.int32)
