@@ -78,17 +78,17 @@ int dev_alloc(spdp_state *s, T **p, int64_t count, const char *what)
 void free_state(spdp_state *s)
 {
     if (!s) return;
-    hipSetDevice(s->device);
-    if (s->st) hipStreamSynchronize(s->st);
-    else hipDeviceSynchronize();
-    for (void *p : s->allocs) hipFree(p);
-    if (s->b.zr_dbg) hipFree(s->b.zr_dbg);
-    if (s->b.tr_w) hipFree(s->b.tr_w);
-    if (s->b.tr_u) hipFree(s->b.tr_u);
+    (void)hipSetDevice(s->device);
+    if (s->st) (void)hipStreamSynchronize(s->st);
+    else (void)hipDeviceSynchronize();
+    for (void *p : s->allocs) (void)hipFree(p);
+    if (s->b.zr_dbg) (void)hipFree(s->b.zr_dbg);
+    if (s->b.tr_w) (void)hipFree(s->b.tr_w);
+    if (s->b.tr_u) (void)hipFree(s->b.tr_u);
     for (auto &v : s->events)
         for (auto &ev : v) {
-            hipEventDestroy(ev.a);
-            hipEventDestroy(ev.b);
+            (void)hipEventDestroy(ev.a);
+            (void)hipEventDestroy(ev.b);
         }
     delete s;
 }
@@ -340,14 +340,14 @@ int create_state(const spdp_corpus *corpus, const spdp_groups *groups, const spd
         words_d = (int32_t *)tmp;
         if (hipMalloc(&tmp, (size_t)(rows + 1) * sizeof(int32_t)) != hipSuccess) {
             (void)hipGetLastError();
-            hipFree(words_d);
+            (void)hipFree(words_d);
             TRY(fail(SPDP_E_NOMEM, "staging buffer for word counts"));
         }
         gw_count = (int32_t *)tmp;
     }
     auto cleanup_staging = [&]() {
-        hipFree(words_d);
-        hipFree(gw_count);
+        (void)hipFree(words_d);
+        (void)hipFree(gw_count);
     };
     hipError_t e = hipSuccess;
     if (N > 0)
@@ -547,7 +547,7 @@ int spdp_counts(const spdp_state *s, int32_t g_begin, int32_t g_end, int32_t *n_
         HIP_TRY(hipMalloc(&stage_n, (size_t)cells * 4));
         hipError_t e = hipMalloc(&stage_t, (size_t)cells * 4);
         if (e != hipSuccess) {
-            hipFree(stage_n);
+            (void)hipFree(stage_n);
             HIP_TRY(e);
         }
     }
@@ -566,8 +566,8 @@ int spdp_counts(const spdp_state *s, int32_t g_begin, int32_t g_end, int32_t *n_
             if (e == hipSuccess) e = hipStreamSynchronize(s->st);
         }
     }
-    if (stage_n) hipFree(stage_n);
-    if (stage_t) hipFree(stage_t);
+    if (stage_n) (void)hipFree(stage_n);
+    if (stage_t) (void)hipFree(stage_t);
     HIP_TRY(e);
     return sync(s);
 }
@@ -636,7 +636,7 @@ int spdp_estimates(spdp_state *s, int32_t g_begin, int32_t g_end, double *theta,
     for (int32_t g = g_begin; phi && g < g_end; ++g)
         out(phi + (int64_t)(g - g_begin) * vk, vk,
             [&](double *d) { return launch_phig(m, s->b, g, d, s->st); });
-    if (stage) hipFree(stage);
+    if (stage) (void)hipFree(stage);
     HIP_TRY(e);
     return sync(s);
 }
@@ -695,11 +695,11 @@ int spdp_heldout(spdp_state *s, const spdp_corpus *test, const spdp_groups *test
         e = hipMemcpyAsync(z_out, z_d, (size_t)N * 4,
                            where ? hipMemcpyDeviceToDevice : hipMemcpyDeviceToHost, s->st);
     if (e == hipSuccess) e = hipStreamSynchronize(s->st);
-    hipFree(gw_d);
-    hipFree(z_d);
-    hipFree(off_d);
-    hipFree(grp_d);
-    hipFree(ll_d);
+    (void)hipFree(gw_d);
+    (void)hipFree(z_d);
+    (void)hipFree(off_d);
+    (void)hipFree(grp_d);
+    (void)hipFree(ll_d);
     HIP_TRY(e);
     double total = 0.0;  // documents in order
     for (int32_t d = 0; d < D; ++d) total += ll[(size_t)d];
@@ -755,7 +755,7 @@ int spdp_hellinger(spdp_state *s, const double *p, int32_t kp, const double *q, 
     if (e == hipSuccess && !where && nh > 0)
         e = hipMemcpyAsync(h, Hd, (size_t)nh * sizeof(double), hipMemcpyDeviceToHost, s->st);
     if (e == hipSuccess) e = hipStreamSynchronize(s->st);
-    for (void *x : tmp) hipFree(x);
+    for (void *x : tmp) (void)hipFree(x);
     HIP_TRY(e);
     return SPDP_OK;
 }
@@ -789,8 +789,8 @@ int spdp_get_assignments(const spdp_state *s, int32_t *z, uint8_t *r, int where)
     if (e == hipSuccess && z) e = hipMemcpyAsync(z, zd, (size_t)m.N * 4, hipMemcpyDeviceToHost, s->st);
     if (e == hipSuccess && r) e = hipMemcpyAsync(r, rd, (size_t)m.N, hipMemcpyDeviceToHost, s->st);
     if (e == hipSuccess) e = hipStreamSynchronize(s->st);
-    hipFree(zd);
-    if (rd) hipFree(rd);
+    (void)hipFree(zd);
+    if (rd) (void)hipFree(rd);
     HIP_TRY(e);
     return SPDP_OK;
 }
@@ -811,9 +811,9 @@ int set_state(spdp_state *s, const int32_t *z, const uint8_t *r, const uint8_t *
         int32_t *zt = nullptr;
         uint8_t *rt = nullptr, *st8 = nullptr;
         auto release = [&]() {
-            if (zt) hipFree(zt);
-            if (rt) hipFree(rt);
-            if (st8) hipFree(st8);
+            if (zt) (void)hipFree(zt);
+            if (rt) (void)hipFree(rt);
+            if (st8) (void)hipFree(st8);
         };
         if (where == 0) {
             hipError_t e = hipMalloc(&zt, (size_t)m.N * sizeof(int32_t));
@@ -884,7 +884,7 @@ int spdp_get_slots(const spdp_state *s, uint8_t *slot, int where)
     hipError_t e = launch_unpack_slot(m, s->b.zr[s->cur], sd, s->st);
     if (e == hipSuccess) e = hipMemcpyAsync(slot, sd, (size_t)m.N, hipMemcpyDeviceToHost, s->st);
     if (e == hipSuccess) e = hipStreamSynchronize(s->st);
-    hipFree(sd);
+    (void)hipFree(sd);
     HIP_TRY(e);
     return SPDP_OK;
 }
@@ -921,8 +921,8 @@ int spdp_debug_conditionals(spdp_state *s, uint32_t sweep, uint64_t seed, int64_
     }
     const bool trace = (w_out != nullptr || u_out != nullptr);
     if (trace && T > b.tr_cap) {
-        if (b.tr_w) hipFree(b.tr_w);
-        if (b.tr_u) hipFree(b.tr_u);
+        if (b.tr_w) (void)hipFree(b.tr_w);
+        if (b.tr_u) (void)hipFree(b.tr_u);
         b.tr_w = nullptr;
         b.tr_u = nullptr;
         b.tr_cap = 0;
@@ -980,8 +980,8 @@ int spdp_kernel_timing(spdp_state *s, int enable)
     if (rc != SPDP_OK) return rc;
     for (auto &v : s->events) {
         for (auto &ev : v) {
-            hipEventDestroy(ev.a);
-            hipEventDestroy(ev.b);
+            (void)hipEventDestroy(ev.a);
+            (void)hipEventDestroy(ev.b);
         }
         v.clear();
     }

@@ -282,12 +282,12 @@ hipError_t build_row_index(const Model &m, DeviceBuffers &b, const int32_t *gw_c
     const size_t temp_bytes = scan_bytes > sort_bytes ? scan_bytes : sort_bytes;
     if ((e = hipMalloc(&temp, temp_bytes > 0 ? temp_bytes : 1)) != hipSuccess) return e;
     if ((e = hipMalloc(&keys_out, (size_t)(m.N > 0 ? m.N : 1) * 4)) != hipSuccess) {
-        hipFree(temp);
+        (void)hipFree(temp);
         return e;
     }
     if ((e = hipMalloc(&vals_in, (size_t)(m.N > 0 ? m.N : 1) * 4)) != hipSuccess) {
-        hipFree(temp);
-        hipFree(keys_out);
+        (void)hipFree(temp);
+        (void)hipFree(keys_out);
         return e;
     }
     size_t tb = temp_bytes;
@@ -303,9 +303,9 @@ hipError_t build_row_index(const Model &m, DeviceBuffers &b, const int32_t *gw_c
         }
     }
     hipError_t e2 = hipStreamSynchronize(st);
-    hipFree(temp);
-    hipFree(keys_out);
-    hipFree(vals_in);
+    (void)hipFree(temp);
+    (void)hipFree(keys_out);
+    (void)hipFree(vals_in);
     return e != hipSuccess ? e : e2;
 }
 
@@ -345,11 +345,11 @@ hipError_t build_visit_order(const Model &m, DeviceBuffers &b, hipStream_t st)
         e = hipcub::DeviceRadixSort::SortPairs(temp, bytes, pos, keys_out, vals_in, b.order,
                                                (int)m.N, 0, end_bit, st);
     hipError_t e2 = hipStreamSynchronize(st);
-    hipFree(pos);
-    hipFree(keys_out);
-    hipFree(vals_in);
-    hipFree(mx);
-    hipFree(temp);
+    (void)hipFree(pos);
+    (void)hipFree(keys_out);
+    (void)hipFree(vals_in);
+    (void)hipFree(mx);
+    (void)hipFree(temp);
     return e != hipSuccess ? e : e2;
 }
 

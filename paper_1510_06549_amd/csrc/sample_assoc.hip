@@ -100,6 +100,28 @@ struct AWave {
     float p_c[SP];
 };
 
+// lds_row with each 16-byte chunk pinned as one value, so that the compiler
+// keeps whole-chunk reads (split 4-byte reads at a 16-byte lane stride would
+// conflict on the LDS banks)
+template <int KPL>
+__device__ __forceinline__ void lds_row_whole(float (&v)[KPL], const float *base, int32_t lane)
+{
+    if constexpr (KPL % 4 == 0) {
+#pragma unroll
+        for (int c = 0; c < KPL / 4; ++c) {
+            typedef float f4 __attribute__((ext_vector_type(4)));
+            f4 x = reinterpret_cast<const f4 *>(base)[c * 64 + lane];
+            asm volatile("" : "+v"(x));
+            v[4 * c + 0] = x[0];
+            v[4 * c + 1] = x[1];
+            v[4 * c + 2] = x[2];
+            v[4 * c + 3] = x[3];
+        }
+    } else {
+        lds_row<KPL>(v, base, lane);
+    }
+}
+
 // Relative distance from a CDF boundary below which the fp32 decision is
 // re-taken in fp64.  A weight carries at most 8 + SP roundings (the p-weighted
 // sum of SP positive terms included) and a prefix at most 2 KPL + 8 further
@@ -248,11 +270,13 @@ __device__ __forceinline__ void sample_token_assoc(const AssocArgs &A, AWave<KPL
     const float doc0 = A.alpha + (float)(W.c_lds[k0] - 1);
     const float m1k0 = doc0 * f1k, m0k0 = doc0 * f0k;
     float a0[KPL], a1[KPL];
-    lds_row<KPL>(a0, W.a0_lds, lane);
-    lds_row<KPL>(a1, W.a1_lds, lane);
+    lds_row_whole<KPL>(a0, W.a0_lds, lane);
+    lds_row_whole<KPL>(a1, W.a1_lds, lane);
 
     // per topic: the base weight of each source slot, their p-weighted sum,
     // the factor of the head outcomes and the running prefix at the topic end
+    // (branch-free: the sole-head case is a uniform select, so the compiler
+    // keeps the LDS rows as whole 16-byte reads)
     float hq[KPL], e[KPL];
     float acc = 0.0f;
 #pragma unroll
@@ -264,15 +288,20 @@ __device__ __forceinline__ void sample_token_assoc(const AssocArgs &A, AWave<KPL
             const float bv = A.gamma + (float)(cur.b(s, j) - ((own && r0 && s == s0) ? 1 : 0));
             beta = __fmaf_rn(p[s], bv, beta);
         }
-        float w0;
-        if (sole) {
-            hq[j] = own ? 1.0f : 0.0f;
-            w0 = 0.0f;
-        } else {
-            hq[j] = __fmul_rn(own ? m1k0 : a1[j], qv[j].y);
-            w0 = __fmul_rn(own ? m0k0 : a0[j], qv[j].x);
-        }
-        if (A.tr_w != nullptr && i >= A.tr_begin && i < A.tr_end && kbase + j < A.K) {
+        const float h_draw = __fmul_rn(own ? m1k0 : a1[j], qv[j].y);
+        const float w0_draw = __fmul_rn(own ? m0k0 : a0[j], qv[j].x);
+        hq[j] = sole ? (own ? 1.0f : 0.0f) : h_draw;
+        const float w0 = sole ? 0.0f : w0_draw;
+        acc = __fadd_rn(acc, __fmul_rn(hq[j], beta));
+        acc = __fadd_rn(acc, w0);
+        e[j] = acc;
+    }
+    if (A.tr_w != nullptr && i >= A.tr_begin && i < A.tr_end) {
+        // debug trace: every outcome's weight, formed again from the same values
+#pragma unroll
+        for (int j = 0; j < KPL; ++j) {
+            if (kbase + j >= A.K) continue;
+            const bool own = (kbase + j == k0);
             float *o = A.tr_w + (i - A.tr_begin) * (int64_t)A.K * (A.S + 1) +
                        (int64_t)(kbase + j) * (A.S + 1);
 #pragma unroll
@@ -283,11 +312,8 @@ __device__ __forceinline__ void sample_token_assoc(const AssocArgs &A, AWave<KPL
                     o[s] = hq[j] * (p[s] * bv);
                 }
             }
-            o[A.S] = w0;
+            o[A.S] = sole ? 0.0f : __fmul_rn(own ? m0k0 : a0[j], qv[j].x);
         }
-        acc = __fadd_rn(acc, __fmul_rn(hq[j], beta));
-        acc = __fadd_rn(acc, w0);
-        e[j] = acc;
     }
     const float incl = wave_inclusive_sum(acc);
     const float excl = wave_shift_right(incl);

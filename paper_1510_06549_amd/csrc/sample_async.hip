@@ -228,10 +228,11 @@ __global__ void __launch_bounds__(64) k_sample_async(AsyncArgs A)
             double acc64 = 0.0;
 #pragma unroll
             for (int j = 0; j < KPL; ++j) {
-                if (kbase + j >= A.K) break;
-                const Exact2 e = exact_async(A, n[j], bw[j], c[j], Nk[j], Tk[j], Bt[j]);
-                acc64 += e.w1;
-                acc64 += e.w0;
+                if (kbase + j < A.K) {
+                    const Exact2 e = exact_async(A, n[j], bw[j], c[j], Nk[j], Tk[j], Bt[j]);
+                    acc64 += e.w1;
+                    acc64 += e.w0;
+                }
             }
             double incl64 = acc64;
 #pragma unroll
@@ -245,7 +246,7 @@ __global__ void __launch_bounds__(64) k_sample_async(AsyncArgs A)
             int32_t cand = -1, lastp = -1;
 #pragma unroll
             for (int j = 0; j < KPL; ++j) {
-                if (kbase + j >= A.K) break;
+                if (kbase + j >= A.K) continue;
                 const Exact2 e = exact_async(A, n[j], bw[j], c[j], Nk[j], Tk[j], Bt[j]);
                 run += e.w1;
                 if (e.w1 > 0.0) {

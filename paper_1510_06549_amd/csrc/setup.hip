@@ -398,9 +398,10 @@ hipError_t launch_totals(const Model &m, const DeviceBuffers &b, const int32_t *
     if ((e = fill(b.Ngk, bins, 0, st)) != hipSuccess) return e;
     if ((e = fill(b.Tgk, bins, 0, st)) != hipSuccess) return e;
     if (m.N > 0) {
+        // (if the queries fail, lds_max stays 0 and the global-atomic histogram runs)
         int dev = 0, lds_max = 0;
-        hipGetDevice(&dev);
-        hipDeviceGetAttribute(&lds_max, hipDeviceAttributeMaxSharedMemoryPerBlock, dev);
+        (void)hipGetDevice(&dev);
+        (void)hipDeviceGetAttribute(&lds_max, hipDeviceAttributeMaxSharedMemoryPerBlock, dev);
         const int64_t lds = bins * (int64_t)sizeof(uint32_t);
         if (lds <= lds_max && lds <= 96 * 1024) {
             const unsigned nb = (unsigned)blocks_for(m.N, kTotalsChunk);
