@@ -103,7 +103,7 @@ typedef struct {
  *   a      Pitman-Yor discount, 0 <= a < 1
  *   b      Pitman-Yor concentration, > 0
  *   gamma  symmetric Dirichlet prior of the shadow base phi0_k, > 0
- * Errors: E_ARG, E_NOMEM, E_HIP, E_RANGE (Stirling cache beyond 4 GiB, or a
+ * Errors: E_ARG, E_NOMEM, E_HIP, E_RANGE (Stirling cache beyond 8 GiB, or a
  * (group, word) pair occurring 65536 times or more: counts are held in 16 bits).
  * On success *out holds the new state; on error *out is NULL.
  */

@@ -34,7 +34,7 @@ int fail(int code, const char *fmt, ...)
             return fail(SPDP_E_HIP, "%s failed: %s", #expr, hipGetErrorString(e_));        \
     } while (0)
 
-constexpr int64_t kStirlingBudget = 4ll << 30;  // bytes for log S + ratio pairs
+constexpr int64_t kStirlingBudget = 8ll << 30;  // bytes for log S + fp32 and fp64 ratio pairs
 
 struct EventPair {
     hipEvent_t a, b;
@@ -393,12 +393,13 @@ int create_state(const spdp_corpus *corpus, const spdp_groups *groups, const spd
     // Stirling cache
     const int64_t n_logS = tri_index(m.ncap + 1, 0);  // rows 0..ncap
     const int64_t n_Q = tri_index(m.ncap, 0);         // rows 0..ncap-1
-    if (n_logS * 8 + n_Q * 8 > kStirlingBudget || m.ncap >= 65535)
+    if (n_logS * 8 + n_Q * 24 > kStirlingBudget || m.ncap >= 65535)
         TRY(fail(SPDP_E_RANGE, "Stirling cache for %d customers exceeds its budget", m.ncap));
     TRY(dev_alloc(s, &B.logS, n_logS, "log Stirling table"));
     TRY(dev_alloc(s, &B.Q, n_Q, "Stirling ratio pairs"));
+    TRY(dev_alloc(s, &B.Q64, n_Q, "fp64 Stirling ratio pairs"));
     TRY(dev_alloc(s, &B.lfact, (int64_t)m.ncap + 1, "log factorials"));
-    TRY_HIP(launch_stirling(m, B.logS, B.Q, B.lfact, s->st));
+    TRY_HIP(launch_stirling(m, B.logS, B.Q, B.Q64, B.lfact, s->st));
 
     // state and counts
     TRY(dev_alloc(s, &B.zr[0], N, "zr"));
@@ -424,6 +425,7 @@ int create_state(const spdp_corpus *corpus, const spdp_groups *groups, const spd
         x.Bk = B.Bk;
         x.B = B.B;
         x.logS = B.logS;
+        x.Q64 = B.Q64;
         x.a = a;
         x.b = b;
         x.Vgamma = (double)V * gamma;

@@ -60,14 +60,26 @@ struct SampleArgs {
 // rotating row buffers.
 constexpr int32_t kChunk = 48;
 
-// Relative distance from a CDF boundary below which the fp32 decision is
-// re-taken in fp64.  The fp32 prefix sums are within about 3e-6 of the exact
-// ones (at most 7 roundings per weight, at most 2 KPL + 6 additions per
-// prefix, KPL <= 16), so outside this margin both decisions agree.
-constexpr float kFixMargin = 8e-6f;
+// Distance from a CDF boundary, as a fraction of the total, below which the
+// fp32 decision is taken again in fp64.  To first order in u = 2^-24 against
+// exact arithmetic: every fp32 weight carries at most 9 relative roundings
+// (alpha, gamma, the per-topic constant and the ratio pair each rounded once
+// from fp64, the two sums with counts, three products), which moves the
+// target's distance to any boundary by at most 9u of the total; the
+// summation of a boundary (2 KPL - 1 lane-local additions, 6 in the wave
+// scan) and of the total behind the target each add at most (2 KPL + 5)u;
+// the target's product, its lane offset, the compared boundary and the
+// distance itself one rounding each.  So the fp32 distance is within
+// (4 KPL + 23)u of the exact one, and outside (4 KPL + 32)u both decisions
+// agree.
+template <int KPL>
+__device__ __forceinline__ float fix_margin()
+{
+    return (float)(4 * KPL + 32) * 5.97e-8f;
+}
 
 // fp64 weights of outcome pair k, evaluated directly from the integer counts
-// and the fp64 log Stirling table (the rare boundary path).
+// and the fp64 ratio pairs (the rare boundary path).
 struct Exact {
     double w1, w0;
 };
@@ -84,17 +96,8 @@ __device__ Exact exact_pair(const ExactCtx &A, int32_t k, int32_t k0, int32_t r0
     const double N = (double)(Ng[k] - del), T = (double)(Tg[k] - del * r0);
     const double Bt = (double)(A.Bk[k] - del * r0);
     const double doc = A.alpha + (double)(c_raw - del);
-    double q0, q1;
-    if (nn <= 0) {
-        q0 = 0.0;
-        q1 = 1.0;
-    } else {
-        const int64_t n_ = nn < A.ncap ? nn : A.ncap - 1;
-        const int64_t t_ = tt < 0 ? 0 : (tt > n_ ? n_ : tt);
-        const double ls = A.logS[tri_index(n_, t_)];
-        q0 = (double)(n_ - t_ + 1) / (double)(n_ + 1) * exp(A.logS[tri_index(n_ + 1, t_)] - ls);
-        q1 = (double)(t_ + 1) / (double)(n_ + 1) * exp(A.logS[tri_index(n_ + 1, t_ + 1)] - ls);
-    }
+    const double2 qq = A.Q64[exact_q_index(A, (int32_t)nn, (int32_t)tt)];
+    const double q0 = qq.x, q1 = qq.y;
     e.w0 = doc / (A.b + N) * q0;
     e.w1 = doc * (A.b + A.a * T) / (A.b + N) * (A.gamma + bw) / (A.Vgamma + Bt) * q1;
     return e;
@@ -111,6 +114,12 @@ struct Rows {
     {
         if constexpr (WIDE) return (int32_t)bw[j];
         else return (int32_t)((bw[j >> 1] >> (16 * (j & 1))) & 0xFFFFu);
+    }
+    // the same for a wave-uniform j that is not a compile-time constant
+    __device__ __forceinline__ int32_t b_at(int j) const
+    {
+        if constexpr (WIDE) return (int32_t)pick(bw, j);
+        else return (int32_t)((pick(bw, j >> 1) >> (16 * (j & 1))) & 0xFFFFu);
     }
 };
 
@@ -254,30 +263,33 @@ __device__ __forceinline__ void sample_token(const SampleArgs &A, DocWave<KPL> &
             // target is within rounding distance of either
             const float hi = readlane_f(excl + s[cL], L);
             const float lo = readlane_f(cL > 0 ? excl + s[cL > 0 ? cL - 1 : 0] : excl, L);
-            const float margin = kFixMargin * total;
+            const float margin = fix_margin<KPL>() * total;
             fix = (target - lo < margin) || (hi - target < margin);
             jstar = L * NO + cL;
         }
         if (fix) {
             // The draw is within rounding distance of a CDF boundary (or the
             // fp32 scan found no crossing): take it again with fp64 weights
-            // from the integer counts, fp64 prefix sums and the same uniform
-            // (rolled loops re-reading the current rows from memory keep this
-            // rare path from raising the kernel's register count).
-            const int32_t q = readlane(W.gw_c, x);
+            // from the integer counts, fp64 prefix sums and the same uniform.
+            // Rolled loops keep this rare path from raising the kernel's
+            // register count; each step picks its cell's counts out of the
+            // rows in registers, so its loads (the group's totals and the
+            // cell's fp64 ratio pair) go out together: one memory round trip.
             const ExactCtx &X = *A.exact;
             const int32_t *__restrict__ Ng = X.Ngk + W.gK;
             const int32_t *__restrict__ Tg = X.Tgk + W.gK;
-            const int32_t *__restrict__ crow = A.nt + (int64_t)q * A.Kp;
-            const int32_t *__restrict__ brow = X.B + (int64_t)(q - W.gV) * A.Kp;
             double acc64 = 0.0;
+            int32_t last64 = -1;
 #pragma unroll 1
             for (int j = 0; j < KPL; ++j) {
                 const int32_t k = kbase + j;
                 if (k >= A.K) break;
-                const Exact e = exact_pair(X, k, k0, r0, crow[k], brow[k], W.c_lds[k], Ng, Tg);
+                const Exact e =
+                    exact_pair(X, k, k0, r0, pick(cur.n, j), cur.b_at(j), W.c_lds[k], Ng, Tg);
                 acc64 += e.w1;
+                if (e.w1 > 0.0) last64 = 2 * j;
                 acc64 += e.w0;
+                if (e.w0 > 0.0) last64 = 2 * j + 1;
             }
             double incl64 = acc64;
 #pragma unroll
@@ -289,23 +301,29 @@ __device__ __forceinline__ void sample_token(const SampleArgs &A, DocWave<KPL> &
             if (lane == 0) run = 0.0;
             const double total64 = __shfl(incl64, 63);
             const double target64 = (double)u * total64;
-            int32_t cand64 = -1, last64 = -1;
+            // the first outcome whose prefix exceeds the target: only lanes
+            // whose prefix ends above the target walk, each up to its first
+            int32_t cand64 = -1;
+            if (incl64 > target64) {
 #pragma unroll 1
-            for (int j = 0; j < KPL; ++j) {
-                const int32_t k = kbase + j;
-                if (k >= A.K) break;
-                const Exact e = exact_pair(X, k, k0, r0, crow[k], brow[k], W.c_lds[k], Ng, Tg);
-                run += e.w1;
-                if (e.w1 > 0.0) {
-                    last64 = 2 * j;
-                    if (cand64 < 0 && run > target64) cand64 = 2 * j;
-                }
-                run += e.w0;
-                if (e.w0 > 0.0) {
-                    last64 = 2 * j + 1;
-                    if (cand64 < 0 && run > target64) cand64 = 2 * j + 1;
+                for (int j = 0; j < KPL; ++j) {
+                    const int32_t k = kbase + j;
+                    if (k >= A.K) break;
+                    const Exact e = exact_pair(X, k, k0, r0, pick(cur.n, j), cur.b_at(j),
+                                               W.c_lds[k], Ng, Tg);
+                    run += e.w1;
+                    if (e.w1 > 0.0 && run > target64) {
+                        cand64 = 2 * j;
+                        break;
+                    }
+                    run += e.w0;
+                    if (e.w0 > 0.0 && run > target64) {
+                        cand64 = 2 * j + 1;
+                        break;
+                    }
                 }
             }
+            // (the last positive outcome if rounding leaves none)
             jstar = -1;
             const unsigned long long m2 = __ballot(cand64 >= 0);
             if (m2) {

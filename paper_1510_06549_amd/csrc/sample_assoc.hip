@@ -83,6 +83,12 @@ struct ARows {
         if constexpr (WIDE) return (int32_t)bw[s][j];
         else return (int32_t)((bw[s][j >> 1] >> (16 * (j & 1))) & 0xFFFFu);
     }
+    // the same for a wave-uniform j that is not a compile-time constant
+    __device__ __forceinline__ int32_t b_at(int s, int j) const
+    {
+        if constexpr (WIDE) return (int32_t)pick(bw[s], j);
+        else return (int32_t)((pick(bw[s], j >> 1) >> (16 * (j & 1))) & 0xFFFFu);
+    }
 };
 
 template <int KPL, int SP>
@@ -122,16 +128,21 @@ __device__ __forceinline__ void lds_row_whole(float (&v)[KPL], const float *base
     }
 }
 
-// Relative distance from a CDF boundary below which the fp32 decision is
-// re-taken in fp64.  A weight carries at most 8 + SP roundings (the p-weighted
-// sum of SP positive terms included) and a prefix at most 2 KPL + 8 further
-// additions of terms below the total, each within 2^-24 relative: the prefix
-// error is below (2 KPL + SP + 16) 2^-24 of the total, and the margin adds
-// that bound, doubled, to the plain kernel's 8e-6.
+// Distance from a CDF boundary, as a fraction of the total, below which the
+// fp32 decision is taken again in fp64.  To first order in u = 2^-24, as in
+// the plain kernel: a topic's head term carries at most 10 + SP relative
+// roundings (the factor (alpha + c) f1 Q1 six, each source's p and gamma + B
+// three, the fused p-weighted sum SP, the product one) and its r = 0 term 6;
+// the summations of a boundary and of the total behind the target each add
+// at most (2 KPL + 5)u; the target, its lane offset, the compared boundary
+// and the distance one rounding each; the crossing topic's slot prefixes are
+// formed with the same roundings.  So the fp32 distance is within
+// (4 KPL + SP + 24)u of the exact one, and outside (4 KPL + SP + 32)u both
+// decisions agree.
 template <int KPL, int SP>
 __device__ __forceinline__ float fix_margin()
 {
-    return 8e-6f + 2.0f * (float)(2 * KPL + SP + 16) * 5.97e-8f;
+    return (float)(4 * KPL + SP + 32) * 5.97e-8f;
 }
 
 template <int KPL, int SP, bool WIDE>
@@ -184,12 +195,14 @@ __device__ __forceinline__ void load_astream(const AssocArgs &A, AWave<KPL, SP> 
     asm volatile("" ::"v"(W.gw_c), "v"(W.zr_c));
 }
 
-// fp64 weights of topic k's SP + 1 outcomes from the integer counts, the fp64
-// log Stirling table and the fp64 p of the row (the rare boundary path).
+// fp64 weights of topic k's SP + 1 outcomes from the integer counts (the
+// packed cell nt_raw, the source-keyed base counts b_raw of the row's
+// sources, the document count c_raw), the fp64 ratio pairs and the fp64 p of
+// the row (the rare boundary path).
 template <int SP>
 __device__ void exact_topic(const ExactCtx &X, int32_t k, int32_t k0, int32_t r0, int32_t s0,
-                            bool sole, int32_t nt_raw, int32_t c_raw, const int32_t *Ng,
-                            const int32_t *Tg, const int32_t *src, const double *p64, int32_t Kp,
+                            bool sole, int32_t nt_raw, const int32_t (&b_raw)[SP], int32_t c_raw,
+                            const int32_t *Ng, const int32_t *Tg, const double *p64,
                             double (&w1)[SP], double &w0)
 {
     const int32_t del = (k == k0) ? 1 : 0;
@@ -197,7 +210,7 @@ __device__ void exact_topic(const ExactCtx &X, int32_t k, int32_t k0, int32_t r0
     if (sole) {
 #pragma unroll
         for (int s = 0; s < SP; ++s) {
-            const int32_t bv = X.B[(int64_t)src[s] * Kp + k] - ((del && s == s0) ? 1 : 0);
+            const int32_t bv = b_raw[s] - ((del && s == s0) ? 1 : 0);
             w1[s] = del ? p64[s] * (X.gamma + (double)bv) : 0.0;
         }
         return;
@@ -207,20 +220,11 @@ __device__ void exact_topic(const ExactCtx &X, int32_t k, int32_t k0, int32_t r0
     const double N = (double)(Ng[k] - del), T = (double)(Tg[k] - del * r0);
     const double Bt = (double)(X.Bk[k] - del * r0);
     const double doc = X.alpha + (double)(c_raw - del);
-    double q0, q1;
-    if (nn <= 0) {
-        q0 = 0.0;
-        q1 = 1.0;
-    } else {
-        const int64_t n_ = nn < X.ncap ? nn : X.ncap - 1;
-        const int64_t t_ = tt < 0 ? 0 : (tt > n_ ? n_ : tt);
-        const double ls = X.logS[tri_index(n_, t_)];
-        q0 = (double)(n_ - t_ + 1) / (double)(n_ + 1) * exp(X.logS[tri_index(n_ + 1, t_)] - ls);
-        q1 = (double)(t_ + 1) / (double)(n_ + 1) * exp(X.logS[tri_index(n_ + 1, t_ + 1)] - ls);
-    }
+    const double2 qq = X.Q64[exact_q_index(X, (int32_t)nn, (int32_t)tt)];
+    const double q0 = qq.x, q1 = qq.y;
 #pragma unroll
     for (int s = 0; s < SP; ++s) {
-        const int32_t bv = X.B[(int64_t)src[s] * Kp + k] - ((del && r0 && s == s0) ? 1 : 0);
+        const int32_t bv = b_raw[s] - ((del && r0 && s == s0) ? 1 : 0);
         w1[s] = p64[s] * doc * (X.b + X.a * T) / (X.b + N) * (X.gamma + (double)bv) /
                 (X.Vgamma + Bt) * q1;
     }
@@ -383,26 +387,34 @@ __device__ __forceinline__ void sample_token_assoc(const AssocArgs &A, AWave<KPL
     }
     if (fix) {
         // fp64 weights from the integer counts, fp64 prefix sums, the same
-        // uniform; rolled loops re-reading the rows keep this rare path from
-        // raising the register count
+        // uniform.  Rolled loops keep this rare path from raising the register
+        // count; each step picks its cell's counts out of the rows in
+        // registers, so its loads (the group's totals and the cell's fp64
+        // ratio pair) go out together: one memory round trip.
         const int32_t q = readlane(W.gw_c, x);
         const ExactCtx &X = *A.exact;
         const int32_t *__restrict__ Ng = X.Ngk + W.gK;
         const int32_t *__restrict__ Tg = X.Tgk + W.gK;
-        const int32_t *__restrict__ crow = A.nt + (int64_t)q * A.Kp;
-        const int32_t *__restrict__ src = X.srcrec + (int64_t)q * (2 * SP);
         const double *__restrict__ p64 = X.p64 + (int64_t)q * SP;
         double acc64 = 0.0;
+        int32_t lastp = -1;
 #pragma unroll 1
         for (int j = 0; j < KPL; ++j) {
             const int32_t k = kbase + j;
             if (k >= A.K) break;
+            int32_t bj[SP];
+#pragma unroll
+            for (int s = 0; s < SP; ++s) bj[s] = cur.b_at(s, j);
             double w1[SP], w0;
-            exact_topic<SP>(X, k, k0, r0, s0, sole, crow[k], W.c_lds[k], Ng, Tg, src, p64, A.Kp,
+            exact_topic<SP>(X, k, k0, r0, s0, sole, pick(cur.n, j), bj, W.c_lds[k], Ng, Tg, p64,
                             w1, w0);
 #pragma unroll
-            for (int s = 0; s < SP; ++s) acc64 += w1[s];
+            for (int s = 0; s < SP; ++s) {
+                acc64 += w1[s];
+                if (w1[s] > 0.0) lastp = j * (SP + 1) + s;
+            }
             acc64 += w0;
+            if (w0 > 0.0) lastp = j * (SP + 1) + SP;
         }
         double incl64 = acc64;
 #pragma unroll
@@ -414,28 +426,31 @@ __device__ __forceinline__ void sample_token_assoc(const AssocArgs &A, AWave<KPL
         if (lane == 0) run = 0.0;
         const double total64 = __shfl(incl64, 63);
         const double target64 = (double)u * total64;
-        int32_t cand = -1, lastp = -1;
+        // the first outcome whose prefix exceeds the target: only lanes whose
+        // prefix ends above the target walk, each up to its first
+        int32_t cand = -1;
+        if (incl64 > target64) {
 #pragma unroll 1
-        for (int j = 0; j < KPL; ++j) {
-            const int32_t k = kbase + j;
-            if (k >= A.K) break;
-            double w1[SP], w0;
-            exact_topic<SP>(X, k, k0, r0, s0, sole, crow[k], W.c_lds[k], Ng, Tg, src, p64, A.Kp,
-                            w1, w0);
+            for (int j = 0; j < KPL; ++j) {
+                const int32_t k = kbase + j;
+                if (k >= A.K) break;
+                int32_t bj[SP];
 #pragma unroll
-            for (int s = 0; s < SP; ++s) {
-                run += w1[s];
-                if (w1[s] > 0.0) {
-                    lastp = j * (SP + 1) + s;
-                    if (cand < 0 && run > target64) cand = j * (SP + 1) + s;
+                for (int s = 0; s < SP; ++s) bj[s] = cur.b_at(s, j);
+                double w1[SP], w0;
+                exact_topic<SP>(X, k, k0, r0, s0, sole, pick(cur.n, j), bj, W.c_lds[k], Ng, Tg,
+                                p64, w1, w0);
+#pragma unroll
+                for (int s = 0; s < SP; ++s) {
+                    run += w1[s];
+                    if (cand < 0 && w1[s] > 0.0 && run > target64) cand = j * (SP + 1) + s;
                 }
-            }
-            run += w0;
-            if (w0 > 0.0) {
-                lastp = j * (SP + 1) + SP;
-                if (cand < 0 && run > target64) cand = j * (SP + 1) + SP;
+                run += w0;
+                if (cand < 0 && w0 > 0.0 && run > target64) cand = j * (SP + 1) + SP;
+                if (cand >= 0) break;
             }
         }
+        // (the last positive outcome if rounding leaves none)
         int32_t jl = -1, Lx = -1;
         const unsigned long long m2 = __ballot(cand >= 0);
         if (m2) {

@@ -109,6 +109,33 @@ __device__ __forceinline__ void load_slice_f(float (&s)[KPL], const float *__res
     for (int j = 0; j < KPL; ++j) s[j] = __int_as_float(tmp[j]);
 }
 
+// Element j of a register array for a j that is not a compile-time constant:
+// a chain of selects, since indexing the array would place it in scratch
+// memory (the empty asm keeps each element an opaque register value, so that
+// the compiler does not turn the chain back into an indexed access).
+template <typename T, int N>
+__device__ __forceinline__ T pick(const T (&v)[N], int j)
+{
+    T r = v[0];
+    asm volatile("" : "+v"(r));
+#pragma unroll
+    for (int i = 1; i < N; ++i) {
+        T x = v[i];
+        asm volatile("" : "+v"(x));
+        r = (j == i) ? x : r;
+    }
+    return r;
+}
+
+// Index of the fp64 ratio pair of a cell with nn customers and tt tables
+// (the token removed); an empty cell takes pair (0, 0) = (0, 1).
+__device__ __forceinline__ int64_t exact_q_index(const ExactCtx &X, int32_t nn, int32_t tt)
+{
+    const int32_t n_ = nn <= 0 ? 0 : (nn < X.ncap ? nn : X.ncap - 1);
+    const int32_t t_ = tt < 0 ? 0 : (tt > n_ ? n_ : tt);
+    return tri_index(n_, t_);
+}
+
 __device__ __forceinline__ int32_t readlane(int32_t x, int32_t lane)
 {
     return __builtin_amdgcn_readlane(x, lane);

@@ -115,29 +115,38 @@ __global__ void __launch_bounds__(1024) k_stirling_rows(int32_t nmax, double a,
     }
 }
 
-// Folded ratio pairs for 0 <= t <= n < nmax, computed in fp64, rounded once:
+// Folded ratio pairs for 0 <= t <= n < nmax, computed in fp64:
 //   Q0(n, t) = (n - t + 1)/(n + 1) * S^{n+1}_t / S^n_t        (outcome r = 0)
 //   Q1(n, t) = (t + 1)/(n + 1) * S^{n+1}_{t+1} / S^n_t        (outcome r = 1)
 // with Q(0, 0) = (0, 1); entries with t = 0 < n (no valid state) are (0, 0).
+// Q holds them rounded once to fp32 (the sampling path), Q64 in fp64 (the
+// boundary path), each factor evaluated as the conditional states it: the
+// count ratio divided out, times the exponential of the log-table difference.
 __global__ void k_stirling_pairs(int32_t nmax, const double *__restrict__ logS,
-                                 float2 *__restrict__ Q)
+                                 float2 *__restrict__ Q, double2 *__restrict__ Q64)
 {
     const int64_t n = blockIdx.y;
     const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (n >= nmax || t > n) return;
     float2 q;
+    double2 q64;
     if (n == 0) {
         q = make_float2(0.0f, 1.0f);
+        q64 = make_double2(0.0, 1.0);
     } else if (t == 0) {
         q = make_float2(0.0f, 0.0f);
+        q64 = make_double2(0.0, 0.0);
     } else {
         const double base = logS[tri_index(n, t)];
         const double r0 = exp(logS[tri_index(n + 1, t)] - base);
         const double r1 = exp(logS[tri_index(n + 1, t + 1)] - base);
         const double inv = 1.0 / (double)(n + 1);
         q = make_float2((float)((double)(n - t + 1) * inv * r0), (float)((double)(t + 1) * inv * r1));
+        q64 = make_double2((double)(n - t + 1) / (double)(n + 1) * r0,
+                           (double)(t + 1) / (double)(n + 1) * r1);
     }
     Q[tri_index(n, t)] = q;
+    Q64[tri_index(n, t)] = q64;
 }
 
 __global__ void k_lfact(int32_t nmax, double *__restrict__ lfact)
@@ -332,14 +341,15 @@ hipError_t launch_max_i32(const int32_t *x, int64_t n, int32_t *out, hipStream_t
     return hipGetLastError();
 }
 
-hipError_t launch_stirling(const Model &m, double *logS, float2 *Q, double *lfact, hipStream_t st)
+hipError_t launch_stirling(const Model &m, double *logS, float2 *Q, double2 *Q64, double *lfact,
+                           hipStream_t st)
 {
     const int32_t nmax = m.ncap;  // rows 0..ncap of log S; pairs for n < ncap
     hipLaunchKernelGGL(k_stirling_rows, dim3(1), dim3(1024), 0, st, nmax, m.a, logS);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     dim3 grid((unsigned)blocks_for(nmax, kBlock), (unsigned)nmax);
-    hipLaunchKernelGGL(k_stirling_pairs, grid, dim3(kBlock), 0, st, nmax, logS, Q);
+    hipLaunchKernelGGL(k_stirling_pairs, grid, dim3(kBlock), 0, st, nmax, logS, Q, Q64);
     e = hipGetLastError();
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(k_lfact, dim3((unsigned)blocks_for(nmax + 1, kBlock)), dim3(kBlock), 0, st,

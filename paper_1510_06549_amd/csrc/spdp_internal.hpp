@@ -104,6 +104,7 @@ struct Model {
 struct ExactCtx {
     const int32_t *Ngk, *Tgk, *Bk, *B;
     const double *logS;
+    const double2 *Q64;  // [tri(ncap)] fp64 (Q0, Q1) ratio pairs
     double a, b, Vgamma, alpha, gamma;
     int32_t K, ncap;
     // word associations: source records and fp64 p of each row (Sp slots)
@@ -132,6 +133,7 @@ struct DeviceBuffers {
                                   //   1/(b + N - 1), and f1 for a removed non-head / head
     float2 *Q = nullptr;          // [tri(ncap)] (Q0, Q1) folded Stirling ratios
     double *logS = nullptr;       // [tri(ncap + 1)] log S^n_{t,a}
+    double2 *Q64 = nullptr;       // [tri(ncap)] the ratio pairs in fp64
     double *lfact = nullptr;      // [ncap + 1] log n!
     uint32_t *rep_part = nullptr; // [G V] heads promoted per row in the last rebuild
     unsigned long long *part = nullptr; // reduction partials
@@ -170,7 +172,8 @@ hipError_t launch_make_gw(const Model &m, const int32_t *words, const int64_t *d
                           const int32_t *doc_group, int32_t *gw, int32_t *gw_count,
                           int32_t *bad, hipStream_t st);
 hipError_t launch_max_i32(const int32_t *x, int64_t n, int32_t *out, hipStream_t st);
-hipError_t launch_stirling(const Model &m, double *logS, float2 *Q, double *lfact, hipStream_t st);
+hipError_t launch_stirling(const Model &m, double *logS, float2 *Q, double2 *Q64, double *lfact,
+                           hipStream_t st);
 hipError_t launch_init_z(const Model &m, uint64_t seed, int32_t *zr, hipStream_t st);
 hipError_t launch_pack_zr(const Model &m, const int32_t *z, const uint8_t *r, int32_t *zr,
                           int32_t *bad, hipStream_t st);
