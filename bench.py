@@ -68,14 +68,15 @@ def dense_bytes_per_token(K: int) -> int:
     return 12 * K + 12
 
 
-def recorded_traffic(workload: str):
-    """HBM bytes per k_sample launch measured with rocprofv3 counters, if they
-    were taken on the current sampler source (profiles/traffic_*.txt holds
-    the figure with the SHA-256 of sample.hip followed by sampler_common.hpp
-    at the time), else None."""
+def recorded_traffic(kernel: str, workload: str):
+    """HBM bytes per launch of the sampling kernel measured with rocprofv3
+    counters, if they were taken on the current source of that kernel
+    (profiles/traffic_<kernel>_<workload>.txt holds the figure with the
+    SHA-256 of the kernel's source followed by sampler_common.hpp at the
+    time), else None."""
     import hashlib
 
-    path = os.path.join(ROOT, "profiles", f"traffic_k_sample_{workload}.txt")
+    path = os.path.join(ROOT, "profiles", f"traffic_{kernel}_{workload}.txt")
     csrc = os.path.join(ROOT, "paper_1510_06549_amd", "csrc")
     if not os.path.exists(path):
         return None
@@ -84,11 +85,11 @@ def recorded_traffic(workload: str):
         if ":" in line and not line.startswith("#"):
             k, v = line.split(":", 1)
             kv[k.strip()] = v.strip()
+    source = {"k_sample": "sample.hip", "k_sample_assoc": "sample_assoc.hip"}[kernel]
     h = hashlib.sha256()
-    for name in ("sample.hip", "sampler_common.hpp"):
+    for name in (source, "sampler_common.hpp"):
         h.update(open(os.path.join(csrc, name), "rb").read())
-    sha = h.hexdigest()
-    if kv.get("sample_hip_sha256") != sha or "bytes_per_launch" not in kv:
+    if kv.get("source_sha256") != h.hexdigest() or "bytes_per_launch" not in kv:
         return None
     return float(kv["bytes_per_launch"])
 
@@ -243,7 +244,7 @@ def main():
         traffic = None
     elif assoc is None:
         bpt = sample_bytes_per_token(wl.K, wide)
-        traffic = recorded_traffic(wl.name)
+        traffic = recorded_traffic("k_sample", wl.name)
     else:
         # mean length of the source list of each token's row
         lens = np.diff(assoc[0])
@@ -251,7 +252,8 @@ def main():
         mean_sources = float(lens[q].mean())
         Sp = 1 if s.S <= 1 else (2 if s.S <= 2 else (4 if s.S <= 4 else 8))
         bpt = assoc_bytes_per_token(wl.K, wide, mean_sources, Sp)
-        traffic = None
+        traffic = (recorded_traffic("k_sample_assoc", f"{wl.name}-assoc{args.assoc}")
+                   if args.assoc_eps == 0.3 else None)
     alg = N * bpt
     achieved = alg / avg_sample_s / 1e9
     roofline = {
