@@ -44,54 +44,65 @@ __global__ void k_iota(int32_t *__restrict__ x, int64_t n)
     if (i < n) x[i] = (int32_t)i;
 }
 
-// One 64-lane block per count row.
+// The row's tokens' states, four per lane in flight: lane l takes row list
+// entries rs + l, rs + l + 64, ... and hands each (list index j, state v) to
+// f in any order.
+template <typename F>
+__device__ __forceinline__ void for_row_states(int32_t rs, int32_t re, int32_t lane,
+                                               const int32_t *__restrict__ perm,
+                                               const int32_t *__restrict__ zr, F &&f)
+{
+    int32_t j = rs + lane;
+    for (; j + 192 < re; j += 256) {
+        int32_t t[4], v[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) t[u] = perm[j + 64 * u];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) v[u] = zr[t[u]];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) f(j + 64 * u, v[u]);
+    }
+    for (; j < re; j += 64) f(j, zr[perm[j]]);
+}
+
+// One 64-lane block per count row; the row's histogram and the first list
+// index of each topic in LDS (2 Kp ints of dynamic shared memory).  Every
+// token's state is read once: a cell left with customers but no table holds
+// only r = 0 tokens, and its first token in the row list (the smallest token
+// index, the list being a stable sort) becomes its head.
 __global__ void __launch_bounds__(64) k_rows(int32_t Kp, const int32_t *__restrict__ row_off,
                                              const int32_t *__restrict__ perm,
                                              int32_t *__restrict__ zr, int32_t *__restrict__ nt,
                                              uint32_t *__restrict__ rep_part)
 {
-    __shared__ int32_t h[SPDP_MAX_K];
-    __shared__ int32_t first[SPDP_MAX_K];
+    extern __shared__ int32_t rows_lds[];
+    int32_t *h = rows_lds, *first = rows_lds + Kp;
     const int64_t q = blockIdx.x;
     const int32_t lane = threadIdx.x;
     const int32_t rs = row_off[q], re = row_off[q + 1];
     uint32_t rep = 0;
     if (rs < re) {
-        for (int32_t k = lane; k < Kp; k += 64) h[k] = 0;
-        __syncthreads();
-        for (int32_t j = rs + lane; j < re; j += 64) {
-            const int32_t v = zr[perm[j]];
-            atomicAdd(&h[v >> 1], 1 + ((v & 1) << 16));
-        }
-        __syncthreads();
-        int broken = 0;
         for (int32_t k = lane; k < Kp; k += 64) {
-            const int32_t x = h[k];
-            const bool br = (x != 0) && ((x >> 16) == 0);
-            first[k] = br ? INT_MAX : -1;
-            broken |= br;
+            h[k] = 0;
+            first[k] = INT_MAX;
         }
-        if (__syncthreads_or(broken)) {
-            // a cell without a table holds only r = 0 tokens; its first one
-            // in token order (= first in the row list) becomes the head
-            for (int32_t j = rs + lane; j < re; j += 64) {
-                const int32_t k = zr[perm[j]] >> 1;
-                if (first[k] >= 0) atomicMin(&first[k], j);
-            }
-            __syncthreads();
-            for (int32_t k = lane; k < Kp; k += 64) {
-                const int32_t j = first[k];
-                if (j >= 0 && j != INT_MAX) {
-                    const int32_t tok = perm[j];
-                    zr[tok] = zr[tok] | 1;
-                    h[k] += 1 << 16;
-                    ++rep;
-                }
-            }
-            __syncthreads();
-        }
+        __syncthreads();
+        for_row_states(rs, re, lane, perm, zr, [&](int32_t j, int32_t v) {
+            atomicAdd(&h[v >> 1], 1 + ((v & 1) << 16));
+            atomicMin(&first[v >> 1], j);
+        });
+        __syncthreads();
         int32_t *__restrict__ row = nt + q * Kp;
-        for (int32_t k = lane; k < Kp; k += 64) row[k] = h[k];
+        for (int32_t k = lane; k < Kp; k += 64) {
+            int32_t x = h[k];
+            if (x != 0 && (x >> 16) == 0) {
+                const int32_t tok = perm[first[k]];
+                zr[tok] = zr[tok] | 1;
+                x += 1 << 16;
+                ++rep;
+            }
+            row[k] = x;
+        }
     }
     for (int o = 32; o > 0; o >>= 1) rep += __shfl_xor(rep, o);
     if (lane == 0) rep_part[q] = rep;
@@ -111,51 +122,39 @@ __global__ void __launch_bounds__(64) k_rows_assoc(int32_t Kp, int32_t Sp,
                                                    int32_t *__restrict__ B,
                                                    uint32_t *__restrict__ rep_part)
 {
-    __shared__ int32_t h[SPDP_MAX_K];
-    __shared__ int32_t first[SPDP_MAX_K];
+    extern __shared__ int32_t rows_lds[];
+    int32_t *h = rows_lds, *first = rows_lds + Kp;
     const int64_t q = blockIdx.x;
     const int32_t lane = threadIdx.x;
     const int32_t rs = row_off[q], re = row_off[q + 1];
     const int32_t *__restrict__ src = srcrec + q * 2 * Sp;
     uint32_t rep = 0;
     if (rs < re) {
-        for (int32_t k = lane; k < Kp; k += 64) h[k] = 0;
+        for (int32_t k = lane; k < Kp; k += 64) {
+            h[k] = 0;
+            first[k] = INT_MAX;
+        }
         __syncthreads();
-        for (int32_t j = rs + lane; j < re; j += 64) {
-            const int32_t v = zr[perm[j]];
+        for_row_states(rs, re, lane, perm, zr, [&](int32_t j, int32_t v) {
             const int32_t k = zr_topic(v);
             atomicAdd(&h[k], 1 + ((v & 1) << 16));
+            atomicMin(&first[k], j);
             if (v & 1) atomicAdd(&B[(int64_t)src[zr_slot(v)] * Kp + k], 1);
-        }
+        });
         __syncthreads();
-        int broken = 0;
-        for (int32_t k = lane; k < Kp; k += 64) {
-            const int32_t x = h[k];
-            const bool br = (x != 0) && ((x >> 16) == 0);
-            first[k] = br ? INT_MAX : -1;
-            broken |= br;
-        }
-        if (__syncthreads_or(broken)) {
-            for (int32_t j = rs + lane; j < re; j += 64) {
-                const int32_t k = zr_topic(zr[perm[j]]);
-                if (first[k] >= 0) atomicMin(&first[k], j);
-            }
-            __syncthreads();
-            const int32_t hs = head_slot[q];
-            for (int32_t k = lane; k < Kp; k += 64) {
-                const int32_t j = first[k];
-                if (j >= 0 && j != INT_MAX) {
-                    const int32_t tok = perm[j];
-                    zr[tok] = zr_pack(k, 1, hs);
-                    h[k] += 1 << 16;
-                    atomicAdd(&B[(int64_t)src[hs] * Kp + k], 1);
-                    ++rep;
-                }
-            }
-            __syncthreads();
-        }
+        const int32_t hs = head_slot[q];
         int32_t *__restrict__ row = nt + q * Kp;
-        for (int32_t k = lane; k < Kp; k += 64) row[k] = h[k];
+        for (int32_t k = lane; k < Kp; k += 64) {
+            int32_t x = h[k];
+            if (x != 0 && (x >> 16) == 0) {
+                const int32_t tok = perm[first[k]];
+                zr[tok] = zr_pack(k, 1, hs);
+                x += 1 << 16;
+                atomicAdd(&B[(int64_t)src[hs] * Kp + k], 1);
+                ++rep;
+            }
+            row[k] = x;
+        }
     }
     for (int o = 32; o > 0; o >>= 1) rep += __shfl_xor(rep, o);
     if (lane == 0) rep_part[q] = rep;
@@ -356,7 +355,8 @@ hipError_t build_visit_order(const Model &m, DeviceBuffers &b, hipStream_t st)
 hipError_t launch_rows(const Model &m, const DeviceBuffers &b, int32_t *zr, hipStream_t st)
 {
     const int64_t rows = (int64_t)m.G * m.V;
-    hipLaunchKernelGGL(k_rows, dim3((unsigned)rows), dim3(64), 0, st, m.Kp, b.row_off, b.perm, zr,
+    const size_t lds = 2 * (size_t)m.Kp * sizeof(int32_t);
+    hipLaunchKernelGGL(k_rows, dim3((unsigned)rows), dim3(64), lds, st, m.Kp, b.row_off, b.perm, zr,
                        b.nt, b.rep_part);
     return hipGetLastError();
 }
@@ -376,8 +376,9 @@ hipError_t launch_rows_assoc(const Model &m, const DeviceBuffers &b, int32_t *zr
     const int64_t rows = (int64_t)m.G * m.V;
     hipError_t e = launch_fill_i32(b.B, (int64_t)m.V * m.Kp, 0, st);
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(k_rows_assoc, dim3((unsigned)rows), dim3(64), 0, st, m.Kp, m.Sp, b.row_off,
-                       b.perm, b.srcrec, b.head_slot, zr, b.nt, b.B, b.rep_part);
+    const size_t lds = 2 * (size_t)m.Kp * sizeof(int32_t);
+    hipLaunchKernelGGL(k_rows_assoc, dim3((unsigned)rows), dim3(64), lds, st, m.Kp, m.Sp,
+                       b.row_off, b.perm, b.srcrec, b.head_slot, zr, b.nt, b.B, b.rep_part);
     return hipGetLastError();
 }
 
