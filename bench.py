@@ -122,6 +122,17 @@ def cpu_baseline(cp, wl, state, target_s: float, assoc=None):
     m.sample_docs(c, *[x.copy() for x in state], 0, 1, 0, d_s)
     dt = time.perf_counter() - t0
     toks = int(m.doc_off[d_s])
+    # the same step on one thread, over a sample a fifth as long in time
+    oracle.set_num_threads(1)
+    try:
+        want1 = int(target_s / 5 / (per_tok * threads))
+        d_1 = max(1, min(int(np.searchsorted(m.doc_off, want1)), m.D))
+        t0 = time.perf_counter()
+        m.sample_docs(c, *[x.copy() for x in state], 0, 1, 0, d_1)
+        dt1 = time.perf_counter() - t0
+    finally:
+        oracle.set_num_threads(threads)
+    toks1 = int(m.doc_off[d_1])
     return {
         "value": toks / dt,
         "unit": "tokens/s",
@@ -130,7 +141,23 @@ def cpu_baseline(cp, wl, state, target_s: float, assoc=None):
         "sample": (f"sampling step of the first {d_s} documents ({toks} tokens) against the full "
                    f"sweep-start counts, fp64, OpenMP over documents, {dt:.1f}s; count rebuild "
                    f"excluded"),
+        "value_1thread": toks1 / dt1,
+        "sample_1thread": f"the first {d_1} documents ({toks1} tokens), {dt1:.1f}s",
+        "host_cpu": host_cpu(),
     }
+
+
+def host_cpu() -> str:
+    """The host CPU's model name and logical CPU count."""
+    name = "unknown"
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                name = line.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
+    return f"{name}, {os.cpu_count()} logical CPUs"
 
 
 def main():

@@ -112,6 +112,8 @@ def lib():
         L.or_chain_histogram_ordered.restype = C.c_int
         L.or_num_threads.argtypes = []
         L.or_num_threads.restype = C.c_int
+        L.or_set_num_threads.argtypes = [C.c_int]
+        L.or_set_num_threads.restype = C.c_int
         L.or_estimates.argtypes = [vp, vp, vp, vp, vp, vp]
         L.or_estimates.restype = None
         L.or_heldout.argtypes = [vp, vp, i32, vp, vp, vp, i32, u64, vp, vp]
@@ -471,6 +473,11 @@ class Counts:
 
 def num_threads() -> int:
     return int(lib().or_num_threads())
+
+
+def set_num_threads(n: int) -> int:
+    """Threads of the oracle's OpenMP loops from now on; returns the new count."""
+    return int(lib().or_set_num_threads(int(n)))
 
 
 from .hellinger import align_topics, hellinger  # noqa: E402  (topic-model comparison)

@@ -492,6 +492,18 @@ int or_num_threads(void)
 #endif
 }
 
+/* Threads of the OpenMP loops that follow (n >= 1); returns the new count. */
+int or_set_num_threads(int n)
+{
+#ifdef _OPENMP
+    if (n >= 1) omp_set_num_threads(n);
+    return omp_get_max_threads();
+#else
+    (void)n;
+    return 1;
+#endif
+}
+
 /* ------------------------------------------------------------------------ */
 /* Word order rearrangement (thesis, subsection "Parallelism With Improved    */
 /* Accuracy: Word Order Rearrangement"): tokens are visited round robin over  */
