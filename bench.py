@@ -147,6 +147,35 @@ def cpu_baseline(cp, wl, state, target_s: float, assoc=None):
     }
 
 
+def read_probe(gib: int = 4, row_bytes: int = 2048, waves: int = 4096):
+    """The device's read bandwidth, measured by the library's probe on a
+    buffer of `gib` GiB: read whole, front to back (by 16 * `waves`
+    wavefronts' worth of threads), and read as random rows of `row_bytes`,
+    one row at a time per wavefront (`waves` of them, 16 per compute unit, as
+    the sampler runs), each timed after one untimed run."""
+    import torch
+
+    from paper_1510_06549_amd import spdp as sp
+
+    nbytes = gib << 30
+    buf = torch.ones(nbytes // 4, dtype=torch.int32, device="cuda")
+    torch.cuda.synchronize()
+    ptr = buf.data_ptr()
+    st = torch.cuda.current_stream().cuda_stream
+    out = {"buffer_GiB": gib, "row_bytes": row_bytes, "waves": waves}
+    for key, rb in (("sequential_GBps", 0), ("random_rows_GBps", row_bytes)):
+        rows = nbytes // max(rb, 1) if rb else 0
+        w = 16 * waves if rb == 0 else waves
+        sp.spdp_read_probe(ptr, nbytes, rb, rows, w, st)
+        ms = sp.spdp_read_probe(ptr, nbytes, rb, rows, w, st)
+        moved = nbytes if rb == 0 else -(-rows // waves) * waves * rb
+        out[key] = round(moved / (ms * 1e-3) / 1e9, 1)
+    del buf
+    torch.cuda.synchronize()
+    log(f"[bench] read probe {out}")
+    return out
+
+
 def host_cpu() -> str:
     """The host CPU's model name and logical CPU count."""
     name = "unknown"
@@ -168,6 +197,8 @@ def main():
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-read-probe", action="store_true",
+                    help="skip the read-bandwidth probe reported beside the roofline")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="also run a plain device copy of this size (counter calibration)")
@@ -306,6 +337,9 @@ def main():
             N * dense_bytes_per_token(wl.K) / avg_sample_s / 1e9, 1)
     else:
         roofline["mean_sources_per_token"] = round(mean_sources, 4)
+
+    if not args.no_read_probe:
+        roofline["read_probe"] = read_probe()
 
     cpu = None
     if not args.no_cpu_baseline:

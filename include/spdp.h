@@ -341,6 +341,28 @@ int spdp_kernel_times(spdp_state *s, double *ms, int64_t *launches);
  */
 int spdp_info(const spdp_state *s, int64_t *out8);
 
+/*
+ * Read-bandwidth probe of the device: the ceiling against which the sampler's
+ * bytes per second are read (a measurement aid, not part of the sampling
+ * path).  Reads the device buffer buf (bytes long, 16-byte aligned, inside one
+ * device allocation; the caller owns it) and returns in *ms the elapsed
+ * milliseconds of the launch, from HIP events on stream (a hipStream_t, or
+ * NULL for the null stream).
+ *   row_bytes = 0     the whole buffer once, front to back, by waves
+ *                     wavefronts' worth of threads (rows is ignored);
+ *   row_bytes = 1024, 2048, 3072, 4096 or 8192
+ *                     waves wavefronts read rows rows in all, one whole row at a
+ *                     time per wavefront at pseudo-random row positions among
+ *                     bytes / row_bytes, two rows in flight per wavefront (as
+ *                     the sampler reads a token's count row).
+ * The bytes read are bytes (row_bytes = 0) or ceil(rows / waves) * waves *
+ * row_bytes.  Synchronises.  Errors: E_ARG (NULL buf or ms, misaligned buf,
+ * other row_bytes, bytes below one row, waves outside [1, 2^20], rows < 1 with
+ * rows read, buf not device memory or bytes past its allocation), E_HIP.
+ */
+int spdp_read_probe(const void *buf, int64_t bytes, int32_t row_bytes, int64_t rows,
+                    int32_t waves, void *stream, double *ms);
+
 /* Text of the calling thread's last error ("" if none). */
 const char *spdp_last_error(void);
 

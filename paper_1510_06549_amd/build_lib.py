@@ -11,7 +11,8 @@ CSRC = os.path.join(HERE, "csrc")
 SOURCES = ["api.hip", "setup.hip", "counts.hip", "sample.hip", "sample_assoc.hip", "sample_async.hip",
            "loglik.hip",
            "estimate.hip",
-           "hellinger.hip"]
+           "hellinger.hip",
+           "probe.hip"]
 LIB = os.path.join(HERE, "libspdp.so")
 ARCH = "gfx950"
 

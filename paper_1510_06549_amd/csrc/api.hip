@@ -974,6 +974,46 @@ int spdp_stats(const spdp_state *s, int64_t *changed, int64_t *repaired)
     return SPDP_OK;
 }
 
+int spdp_read_probe(const void *buf, int64_t bytes, int32_t row_bytes, int64_t rows,
+                    int32_t waves, void *stream, double *ms)
+{
+    if (!buf || !ms) return fail(SPDP_E_ARG, "buf or ms is NULL");
+    if ((reinterpret_cast<uintptr_t>(buf) & 15) != 0)
+        return fail(SPDP_E_ARG, "buf is not 16-byte aligned");
+    if (!(row_bytes == 0 || row_bytes == 1024 || row_bytes == 2048 || row_bytes == 3072 ||
+          row_bytes == 4096 || row_bytes == 8192))
+        return fail(SPDP_E_ARG, "row_bytes %d is not 0, 1024, 2048, 3072, 4096 or 8192",
+                    row_bytes);
+    if (bytes < 16 || (row_bytes > 0 && bytes < row_bytes))
+        return fail(SPDP_E_ARG, "bytes %lld is below one row", (long long)bytes);
+    if (waves < 1 || waves > (1 << 20)) return fail(SPDP_E_ARG, "waves %d not in [1, 2^20]", waves);
+    if (row_bytes > 0 && rows < 1) return fail(SPDP_E_ARG, "rows must be positive");
+    hipDeviceptr_t base = nullptr;
+    size_t size = 0;
+    if (hipMemGetAddressRange(&base, &size, const_cast<void *>(buf)) != hipSuccess) {
+        (void)hipGetLastError();
+        return fail(SPDP_E_ARG, "buf is not device memory");
+    }
+    const char *b0 = static_cast<const char *>(base);
+    if (static_cast<const char *>(buf) + bytes > b0 + size)
+        return fail(SPDP_E_ARG, "bytes %lld run past the allocation", (long long)bytes);
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    hipEvent_t a = nullptr, b = nullptr;
+    hipError_t e = hipEventCreate(&a);
+    if (e == hipSuccess) e = hipEventCreate(&b);
+    if (e == hipSuccess) e = hipEventRecord(a, st);
+    if (e == hipSuccess) e = launch_read_probe(buf, bytes, row_bytes, rows, waves, st);
+    if (e == hipSuccess) e = hipEventRecord(b, st);
+    if (e == hipSuccess) e = hipEventSynchronize(b);
+    float t = 0.0f;
+    if (e == hipSuccess) e = hipEventElapsedTime(&t, a, b);
+    if (a) (void)hipEventDestroy(a);
+    if (b) (void)hipEventDestroy(b);
+    HIP_TRY(e);
+    *ms = t;
+    return SPDP_OK;
+}
+
 int spdp_kernel_timing(spdp_state *s, int enable)
 {
     if (!s) return fail(SPDP_E_ARG, "state is NULL");

@@ -248,6 +248,8 @@ hipError_t launch_hellinger(const HellingerPlan &p, const double *P, int32_t kp,
 double align_topics_host(const double *c, int32_t kp, int32_t kq, int32_t *match);
 
 // The sampler's per-lane topic count for K topics (4 at most per dwordx4).
+hipError_t launch_read_probe(const void *buf, int64_t bytes, int32_t row_bytes, int64_t rows,
+                             int32_t waves, hipStream_t st);
 int sampler_kpl(int32_t K);
 int32_t padded_K(int32_t K);
 

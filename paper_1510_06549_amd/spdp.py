@@ -33,7 +33,7 @@ EXPORTS = (
     "spdp_kernel_timing", "spdp_kernel_times", "spdp_info", "spdp_last_error",
     "spdp_estimates", "spdp_heldout", "spdp_hellinger", "spdp_align_topics",
     "spdp_create_assoc", "spdp_get_slots", "spdp_set_assignments_assoc", "spdp_max_sources",
-    "spdp_sweep_async",
+    "spdp_sweep_async", "spdp_read_probe",
 )
 
 
@@ -102,6 +102,8 @@ def load_library() -> C.CDLL:
     L.spdp_kernel_times.restype = cint
     L.spdp_info.argtypes = [vp, vp]
     L.spdp_info.restype = cint
+    L.spdp_read_probe.argtypes = [vp, i64, cint, i64, cint, vp, vp]
+    L.spdp_read_probe.restype = cint
     L.spdp_last_error.argtypes = []
     L.spdp_last_error.restype = C.c_char_p
     L.spdp_estimates.argtypes = [vp, i32, i32, vp, vp, vp, cint]
@@ -290,6 +292,17 @@ def spdp_kernel_times(h):
     n = np.zeros(SPDP_NKERNELS, dtype=np.int64)
     _check(lib().spdp_kernel_times(h, ms.ctypes.data, n.ctypes.data))
     return {k: (float(ms[i]), int(n[i])) for i, k in enumerate(KERNEL_CLASSES)}
+
+
+def spdp_read_probe(buf_ptr: int, nbytes: int, row_bytes: int = 0, rows: int = 0,
+                    waves: int = 4096, stream=None) -> float:
+    """Milliseconds to read a device buffer: whole (row_bytes = 0) or rows of
+    row_bytes at pseudo-random positions, one row at a time per wavefront."""
+    ms = C.c_double(0.0)
+    _check(lib().spdp_read_probe(C.c_void_p(buf_ptr), int(nbytes), int(row_bytes), int(rows),
+                                 int(waves), None if stream is None else C.c_void_p(int(stream)),
+                                 C.byref(ms)))
+    return ms.value
 
 
 def spdp_info(h) -> dict:

@@ -105,3 +105,21 @@ def test_invalid_associations_rejected_without_gpu():
     assert L.spdp_create_assoc(None, None, None, 2, 0.1, 0.5, 1.0, 0.1, None) == sp.SPDP_E_ARG
     assert L.spdp_get_slots(None, None, 0) == sp.SPDP_E_ARG
     assert L.spdp_max_sources(None, None) == sp.SPDP_E_ARG
+
+
+def test_read_probe_arguments_rejected_without_gpu():
+    from paper_1510_06549_amd import spdp as sp
+
+    bad = [
+        dict(buf_ptr=0, nbytes=1 << 20),                              # NULL buffer
+        dict(buf_ptr=16 * 1001 + 8, nbytes=1 << 20),                  # misaligned
+        dict(buf_ptr=1 << 20, nbytes=1 << 20, row_bytes=512, rows=1),  # row size
+        dict(buf_ptr=1 << 20, nbytes=8),                               # below 16 bytes
+        dict(buf_ptr=1 << 20, nbytes=1024, row_bytes=2048, rows=1),    # below one row
+        dict(buf_ptr=1 << 20, nbytes=1 << 20, waves=0),
+        dict(buf_ptr=1 << 20, nbytes=1 << 20, row_bytes=1024, rows=0),
+    ]
+    for kw in bad:
+        with pytest.raises(sp.SpdpError) as e:
+            sp.spdp_read_probe(**kw)
+        assert e.value.code == sp.SPDP_E_ARG, kw
