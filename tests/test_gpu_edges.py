@@ -132,3 +132,27 @@ def test_shadow_base_counts_beyond_16_bits():
     rep, ch, rp = parity.one_step(s, m, 0, 21)
     say(f"  {rep}")
     s.close()
+
+
+def test_read_probe_on_a_device_buffer():
+    """The read probe measures a device buffer and refuses a range past it."""
+    import torch
+
+    from paper_1510_06549_amd import spdp as sp
+
+    say("read probe on a 64 MiB device buffer")
+    nbytes = 64 << 20
+    buf = torch.ones(nbytes // 4, dtype=torch.int32, device="cuda")
+    torch.cuda.synchronize()
+    st = torch.cuda.current_stream().cuda_stream
+    assert sp.spdp_read_probe(buf.data_ptr(), nbytes, 0, 0, 1024, st) > 0.0
+    for rb in (1024, 2048, 3072, 4096, 8192):
+        assert sp.spdp_read_probe(buf.data_ptr(), nbytes, rb, nbytes // rb, 512, st) > 0.0
+    with pytest.raises(sp.SpdpError) as e:
+        sp.spdp_read_probe(buf.data_ptr(), nbytes + 4096, 0, 0, 64, st)
+    assert e.value.code == sp.SPDP_E_ARG
+    host = np.ones(1 << 16, np.int32)
+    with pytest.raises(sp.SpdpError) as e:
+        sp.spdp_read_probe(host.ctypes.data, host.nbytes, 0, 0, 64, st)
+    assert e.value.code == sp.SPDP_E_ARG
+    assert torch.all(buf == 1)
