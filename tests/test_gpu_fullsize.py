@@ -6,7 +6,8 @@ The oracle cannot run a whole sweep of this size in test time, so:
     groups equal the oracle's rebuild of the library's state, bit for bit;
   * sampling: for documents sampled at the start, middle and end of the corpus
     the library's weights, uniforms and draws are compared with the oracle's
-    one by one (same protocol as the small workloads);
+    one by one (same protocol as the small workloads), and the draws of 30 000
+    whole documents (7.5 M tokens) with the oracle's sampling step;
   * update and repair: the library's state after the sweep equals the
     oracle's rebuild and repair of the library's sampled (pre-repair) state,
     for every token.
@@ -83,10 +84,24 @@ def test_largest_workload_sampled_parity():
         assert np.array_equal(u_g[sel].astype(np.float64), u_o[sel])
         del w_g, w_o
 
+    # the draws of 30 000 whole documents (7.5 M tokens) against the oracle's
+    # sampling step, without traces
+    zr_pre = s.sampled(sweep, seed)
+    zgp, rgp = (zr_pre >> 1).astype(np.int32), (zr_pre & 1).astype(np.uint8)
+    zo, ro = z.copy(), r.copy()
+    for d0 in (0, m.D // 2 - 5000, m.D - 10000):
+        d1 = d0 + 10000
+        tb, te = int(m.doc_off[d0]), int(m.doc_off[d1])
+        say(f"  draws of documents [{d0}, {d1}) (tokens [{tb}, {te})) against the oracle")
+        m.sample_docs(c, zo, ro, sweep, seed, d0, d1)
+        same = (zgp[tb:te] == zo[tb:te]) & (rgp[tb:te] == ro[tb:te])
+        say(f"    {int((~same).sum())} of {te - tb} differ")
+        assert same.mean() >= parity.MATCH_FRAC, same.mean()
+    del zgp, rgp, zo, ro
+
     # the whole sweep: library state after update and repair vs the oracle's
     # rebuild and repair of the library's sampled state
     say("  whole sweep: update and repair of all tokens")
-    zr_pre = s.sampled(sweep, seed)
     s.sweep(sweep, seed)
     zs, rs = s.assignments()
     zp, rp = (zr_pre >> 1).astype(np.int32), (zr_pre & 1).astype(np.uint8)
