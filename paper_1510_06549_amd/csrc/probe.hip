@@ -81,6 +81,15 @@ __global__ void __launch_bounds__(64) k_read_rows(const uint4 *__restrict__ p, i
     keep(acc);
 }
 
+template <int CH>
+hipError_t launch_rows(const uint4 *p, int64_t nrows, int64_t per_wave, int32_t waves,
+                       hipStream_t st)
+{
+    hipLaunchKernelGGL((k_read_rows<CH>), dim3((unsigned)waves), dim3(64), 0, st, p, nrows,
+                       per_wave);
+    return hipGetLastError();
+}
+
 }  // namespace
 
 hipError_t launch_read_probe(const void *buf, int64_t bytes, int32_t row_bytes, int64_t rows,
@@ -88,21 +97,20 @@ hipError_t launch_read_probe(const void *buf, int64_t bytes, int32_t row_bytes, 
 {
     const uint4 *p = static_cast<const uint4 *>(buf);
     if (row_bytes == 0) {
-        hipLaunchKernelGGL(k_read_seq, dim3((unsigned)(waves / 4 > 0 ? waves / 4 : 1)), dim3(256),
-                           0, st, p, bytes / 16);
+        const unsigned blocks = (unsigned)(waves / 4 > 0 ? waves / 4 : 1);
+        hipLaunchKernelGGL(k_read_seq, dim3(blocks), dim3(256), 0, st, p, bytes / 16);
         return hipGetLastError();
     }
     const int64_t nrows = bytes / row_bytes;
     const int64_t per_wave = (rows + waves - 1) / waves;
     switch (row_bytes / 1024) {
-    case 1: hipLaunchKernelGGL((k_read_rows<1>), dim3((unsigned)waves), dim3(64), 0, st, p, nrows, per_wave); break;
-    case 2: hipLaunchKernelGGL((k_read_rows<2>), dim3((unsigned)waves), dim3(64), 0, st, p, nrows, per_wave); break;
-    case 3: hipLaunchKernelGGL((k_read_rows<3>), dim3((unsigned)waves), dim3(64), 0, st, p, nrows, per_wave); break;
-    case 4: hipLaunchKernelGGL((k_read_rows<4>), dim3((unsigned)waves), dim3(64), 0, st, p, nrows, per_wave); break;
-    case 8: hipLaunchKernelGGL((k_read_rows<8>), dim3((unsigned)waves), dim3(64), 0, st, p, nrows, per_wave); break;
+    case 1: return launch_rows<1>(p, nrows, per_wave, waves, st);
+    case 2: return launch_rows<2>(p, nrows, per_wave, waves, st);
+    case 3: return launch_rows<3>(p, nrows, per_wave, waves, st);
+    case 4: return launch_rows<4>(p, nrows, per_wave, waves, st);
+    case 8: return launch_rows<8>(p, nrows, per_wave, waves, st);
     default: return hipErrorInvalidValue;
     }
-    return hipGetLastError();
 }
 
 }  // namespace spdp
