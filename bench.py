@@ -9,13 +9,18 @@ duration) and the fp64 oracle timed on the host cores over a bounded sample
 of documents.
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME|IDX]
-                       [--assoc S [--assoc-eps E]]
+                       [--assoc S [--assoc-eps E]] [--heldout S]
 
 --assoc S runs the model with word associations instead (sparse
 transformation matrices with S sources per word, from synth.associations)
 and reports the same line for it.  --async runs the thesis's asynchronous
 sweep (an ablation: live atomics, racy reads; --async-waves wavefronts, 0 for
-the library's default) instead of the snapshot sweep.
+the library's default) instead of the snapshot sweep.  --heldout S times the
+held-out fold-in instead (P = I): the last 10 % of each group's documents are
+held out, the rest trained for the warm-up sweeps, and the line reports test
+tokens folded in per second of one fold-in sweep, taken as the difference
+between an S-sweep and a 1-sweep held-out call (their uploads and host sums
+cancel).
 """
 from __future__ import annotations
 
@@ -53,6 +58,13 @@ def assoc_bytes_per_token(K: int, wide: bool, mean_sources: float, Sp: int) -> f
     average), the token stream (row index and state in, state out) and the
     row's source record (Sp source words and Sp fp32 p)."""
     return 4 * K + (4 if wide else 2) * K * mean_sources + 12 + 8 * Sp
+
+
+def foldin_bytes_per_token(K: int) -> int:
+    """Bytes one fold-in sweep must move per test token with P = I: the K-cell
+    packed count row of (group, word), the word's K-entry int32 shadow-base
+    row, and the token stream (row index and topic in, topic out)."""
+    return 8 * K + 12
 
 
 def async_bytes_per_token(K: int) -> int:
@@ -176,6 +188,103 @@ def read_probe(gib: int = 4, row_bytes: int = 2048, waves: int = 4096):
     return out
 
 
+def copy_probe(mib: int):
+    """A plain device copy of mib MiB: the known bytes that scale the HBM
+    counters of the other kernels."""
+    if mib <= 0:
+        return
+    import torch
+    nbytes = mib << 20
+    src = torch.ones(nbytes // 4, dtype=torch.int32, device="cuda")
+    dst = torch.empty_like(src)
+    torch.cuda.synchronize()
+    dst.copy_(src)
+    torch.cuda.synchronize()
+    log(f"[bench] copy probe: {nbytes} bytes read + {nbytes} bytes written")
+    del src, dst
+
+
+def heldout_bench(args, wl, cp):
+    """--heldout S: fold-in sweeps of the test documents against the trained state."""
+    import torch
+
+    import synth
+    from paper_1510_06549_amd import spdp as sp
+
+    S = args.heldout
+    if S < 2:
+        print("bench.py: --heldout needs at least 2 fold-in sweeps", file=sys.stderr)
+        sys.exit(2)
+    tr, te = synth.split_heldout(cp, 0.1)
+    log(f"[bench] held out: train {tr.n_tokens} tokens, test {te.n_tokens} tokens in "
+        f"{te.n_docs} documents")
+    s = sp.Sampler(tr.words, tr.doc_off, tr.doc_group, tr.n_groups, wl.vocab, wl.K, wl.alpha,
+                   wl.a, wl.b, wl.gamma, init_seed=args.seed,
+                   hip_stream=torch.cuda.current_stream().cuda_stream)
+    copy_probe(args.copy_probe_mib)
+    seed = 1000 + args.seed
+    for w in range(max(args.warmup, 1)):
+        s.sweep(w, seed)
+    s.heldout(te.words, te.doc_off, te.doc_group, 1, seed)
+    torch.cuda.synchronize()
+    log(f"[bench] {max(args.warmup, 1)} training sweep(s) and a warm-up fold-in done")
+    t_one = t_many = 0.0
+    ppl = None
+    for k in range(args.steps):
+        for n, acc in ((1, "one"), (S, "many")):
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            ppl, _, _ = s.heldout(te.words, te.doc_off, te.doc_group, n, seed + k)
+            torch.cuda.synchronize()
+            dt = time.perf_counter() - t0
+            if acc == "one":
+                t_one += dt
+            else:
+                t_many += dt
+        log(f"[bench] step {k}: held-out calls of 1 and {S} sweeps done, perplexity {ppl:.1f}")
+    s.close()
+    per_sweep = (t_many - t_one) / args.steps / (S - 1)
+    T = te.n_tokens
+    bpt = foldin_bytes_per_token(wl.K)
+    achieved = T * bpt / per_sweep / 1e9
+    out = {
+        "metric": "held-out test tokens folded in/sec per fold-in sweep (1 GPU) + % of HBM roofline",
+        "value": round(T / per_sweep, 1),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(per_sweep * 1000.0, 3),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f64",
+        "data": "synthetic",
+        "config": {
+            "workload": f"{wl.name}-heldout",
+            "train_tokens": tr.n_tokens,
+            "test_tokens": T,
+            "test_docs": te.n_docs,
+            "foldin_sweeps": S,
+            "topics": wl.K,
+        },
+        "perplexity": round(ppl, 2),
+        "roofline": {
+            "bound": "hbm",
+            "kernel": "k_foldin",
+            "achieved": round(achieved, 1),
+            "peak": HBM_PEAK_GBS,
+            "unit": "GB/s",
+            "frac": round(achieved / HBM_PEAK_GBS, 4),
+            "traffic": None,
+            "bytes_per_token": bpt,
+            "ms_per_foldin_sweep": round(per_sweep * 1000.0, 3),
+        },
+        "cpu_baseline": None,
+    }
+    print(json.dumps(out), flush=True)
+
+
 def host_cpu() -> str:
     """The host CPU's model name and logical CPU count."""
     name = "unknown"
@@ -212,6 +321,8 @@ def main():
                     help="wavefronts of the asynchronous sweep (0: library default)")
     ap.add_argument("--async-live-totals", action="store_true",
                     help="asynchronous sweep with the sums N, T, B_k updated live")
+    ap.add_argument("--heldout", type=int, default=0,
+                    help="time the held-out fold-in with this many sweeps instead (P = I)")
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -234,6 +345,13 @@ def main():
     log(f"[bench] workload {wl.name}: {cp.n_tokens} tokens, {cp.n_docs} docs, generated in "
         f"{time.time() - t0:.1f}s")
 
+    if args.heldout:
+        if args.assoc or args.async_sweep:
+            print("bench.py: --heldout times the P = I fold-in only", file=sys.stderr)
+            sys.exit(2)
+        heldout_bench(args, wl, cp)
+        return
+
     assoc = None
     if args.assoc > 0:
         t0 = time.time()
@@ -250,15 +368,7 @@ def main():
     info = s.info
     log(f"[bench] state created in {time.time() - t0:.1f}s: {info}")
 
-    if args.copy_probe_mib > 0:
-        nbytes = args.copy_probe_mib << 20
-        src = torch.ones(nbytes // 4, dtype=torch.int32, device="cuda")
-        dst = torch.empty_like(src)
-        torch.cuda.synchronize()
-        dst.copy_(src)
-        torch.cuda.synchronize()
-        log(f"[bench] copy probe: {nbytes} bytes read + {nbytes} bytes written")
-        del src, dst
+    copy_probe(args.copy_probe_mib)
 
     if args.async_sweep and assoc is not None:
         print("bench.py: the asynchronous sweep is built for P = I only", file=sys.stderr)

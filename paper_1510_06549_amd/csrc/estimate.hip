@@ -24,7 +24,7 @@
 // With word associations (non-identity P^g) phi0 is over source words and the
 // base of group g's Pitman-Yor process is P^g phi0_k:
 //   phi[g][w][k] = (n - a t + (b + a T_gk) sum_v p_{g,w,v} phi0[v][k]) / (b + N_gk).
-#include "spdp_internal.hpp"
+#include "sampler_common.hpp"
 
 namespace spdp {
 
@@ -163,7 +163,76 @@ __device__ __forceinline__ void phi_row(const FoldArgs &A, int64_t q, int32_t w,
     }
 }
 
+// With P = I: this lane's slices of a test token's packed count row and of
+// its int32 shadow-base row, loaded whole (padding chunks re-read the row
+// start; their topics weigh nothing), and the group estimate from them, the
+// same expression as phi_row.
 template <int KPL>
+struct FoldRows {
+    int32_t n[KPL], b[KPL];
+};
+
+template <int KPL>
+__device__ __forceinline__ void load_fold_rows(const FoldArgs &A, int32_t q, int32_t g,
+                                               int32_t kbase, FoldRows<KPL> &R)
+{
+    load_row<KPL>(R.n, A.nt + (int64_t)q * A.Kp, kbase, A.Kp);
+    load_row<KPL>(R.b, A.B + (int64_t)(q - g * A.V) * A.Kp, kbase, A.Kp);
+}
+
+template <int KPL>
+__device__ __forceinline__ void phi_from_rows(const FoldArgs &A, const FoldRows<KPL> &R,
+                                              int32_t kbase, const double *inv, const double *base,
+                                              double (&ph)[KPL])
+{
+#pragma unroll
+    for (int j = 0; j < KPL; ++j) {
+        const int32_t k = kbase + j;
+        const double n = (double)(R.n[j] & kCountMax), t = (double)(R.n[j] >> kCountBits);
+        const double bw = A.gamma + (double)R.b[j];
+        ph[j] = (k < A.K) ? (n - A.a * t) * inv[k] + bw * base[k] : 0.0;
+    }
+}
+
+// The group estimates of tokens 0 .. nc - 1 of a chunk (row indices in the
+// lanes of gw_c), in order, handed to f(x, ph).  With P = I the rows of token
+// x + 1 are requested before token x is evaluated (two register sets
+// alternate); with word associations phi_row reads each token's rows.
+template <int KPL, bool ASSOC, typename F>
+__device__ __forceinline__ void for_chunk_phi(const FoldArgs &A, int32_t g, int32_t kbase,
+                                              int32_t gw_c, int32_t nc, const double *inv,
+                                              const double *base, F &&f)
+{
+    if constexpr (ASSOC) {
+        for (int32_t x = 0; x < nc; ++x) {
+            const int32_t q = __builtin_amdgcn_readlane(gw_c, x);
+            double ph[KPL];
+            phi_row<KPL>(A, q, q - g * A.V, kbase, inv, base, ph);
+            f(x, ph);
+        }
+    } else {
+        FoldRows<KPL> ra, rb;
+        load_fold_rows<KPL>(A, __builtin_amdgcn_readlane(gw_c, 0), g, kbase, ra);
+        for (int32_t x = 0; x < nc; x += 2) {
+            const int32_t x1 = x + 1 < nc ? x + 1 : x;
+            load_fold_rows<KPL>(A, __builtin_amdgcn_readlane(gw_c, x1), g, kbase, rb);
+            {
+                double ph[KPL];
+                phi_from_rows<KPL>(A, ra, kbase, inv, base, ph);
+                f(x, ph);
+            }
+            if (x + 1 < nc) {
+                const int32_t x2 = x + 2 < nc ? x + 2 : x + 1;
+                load_fold_rows<KPL>(A, __builtin_amdgcn_readlane(gw_c, x2), g, kbase, ra);
+                double ph[KPL];
+                phi_from_rows<KPL>(A, rb, kbase, inv, base, ph);
+                f(x + 1, ph);
+            }
+        }
+    }
+}
+
+template <int KPL, bool ASSOC>
 __global__ void __launch_bounds__(64) k_foldin(FoldArgs A)
 {
     // document counts and the group's per-topic factors 1/(b + N) and
@@ -206,12 +275,10 @@ __global__ void __launch_bounds__(64) k_foldin(FoldArgs A)
             const bool mine = lane < nc;
             const int32_t gw_c = mine ? A.gw[cb + lane] : 0;
             int32_t z_c = mine ? A.z[cb + lane] : 0;
-            for (int32_t x = 0; x < nc; ++x) {
+            for_chunk_phi<KPL, ASSOC>(A, g, kbase, gw_c, nc, inv, base, [&](int32_t x,
+                                                                            const double(&ph)[KPL]) {
                 const int64_t i = cb + x;
-                const int32_t q = __builtin_amdgcn_readlane(gw_c, x);
                 const int32_t k0 = __builtin_amdgcn_readlane(z_c, x);
-                double ph[KPL];
-                phi_row<KPL>(A, q, q - g * A.V, kbase, inv, base, ph);
                 double pre[KPL];
                 double acc = 0.0;
 #pragma unroll
@@ -248,7 +315,7 @@ __global__ void __launch_bounds__(64) k_foldin(FoldArgs A)
                     c[k0] -= 1;
                     c[k1] += 1;
                 }
-            }
+            });
             if (mine) A.z[cb + lane] = z_c;
         }
     }
@@ -264,15 +331,13 @@ __global__ void __launch_bounds__(64) k_foldin(FoldArgs A)
     for (int64_t cb = beg; cb < end; cb += 64) {
         const int32_t nc = (int32_t)min((int64_t)64, end - cb);
         const int32_t gw_c = (lane < nc) ? A.gw[cb + lane] : 0;
-        for (int32_t x = 0; x < nc; ++x) {
-            const int32_t q = __builtin_amdgcn_readlane(gw_c, x);
-            double ph[KPL];
-            phi_row<KPL>(A, q, q - g * A.V, kbase, inv, base, ph);
-            double p = 0.0;
+        for_chunk_phi<KPL, ASSOC>(A, g, kbase, gw_c, nc, inv, base,
+                                  [&](int32_t, const double(&ph)[KPL]) {
+                                      double p = 0.0;
 #pragma unroll
-            for (int j = 0; j < KPL; ++j) p += ph[j] * th[j];
-            ll += log(wave_sum(p));
-        }
+                                      for (int j = 0; j < KPL; ++j) p += ph[j] * th[j];
+                                      ll += log(wave_sum(p));
+                                  });
     }
     if (lane == 0) A.ll_doc[d] = ll;
 }
@@ -280,7 +345,10 @@ __global__ void __launch_bounds__(64) k_foldin(FoldArgs A)
 template <int KPL>
 hipError_t launch_fold(const FoldArgs &A, hipStream_t st)
 {
-    hipLaunchKernelGGL(k_foldin<KPL>, dim3((unsigned)A.D), dim3(64), 0, st, A);
+    if (A.Sp > 0)
+        hipLaunchKernelGGL((k_foldin<KPL, true>), dim3((unsigned)A.D), dim3(64), 0, st, A);
+    else
+        hipLaunchKernelGGL((k_foldin<KPL, false>), dim3((unsigned)A.D), dim3(64), 0, st, A);
     return hipGetLastError();
 }
 
