@@ -132,56 +132,43 @@ __device__ __forceinline__ double wave_sum(double x)
     return x;
 }
 
-// This lane's KPL values of the group estimate for row q (topics kbase..);
-// with word associations the base weight gamma + B sums over the row's
-// sources, p-weighted.
-template <int KPL>
-__device__ __forceinline__ void phi_row(const FoldArgs &A, int64_t q, int32_t w, int32_t kbase,
-                                        const double *inv, const double *base, double (&ph)[KPL])
+// This lane's slices of the rows a test token's group estimate reads, loaded
+// whole (padding chunks re-read the row start; their topics weigh nothing):
+// the packed count row of q = g V + w and, with P = I (SP = 0), the int32
+// shadow-base row of w; with word associations (SP sources per row) the
+// shadow-base rows of the row's sources and their p (a padding slot repeats
+// the first source with p = 0).
+template <int KPL, int SP>
+struct FoldRows {
+    static constexpr int NB = SP > 0 ? SP : 1;
+    int32_t n[KPL];
+    int32_t b[NB][KPL];
+    double p[NB];
+};
+
+template <int KPL, int SP>
+__device__ __forceinline__ void load_fold_rows(const FoldArgs &A, int32_t q, int32_t g,
+                                               int32_t kbase, FoldRows<KPL, SP> &R)
 {
+    load_row<KPL>(R.n, A.nt + (int64_t)q * A.Kp, kbase, A.Kp);
+    if constexpr (SP == 0) {
+        load_row<KPL>(R.b[0], A.B + (int64_t)(q - g * A.V) * A.Kp, kbase, A.Kp);
+    } else {
 #pragma unroll
-    for (int j = 0; j < KPL; ++j) {
-        const int32_t k = kbase + j;
-        ph[j] = 0.0;
-        if (k < A.K) {
-            const int32_t x = A.nt[q * A.Kp + k];
-            const double n = (double)(x & kCountMax), t = (double)(x >> kCountBits);
-            double bw;
-            if (A.Sp == 0) {
-                bw = A.gamma + (double)A.B[(int64_t)w * A.Kp + k];
-            } else {
-                bw = 0.0;
-                for (int32_t s = 0; s < A.Sp; ++s) {
-                    const double pv = A.p64[q * A.Sp + s];
-                    if (pv > 0.0)
-                        bw += pv * (A.gamma +
-                                    (double)A.B[(int64_t)A.srcrec[q * 2 * A.Sp + s] * A.Kp + k]);
-                }
-            }
-            ph[j] = (n - A.a * t) * inv[k] + bw * base[k];
+        for (int s = 0; s < SP; ++s) {
+            const int32_t v = A.srcrec[(int64_t)q * 2 * SP + s];
+            R.p[s] = A.p64[(int64_t)q * SP + s];
+            load_row<KPL>(R.b[s], A.B + (int64_t)v * A.Kp, kbase, A.Kp);
         }
     }
 }
 
-// With P = I: this lane's slices of a test token's packed count row and of
-// its int32 shadow-base row, loaded whole (padding chunks re-read the row
-// start; their topics weigh nothing), and the group estimate from them, the
-// same expression as phi_row.
-template <int KPL>
-struct FoldRows {
-    int32_t n[KPL], b[KPL];
-};
-
-template <int KPL>
-__device__ __forceinline__ void load_fold_rows(const FoldArgs &A, int32_t q, int32_t g,
-                                               int32_t kbase, FoldRows<KPL> &R)
-{
-    load_row<KPL>(R.n, A.nt + (int64_t)q * A.Kp, kbase, A.Kp);
-    load_row<KPL>(R.b, A.B + (int64_t)(q - g * A.V) * A.Kp, kbase, A.Kp);
-}
-
-template <int KPL>
-__device__ __forceinline__ void phi_from_rows(const FoldArgs &A, const FoldRows<KPL> &R,
+// The group estimate of this lane's topics: (n - a t)/(b + N) plus the base
+// weight times (b + a T)/(b + N)/(V gamma + B_k), the base weight being
+// gamma + B[w][k], or with word associations the sum over the sources, in
+// slot order, of p (gamma + B[v][k]) for p > 0.
+template <int KPL, int SP>
+__device__ __forceinline__ void phi_from_rows(const FoldArgs &A, const FoldRows<KPL, SP> &R,
                                               int32_t kbase, const double *inv, const double *base,
                                               double (&ph)[KPL])
 {
@@ -189,50 +176,60 @@ __device__ __forceinline__ void phi_from_rows(const FoldArgs &A, const FoldRows<
     for (int j = 0; j < KPL; ++j) {
         const int32_t k = kbase + j;
         const double n = (double)(R.n[j] & kCountMax), t = (double)(R.n[j] >> kCountBits);
-        const double bw = A.gamma + (double)R.b[j];
+        double bw;
+        if constexpr (SP == 0) {
+            bw = A.gamma + (double)R.b[0][j];
+        } else {
+            bw = 0.0;
+#pragma unroll
+            for (int s = 0; s < SP; ++s)
+                if (R.p[s] > 0.0) bw += R.p[s] * (A.gamma + (double)R.b[s][j]);
+        }
         ph[j] = (k < A.K) ? (n - A.a * t) * inv[k] + bw * base[k] : 0.0;
     }
 }
 
 // The group estimates of tokens 0 .. nc - 1 of a chunk (row indices in the
-// lanes of gw_c), in order, handed to f(x, ph).  With P = I the rows of token
-// x + 1 are requested before token x is evaluated (two register sets
-// alternate); with word associations phi_row reads each token's rows.
-template <int KPL, bool ASSOC, typename F>
+// lanes of gw_c), in order, handed to f(x, ph).  Where two register sets of
+// rows fit, the rows of token x + 1 are requested before token x is
+// evaluated; otherwise each token's rows are loaded together, then used.
+template <int KPL, int SP, typename F>
 __device__ __forceinline__ void for_chunk_phi(const FoldArgs &A, int32_t g, int32_t kbase,
                                               int32_t gw_c, int32_t nc, const double *inv,
                                               const double *base, F &&f)
 {
-    if constexpr (ASSOC) {
+    constexpr int kRows = SP > 0 ? SP + 1 : 2;
+    if constexpr (KPL * kRows > 48) {
         for (int32_t x = 0; x < nc; ++x) {
-            const int32_t q = __builtin_amdgcn_readlane(gw_c, x);
+            FoldRows<KPL, SP> r;
+            load_fold_rows<KPL, SP>(A, __builtin_amdgcn_readlane(gw_c, x), g, kbase, r);
             double ph[KPL];
-            phi_row<KPL>(A, q, q - g * A.V, kbase, inv, base, ph);
+            phi_from_rows<KPL, SP>(A, r, kbase, inv, base, ph);
             f(x, ph);
         }
     } else {
-        FoldRows<KPL> ra, rb;
-        load_fold_rows<KPL>(A, __builtin_amdgcn_readlane(gw_c, 0), g, kbase, ra);
+        FoldRows<KPL, SP> ra, rb;
+        load_fold_rows<KPL, SP>(A, __builtin_amdgcn_readlane(gw_c, 0), g, kbase, ra);
         for (int32_t x = 0; x < nc; x += 2) {
             const int32_t x1 = x + 1 < nc ? x + 1 : x;
-            load_fold_rows<KPL>(A, __builtin_amdgcn_readlane(gw_c, x1), g, kbase, rb);
+            load_fold_rows<KPL, SP>(A, __builtin_amdgcn_readlane(gw_c, x1), g, kbase, rb);
             {
                 double ph[KPL];
-                phi_from_rows<KPL>(A, ra, kbase, inv, base, ph);
+                phi_from_rows<KPL, SP>(A, ra, kbase, inv, base, ph);
                 f(x, ph);
             }
             if (x + 1 < nc) {
                 const int32_t x2 = x + 2 < nc ? x + 2 : x + 1;
-                load_fold_rows<KPL>(A, __builtin_amdgcn_readlane(gw_c, x2), g, kbase, ra);
+                load_fold_rows<KPL, SP>(A, __builtin_amdgcn_readlane(gw_c, x2), g, kbase, ra);
                 double ph[KPL];
-                phi_from_rows<KPL>(A, rb, kbase, inv, base, ph);
+                phi_from_rows<KPL, SP>(A, rb, kbase, inv, base, ph);
                 f(x + 1, ph);
             }
         }
     }
 }
 
-template <int KPL, bool ASSOC>
+template <int KPL, int SP>
 __global__ void __launch_bounds__(64) k_foldin(FoldArgs A)
 {
     // document counts and the group's per-topic factors 1/(b + N) and
@@ -275,7 +272,7 @@ __global__ void __launch_bounds__(64) k_foldin(FoldArgs A)
             const bool mine = lane < nc;
             const int32_t gw_c = mine ? A.gw[cb + lane] : 0;
             int32_t z_c = mine ? A.z[cb + lane] : 0;
-            for_chunk_phi<KPL, ASSOC>(A, g, kbase, gw_c, nc, inv, base, [&](int32_t x,
+            for_chunk_phi<KPL, SP>(A, g, kbase, gw_c, nc, inv, base, [&](int32_t x,
                                                                             const double(&ph)[KPL]) {
                 const int64_t i = cb + x;
                 const int32_t k0 = __builtin_amdgcn_readlane(z_c, x);
@@ -331,7 +328,7 @@ __global__ void __launch_bounds__(64) k_foldin(FoldArgs A)
     for (int64_t cb = beg; cb < end; cb += 64) {
         const int32_t nc = (int32_t)min((int64_t)64, end - cb);
         const int32_t gw_c = (lane < nc) ? A.gw[cb + lane] : 0;
-        for_chunk_phi<KPL, ASSOC>(A, g, kbase, gw_c, nc, inv, base,
+        for_chunk_phi<KPL, SP>(A, g, kbase, gw_c, nc, inv, base,
                                   [&](int32_t, const double(&ph)[KPL]) {
                                       double p = 0.0;
 #pragma unroll
@@ -345,10 +342,15 @@ __global__ void __launch_bounds__(64) k_foldin(FoldArgs A)
 template <int KPL>
 hipError_t launch_fold(const FoldArgs &A, hipStream_t st)
 {
-    if (A.Sp > 0)
-        hipLaunchKernelGGL((k_foldin<KPL, true>), dim3((unsigned)A.D), dim3(64), 0, st, A);
-    else
-        hipLaunchKernelGGL((k_foldin<KPL, false>), dim3((unsigned)A.D), dim3(64), 0, st, A);
+    const dim3 grid((unsigned)A.D);
+    switch (A.Sp) {
+    case 0: hipLaunchKernelGGL((k_foldin<KPL, 0>), grid, dim3(64), 0, st, A); break;
+    case 1: hipLaunchKernelGGL((k_foldin<KPL, 1>), grid, dim3(64), 0, st, A); break;
+    case 2: hipLaunchKernelGGL((k_foldin<KPL, 2>), grid, dim3(64), 0, st, A); break;
+    case 4: hipLaunchKernelGGL((k_foldin<KPL, 4>), grid, dim3(64), 0, st, A); break;
+    case 8: hipLaunchKernelGGL((k_foldin<KPL, 8>), grid, dim3(64), 0, st, A); break;
+    default: return hipErrorInvalidValue;
+    }
     return hipGetLastError();
 }
 
