@@ -8,7 +8,8 @@ transformation matrices P^g) against the fp64 oracle, through the C ABI.
   1e-5, samples identical on >= 99.99% of tokens with every first mismatch at a
   CDF boundary, update and repair bit-exact); source lists of 1..8 entries,
   K at the lane-layout boundaries, the 32-bit shadow-base path.
-* Joint to 1e-6, estimates to fp64 rounding, held-out fold-in topics identical.
+* Joint to 1e-6, estimates to fp64 rounding, held-out fold-in topics identical
+  (1, 2, 4 and 8 source slots; 1 to 12 topics per lane).
 * Checkpoint/resume with slots; invalid slots rejected.
 Each test prints the case it runs before touching the GPU.
 """
@@ -216,6 +217,32 @@ def test_heldout_matches_oracle(idx):
     ppl, tot, zt = s.heldout(test.words, test.doc_off, test.doc_group, 10, 6)
     agree = float(np.mean(zt == zt_o)) if zt.size else 1.0
     say(f"  perplexity {ppl}, oracle total {tot_o}, library total {tot}, agreement {agree}")
+    assert agree >= parity.MATCH_FRAC
+    assert abs(tot - tot_o) <= 1e-9 * abs(tot_o)
+    s.close()
+
+
+@pytest.mark.parametrize("K,S", [(10, 1), (130, 2), (500, 4), (700, 4), (200, 8), (500, 8)])
+def test_heldout_source_and_topic_layouts(K, S):
+    """The fold-in's source-count and lane-layout instances (1, 2, 4 and 8
+    source slots; 1 to 12 topics per lane), with and without the one-token
+    prefetch (four sources past K = 512 and eight past K = 256 load each
+    token's rows, then use them)."""
+    w0 = synth.workload(0)
+    say(f"association held-out fold-in, K = {K}, {S} sources per word")
+    cp = synth.generate(w0, 3)
+    train, test = synth.split_heldout(cp, 0.1)
+    assoc = synth.associations(cp.n_groups, cp.vocab, S, 0.3 if S > 1 else 0.0, 8)
+    s, m = parity.make_pair(train, W(K, w0.alpha, w0.a, w0.b, w0.gamma), assoc=assoc)
+    for sw in range(3):
+        s.sweep(sw, 29)
+    st = parity.state_of(s, m)
+    c = m.rebuild(*st)
+    _, _, pg_o = m.estimates(st[0], c)
+    tot_o, zt_o, _ = m.heldout(pg_o, test.words, test.doc_off, test.doc_group, 6, 11)
+    ppl, tot, zt = s.heldout(test.words, test.doc_off, test.doc_group, 6, 11)
+    agree = float(np.mean(zt == zt_o))
+    say(f"  {test.n_tokens} test tokens, agreement {agree}, totals {tot} / {tot_o}")
     assert agree >= parity.MATCH_FRAC
     assert abs(tot - tot_o) <= 1e-9 * abs(tot_o)
     s.close()
