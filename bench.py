@@ -214,9 +214,6 @@ def heldout_bench(args, wl, cp):
     from paper_1510_06549_amd import spdp as sp
 
     S = args.heldout
-    if S < 2:
-        print("bench.py: --heldout needs at least 2 fold-in sweeps", file=sys.stderr)
-        sys.exit(2)
     tr, te = synth.split_heldout(cp, 0.1)
     log(f"[bench] held out: train {tr.n_tokens} tokens, test {te.n_tokens} tokens in "
         f"{te.n_docs} documents")
@@ -345,6 +342,13 @@ def main():
         print("bench.py measures one GPU: the multi-GPU (group-sharded) sweep is not built; "
               "run with --gpus 1", file=sys.stderr)
         sys.exit(2)
+    if args.heldout and (args.heldout < 2 or args.async_sweep):
+        print("bench.py: --heldout needs at least 2 fold-in sweeps and times the fold-in, "
+              "not a sweep variant", file=sys.stderr)
+        sys.exit(2)
+    if args.async_sweep and args.assoc > 0:
+        print("bench.py: the asynchronous sweep is built for P = I only", file=sys.stderr)
+        sys.exit(2)
 
     import numpy as np
     import torch
@@ -362,9 +366,6 @@ def main():
         f"{time.time() - t0:.1f}s")
 
     if args.heldout:
-        if args.async_sweep:
-            print("bench.py: --heldout times the fold-in, not a sweep variant", file=sys.stderr)
-            sys.exit(2)
         heldout_bench(args, wl, cp)
         return
 
@@ -385,10 +386,6 @@ def main():
     log(f"[bench] state created in {time.time() - t0:.1f}s: {info}")
 
     copy_probe(args.copy_probe_mib)
-
-    if args.async_sweep and assoc is not None:
-        print("bench.py: the asynchronous sweep is built for P = I only", file=sys.stderr)
-        sys.exit(2)
 
     def one_sweep(k):
         if args.async_sweep:
