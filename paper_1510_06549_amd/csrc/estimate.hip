@@ -285,15 +285,9 @@ __global__ void __launch_bounds__(64) k_foldin(FoldArgs A)
                     acc += (k < A.K) ? cw * ph[j] : 0.0;
                     pre[j] = acc;
                 }
-                double incl = acc;
-#pragma unroll
-                for (int o = 1; o < 64; o <<= 1) {
-                    const double y = __shfl_up(incl, o);
-                    if (lane >= o) incl += y;
-                }
-                double excl = __shfl_up(incl, 1);
-                if (lane == 0) excl = 0.0;
-                const double total = __shfl(incl, 63);
+                const double incl = wave_inclusive_sum64(acc);
+                const double excl = wave_shift_right64(incl);
+                const double total = readlane64(incl, 63);
                 const uint32_t xr = philox_x0(A.seed, (uint64_t)i, (uint32_t)s, kPurposeFoldin);
                 const double target = (double)(xr >> 8) * (1.0 / 16777216.0) * total;
                 const double rel = target - excl;
