@@ -125,11 +125,10 @@ struct FoldArgs {
     double alpha, a, b, gamma, Vgamma;
 };
 
+// sum over the wave's 64 lanes (the last lane's inclusive prefix sum)
 __device__ __forceinline__ double wave_sum(double x)
 {
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) x += __shfl_xor(x, o);
-    return x;
+    return readlane64(wave_inclusive_sum64(x), 63);
 }
 
 // This lane's slices of the rows a test token's group estimate reads, loaded
