@@ -21,7 +21,9 @@ import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRC = os.path.join(_HERE, "oracle.c")
-_LIB_PATH = os.path.join(_HERE, "liboracle.so")
+# SPDP_ORACLE_LIB names another build of oracle.c to load instead (the
+# sanitizer test runs the pins against an AddressSanitizer/UBSan build)
+_LIB_PATH = os.environ.get("SPDP_ORACLE_LIB") or os.path.join(_HERE, "liboracle.so")
 
 PURPOSE_SAMPLE = 0
 PURPOSE_INIT = 1
@@ -29,6 +31,8 @@ PURPOSE_INIT = 1
 
 def build(force: bool = True) -> str:
     """Compile oracle.c into liboracle.so (gcc, -O2, OpenMP)."""
+    if os.environ.get("SPDP_ORACLE_LIB"):
+        return _LIB_PATH  # a build made elsewhere (see build_sanitized)
     if force or not os.path.exists(_LIB_PATH):
         tmp = _LIB_PATH + ".tmp"
         subprocess.check_call(
@@ -36,6 +40,19 @@ def build(force: bool = True) -> str:
         )
         os.replace(tmp, _LIB_PATH)
     return _LIB_PATH
+
+
+SANITIZE_FLAGS = ["-fsanitize=address,undefined", "-fno-sanitize-recover=all",
+                  "-fno-omit-frame-pointer", "-g", "-O1"]
+
+
+def build_sanitized(path: str) -> str:
+    """Compile oracle.c with AddressSanitizer and UndefinedBehaviorSanitizer
+    (host code only) into `path`; load it by setting SPDP_ORACLE_LIB, with
+    the ASan runtime preloaded into the interpreter."""
+    subprocess.check_call(["gcc", *SANITIZE_FLAGS, "-fopenmp", "-fPIC", "-shared", _SRC, "-lm",
+                           "-o", path])
+    return path
 
 
 class _Model(C.Structure):
@@ -76,70 +93,94 @@ def lib():
     if _lib is None:
         if not os.path.exists(_LIB_PATH):
             build(force=True)
-        L = C.CDLL(_LIB_PATH)
-        vp, i32, i64, u32, u64, dbl = C.c_void_p, C.c_int32, C.c_int64, C.c_uint32, C.c_uint64, C.c_double
-        L.or_philox4x32_10.argtypes = [vp, vp, vp]
-        L.or_philox4x32_10.restype = None
-        L.or_philox_word0.argtypes = [u64, i64, u32, u32]
-        L.or_philox_word0.restype = u32
-        L.or_uniform.argtypes = [u64, i64, u32]
-        L.or_uniform.restype = dbl
-        L.or_stirling_log_table.argtypes = [i32, dbl, vp]
-        L.or_stirling_log_table.restype = C.c_int
-        L.or_init.argtypes = [vp, u64, vp, vp]
-        L.or_init.restype = None
-        L.or_rebuild.argtypes = [vp, vp, vp, vp]
-        L.or_rebuild.restype = None
-        L.or_repair.argtypes = [vp, vp, vp, vp]
-        L.or_repair.restype = i64
-        L.or_token_weights.argtypes = [vp, vp, vp, i32, i32, i32, i32, vp]
-        L.or_token_weights.restype = C.c_int
-        L.or_sample_docs.argtypes = [vp, vp, vp, vp, u32, u64, i32, i32, vp, vp, vp, i64, i64]
-        L.or_sample_docs.restype = i64
-        L.or_sweep.argtypes = [vp, vp, vp, vp, u32, u64, C.c_int, vp]
-        L.or_sweep.restype = C.c_int
-        L.or_loglik.argtypes = [vp, vp, vp, vp]
-        L.or_loglik.restype = dbl
-        L.or_max_group_word_count.argtypes = [vp]
-        L.or_max_group_word_count.restype = i32
-        L.or_chain_histogram.argtypes = [vp, vp, vp, vp, u32, i64, u64, C.c_int, vp, i64]
-        L.or_chain_histogram.restype = C.c_int
-        L.or_interleaved_order.argtypes = [vp, vp]
-        L.or_interleaved_order.restype = None
-        L.or_sweep_ordered.argtypes = [vp, vp, vp, vp, u32, u64, vp, C.c_int, vp]
-        L.or_sweep_ordered.restype = C.c_int
-        L.or_chain_histogram_ordered.argtypes = [vp, vp, vp, vp, u32, i64, u64, vp, vp, i64]
-        L.or_chain_histogram_ordered.restype = C.c_int
-        L.or_num_threads.argtypes = []
-        L.or_num_threads.restype = C.c_int
-        L.or_set_num_threads.argtypes = [C.c_int]
-        L.or_set_num_threads.restype = C.c_int
-        L.or_estimates.argtypes = [vp, vp, vp, vp, vp, vp]
-        L.or_estimates.restype = None
-        L.or_heldout.argtypes = [vp, vp, i32, vp, vp, vp, i32, u64, vp, vp]
-        L.or_heldout.restype = dbl
-        L.or_head_source.argtypes = [vp, vp, i32, i32]
-        L.or_head_source.restype = i32
-        L.or_rebuild_assoc.argtypes = [vp, vp, vp, vp, vp, vp]
-        L.or_rebuild_assoc.restype = None
-        L.or_repair_assoc.argtypes = [vp, vp, vp, vp, vp, vp]
-        L.or_repair_assoc.restype = i64
-        L.or_token_weights_assoc.argtypes = [vp, vp, vp, vp, i32, i32, i32, i32, i32, vp]
-        L.or_token_weights_assoc.restype = C.c_int
-        L.or_sample_docs_assoc.argtypes = [vp, vp, vp, vp, vp, vp, u32, u64, i32, i32, vp, vp,
-                                           vp, i64, i64]
-        L.or_sample_docs_assoc.restype = i64
-        L.or_sweep_assoc.argtypes = [vp, vp, vp, vp, vp, vp, u32, u64, C.c_int, vp]
-        L.or_sweep_assoc.restype = C.c_int
-        L.or_loglik_assoc.argtypes = [vp, vp, vp, vp, vp, vp]
-        L.or_loglik_assoc.restype = dbl
-        L.or_estimates_assoc.argtypes = [vp, vp, vp, vp, vp, vp, vp]
-        L.or_estimates_assoc.restype = None
-        L.or_chain_histogram_assoc.argtypes = [vp, vp, vp, vp, vp, vp, u32, i64, u64, C.c_int,
-                                               vp, i64]
-        L.or_chain_histogram_assoc.restype = C.c_int
-        _lib = L
+        _lib = _bind(C.CDLL(_LIB_PATH))
     return _lib
+
+
+class swap_library:
+    """Context manager: every call of this module goes to the library at
+    `path` (a variant of oracle.c built by a test, e.g. with a planted
+    mistake) until the block ends."""
+
+    def __init__(self, path: str):
+        self.path = path
+
+    def __enter__(self):
+        global _lib
+        self._saved = lib()
+        _lib = _bind(C.CDLL(self.path))
+        return _lib
+
+    def __exit__(self, *exc):
+        global _lib
+        _lib = self._saved
+        return False
+
+
+def _bind(L):
+    """Argument and return types of the library's entry points."""
+    vp, i32, i64, u32, u64, dbl = C.c_void_p, C.c_int32, C.c_int64, C.c_uint32, C.c_uint64, C.c_double
+    L.or_philox4x32_10.argtypes = [vp, vp, vp]
+    L.or_philox4x32_10.restype = None
+    L.or_philox_word0.argtypes = [u64, i64, u32, u32]
+    L.or_philox_word0.restype = u32
+    L.or_uniform.argtypes = [u64, i64, u32]
+    L.or_uniform.restype = dbl
+    L.or_stirling_log_table.argtypes = [i32, dbl, vp]
+    L.or_stirling_log_table.restype = C.c_int
+    L.or_init.argtypes = [vp, u64, vp, vp]
+    L.or_init.restype = None
+    L.or_rebuild.argtypes = [vp, vp, vp, vp]
+    L.or_rebuild.restype = None
+    L.or_repair.argtypes = [vp, vp, vp, vp]
+    L.or_repair.restype = i64
+    L.or_token_weights.argtypes = [vp, vp, vp, i32, i32, i32, i32, vp]
+    L.or_token_weights.restype = C.c_int
+    L.or_sample_docs.argtypes = [vp, vp, vp, vp, u32, u64, i32, i32, vp, vp, vp, i64, i64]
+    L.or_sample_docs.restype = i64
+    L.or_sweep.argtypes = [vp, vp, vp, vp, u32, u64, C.c_int, vp]
+    L.or_sweep.restype = C.c_int
+    L.or_loglik.argtypes = [vp, vp, vp, vp]
+    L.or_loglik.restype = dbl
+    L.or_max_group_word_count.argtypes = [vp]
+    L.or_max_group_word_count.restype = i32
+    L.or_chain_histogram.argtypes = [vp, vp, vp, vp, u32, i64, u64, C.c_int, vp, i64]
+    L.or_chain_histogram.restype = C.c_int
+    L.or_interleaved_order.argtypes = [vp, vp]
+    L.or_interleaved_order.restype = None
+    L.or_sweep_ordered.argtypes = [vp, vp, vp, vp, u32, u64, vp, C.c_int, vp]
+    L.or_sweep_ordered.restype = C.c_int
+    L.or_chain_histogram_ordered.argtypes = [vp, vp, vp, vp, u32, i64, u64, vp, vp, i64]
+    L.or_chain_histogram_ordered.restype = C.c_int
+    L.or_num_threads.argtypes = []
+    L.or_num_threads.restype = C.c_int
+    L.or_set_num_threads.argtypes = [C.c_int]
+    L.or_set_num_threads.restype = C.c_int
+    L.or_estimates.argtypes = [vp, vp, vp, vp, vp, vp]
+    L.or_estimates.restype = None
+    L.or_heldout.argtypes = [vp, vp, i32, vp, vp, vp, i32, u64, vp, vp]
+    L.or_heldout.restype = dbl
+    L.or_head_source.argtypes = [vp, vp, i32, i32]
+    L.or_head_source.restype = i32
+    L.or_rebuild_assoc.argtypes = [vp, vp, vp, vp, vp, vp]
+    L.or_rebuild_assoc.restype = None
+    L.or_repair_assoc.argtypes = [vp, vp, vp, vp, vp, vp]
+    L.or_repair_assoc.restype = i64
+    L.or_token_weights_assoc.argtypes = [vp, vp, vp, vp, i32, i32, i32, i32, i32, vp]
+    L.or_token_weights_assoc.restype = C.c_int
+    L.or_sample_docs_assoc.argtypes = [vp, vp, vp, vp, vp, vp, u32, u64, i32, i32, vp, vp,
+                                       vp, i64, i64]
+    L.or_sample_docs_assoc.restype = i64
+    L.or_sweep_assoc.argtypes = [vp, vp, vp, vp, vp, vp, u32, u64, C.c_int, vp]
+    L.or_sweep_assoc.restype = C.c_int
+    L.or_loglik_assoc.argtypes = [vp, vp, vp, vp, vp, vp]
+    L.or_loglik_assoc.restype = dbl
+    L.or_estimates_assoc.argtypes = [vp, vp, vp, vp, vp, vp, vp]
+    L.or_estimates_assoc.restype = None
+    L.or_chain_histogram_assoc.argtypes = [vp, vp, vp, vp, vp, vp, u32, i64, u64, C.c_int,
+                                           vp, i64]
+    L.or_chain_histogram_assoc.restype = C.c_int
+    return L
 
 
 def _p(a: np.ndarray):

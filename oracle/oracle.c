@@ -532,8 +532,8 @@ void or_interleaved_order(const or_model *m, int32_t *order)
 /* conditionals at their sweep-start values (the token's own contribution    */
 /* removed), while n, t, B_kw and the document counts stay live -- the       */
 /* thesis lets the sums drift during an iteration and corrects them          */
-/* regularly; this variant is not exact Gibbs (parity unpinned: only its     */
-/* invariants and its single-wave GPU counterpart check it).               */
+/* regularly; this variant is not exact Gibbs.  It is pinned by a re-walk   */
+/* that keeps the live and the held counts itself (tests).                  */
 /* ------------------------------------------------------------------------ */
 int or_sweep_ordered(const or_model *m, or_counts *c, int32_t *z, uint8_t *r, uint32_t sweep,
                      uint64_t seed, const int32_t *order, int stale_totals, int64_t *out_stats)
