@@ -31,9 +31,9 @@
  *     hyperparameters, init seed, sequence of (sweep, seed)), independent of
  *     launch configuration and scheduling.
  *
- * Layouts: topics of one (group, word) row are contiguous.  n and t are
- * exported as [g][w][k] (group-major, then word, then topic); the shadow-base
- * table counts B as [w][k]; per-restaurant totals as [g][k].
+ * Layouts: n and t are exported as [g][k][w] (group, then topic, then word:
+ * the order of the thesis's n_{i,k,w}); the shadow-base table counts B as
+ * [w][k] (topics contiguous); per-restaurant totals as [g][k].
  * The (z, r) state is per token in corpus order.
  */
 #ifndef SPDP_H
@@ -173,11 +173,12 @@ int spdp_sweep_async(spdp_state *s, uint32_t sweep, uint64_t seed, int32_t waves
 
 /*
  * Export customer counts n and table counts t of groups [g_begin, g_end) as
- * [g_end - g_begin][V][K] int32 each (either pointer may be NULL to skip it).
- * Synchronises.  Errors: E_ARG, E_HIP.
+ * [g_end - g_begin][K][V] int32 each: element ((g - g_begin) K + k) V + w is
+ * n[g][k][w] (either pointer may be NULL to skip it).  Synchronises.
+ * Errors: E_ARG, E_HIP.
  */
-int spdp_counts(const spdp_state *s, int32_t g_begin, int32_t g_end, int32_t *n_gwk,
-                int32_t *t_gwk, int where);
+int spdp_counts(const spdp_state *s, int32_t g_begin, int32_t g_end, int32_t *n_gkw,
+                int32_t *t_gkw, int where);
 
 /*
  * Export the totals: customers N[g][k] = sum_w n, tables T[g][k] = sum_w t,
@@ -262,7 +263,7 @@ int spdp_hellinger(spdp_state *s, const double *p, int32_t kp, const double *q, 
                    int32_t n_outcomes, double *h, int where);
 
 /*
- * Topic alignment for comparing two models ("re-ordered to align" in the
+ * Topic alignment for comparing two models (the topics are reordered to line up in the
  * Hellinger comparison): the one-to-one matching of the kp rows of h
  * [kp][kq] (kp <= kq; e.g. distances from spdp_hellinger) to columns that
  * minimises the summed entries.  match [kp] int32 receives the column of each
@@ -332,6 +333,33 @@ int spdp_stats(const spdp_state *s, int64_t *changed, int64_t *repaired);
 #define SPDP_NKERNELS 4
 int spdp_kernel_timing(spdp_state *s, int enable);
 int spdp_kernel_times(spdp_state *s, double *ms, int64_t *launches);
+
+/*
+ * Invariant check of the count state: the stored counts are recounted from
+ * the tokens' (z, r) (and sources, with word associations) and compared, and
+ * every cell must satisfy 0 <= t <= n with t > 0 exactly when n > 0 (a cell
+ * with customers but no table has joint probability zero).  Checked: every
+ * count row (and the 16-bit copy of a narrow row), the totals N_gk, T_gk,
+ * B_k, the shadow-base counts B and their 16-bit copy and width flag, and
+ * every token's topic and source slot.  The read-only counterpart of the
+ * count regeneration the thesis runs on the host after a parallel iteration
+ * (Algorithm MGPU-DP-SPDP Host).  *bad (may be NULL) receives the number of
+ * failing cells, tokens and totals.  Allocates and frees device scratch of
+ * (2 G + 1) Kp ints (+ V Kp with word associations).  Synchronises.
+ * Errors: E_ARG, E_NOMEM, E_HIP, E_STATE (some check failed; the message
+ * gives the counts).
+ */
+int spdp_check(spdp_state *s, int64_t *bad);
+
+/*
+ * Test hook: add dn customers and dt tables to the stored count cell of
+ * (group g, word w, topic k) -- the 32-bit row only, nothing else -- so that
+ * tests can make the state inconsistent and see spdp_check report it (any
+ * later rebuild, e.g. spdp_set_assignments, restores consistent counts).
+ * Synchronises.  Errors: E_ARG (cell out of range, or a count would leave
+ * [0, 65535]), E_HIP.
+ */
+int spdp_debug_poke(spdp_state *s, int32_t g, int32_t w, int32_t k, int32_t dn, int32_t dt);
 
 /*
  * Shape of the state: out[0] = N, [1] = D, [2] = V, [3] = G, [4] = K,

@@ -12,7 +12,7 @@ for discrete distributions p, q over the same outcomes,
 
     H(p, q) = sqrt( 1/2 * sum_v (sqrt(p_v) - sqrt(q_v))^2 )   in [0, 1],
 
-and takes "re-ordered to align" as the one-to-one matching of topics of least
+and takes the reordering of topics as the one-to-one matching of topics of least
 total distance (a linear assignment problem, solved here by scipy's library
 routine).
 """

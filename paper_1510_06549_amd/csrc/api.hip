@@ -49,6 +49,7 @@ struct spdp_state {
     int device = 0;
     int cur = 0;
     int64_t bytes = 0;
+    int64_t n_narrow_rows = 0;
     bool timing = false;
     std::vector<EventPair> events[SPDP_NKERNELS];
     std::vector<void *> allocs;
@@ -376,16 +377,28 @@ int create_state(const spdp_corpus *corpus, const spdp_groups *groups, const spd
     m.ncap = herr[1] < 1 ? 1 : herr[1];
     TRY_HIP(launch_fill_i32(B.err, 2, 0, s->st));
 
-    // tokens grouped by count row (the count rebuild walks rows)
+    // tokens grouped by count row (the count rebuild walks rows); the rows
+    // whose (group, word) pair occurs at most kNarrowMax times (fixed by the
+    // corpus) also get 16-bit copies
+    unsigned long long n_narrow = 0;
     {
         int rc2 = dev_alloc(s, &B.perm, N, "row-sorted tokens");
         if (rc2 == SPDP_OK) rc2 = dev_alloc(s, &B.row_off, rows + 1, "row offsets");
+        if (rc2 == SPDP_OK) rc2 = dev_alloc(s, &B.row_narrow, rows, "narrow-row flags");
+        if (rc2 == SPDP_OK) rc2 = dev_alloc(s, &B.tok_narrow, N, "narrow-row flags of tokens");
         if (rc2 != SPDP_OK) cleanup_staging();
         TRY(rc2);
         e = build_row_index(m, B, gw_count, s->st);
+        if (e == hipSuccess) e = launch_fill_u64(B.ctr, 4, 0, s->st);
+        if (e == hipSuccess)
+            e = launch_narrow_flags(m, B.gw, gw_count, B.row_narrow, B.tok_narrow, B.ctr, s->st);
+        if (e == hipSuccess)
+            e = hipMemcpyAsync(&n_narrow, B.ctr, sizeof n_narrow, hipMemcpyDeviceToHost, s->st);
+        if (e == hipSuccess) e = hipStreamSynchronize(s->st);
         cleanup_staging();
         TRY_HIP(e);
     }
+    s->n_narrow_rows = (int64_t)n_narrow;
 
     // word associations
     if (assoc) TRY(upload_assoc(s, assoc));
@@ -409,6 +422,13 @@ int create_state(const spdp_corpus *corpus, const spdp_groups *groups, const spd
     TRY(dev_alloc(s, &B.B16, (int64_t)V * m.Kp, "16-bit shadow-base table counts"));
     TRY(dev_alloc(s, &B.wide, 1, "shadow-base width flag"));
     TRY_HIP(launch_fill_i32(B.nt, rows * m.Kp, 0, s->st));
+    // (the 16-bit copies: a buffer of the full row count, so that row q's copy
+    // sits at q Kp; only the narrow rows' copies are written and read; the
+    // sampler's vector reads of a narrow row run at most 4 cells past its
+    // end, which the 64-cell tail keeps inside the buffer)
+    const int64_t n16 = (n_narrow > 0 ? rows * m.Kp : 0) + 64;
+    TRY(dev_alloc(s, &B.nt16, n16, "narrow count rows"));
+    TRY_HIP(launch_fill_i32(reinterpret_cast<int32_t *>(B.nt16), n16 / 2, 0, s->st));
     TRY(dev_alloc(s, &B.Ngk, (int64_t)G * m.Kp, "N_gk"));
     TRY(dev_alloc(s, &B.Tgk, (int64_t)G * m.Kp, "T_gk"));
     TRY(dev_alloc(s, &B.Bk, m.Kp, "B_k"));
@@ -533,15 +553,15 @@ int spdp_sweep_async(spdp_state *s, uint32_t sweep, uint64_t seed, int32_t waves
     return SPDP_OK;
 }
 
-int spdp_counts(const spdp_state *s, int32_t g_begin, int32_t g_end, int32_t *n_gwk,
-                int32_t *t_gwk, int where)
+int spdp_counts(const spdp_state *s, int32_t g_begin, int32_t g_end, int32_t *n_gkw,
+                int32_t *t_gkw, int where)
 {
     if (!s) return fail(SPDP_E_ARG, "state is NULL");
     const Model &m = s->m;
     if (g_begin < 0 || g_end > m.G || g_begin > g_end) return fail(SPDP_E_ARG, "bad group range");
     if (where != 0 && where != 1) return fail(SPDP_E_ARG, "where must be 0 or 1");
     HIP_TRY(hipSetDevice(s->device));
-    if (!n_gwk && !t_gwk) return SPDP_OK;
+    if (!n_gkw && !t_gkw) return SPDP_OK;
     const int64_t cells = (int64_t)m.V * m.K;
     int32_t *stage_n = nullptr, *stage_t = nullptr;
     if (where == 0) {
@@ -557,14 +577,14 @@ int spdp_counts(const spdp_state *s, int32_t g_begin, int32_t g_end, int32_t *n_
     for (int32_t g = g_begin; g < g_end && e == hipSuccess; ++g) {
         const int64_t off = (int64_t)(g - g_begin) * cells;
         if (where == 1) {
-            e = launch_unpack_counts(m, s->b, g, n_gwk ? n_gwk + off : nullptr,
-                                     t_gwk ? t_gwk + off : nullptr, s->st);
+            e = launch_unpack_counts(m, s->b, g, n_gkw ? n_gkw + off : nullptr,
+                                     t_gkw ? t_gkw + off : nullptr, s->st);
         } else {
             e = launch_unpack_counts(m, s->b, g, stage_n, stage_t, s->st);
-            if (e == hipSuccess && n_gwk)
-                e = hipMemcpyAsync(n_gwk + off, stage_n, (size_t)cells * 4, hipMemcpyDeviceToHost, s->st);
-            if (e == hipSuccess && t_gwk)
-                e = hipMemcpyAsync(t_gwk + off, stage_t, (size_t)cells * 4, hipMemcpyDeviceToHost, s->st);
+            if (e == hipSuccess && n_gkw)
+                e = hipMemcpyAsync(n_gkw + off, stage_n, (size_t)cells * 4, hipMemcpyDeviceToHost, s->st);
+            if (e == hipSuccess && t_gkw)
+                e = hipMemcpyAsync(t_gkw + off, stage_t, (size_t)cells * 4, hipMemcpyDeviceToHost, s->st);
             if (e == hipSuccess) e = hipStreamSynchronize(s->st);
         }
     }
@@ -1048,6 +1068,53 @@ int spdp_kernel_times(spdp_state *s, double *ms, int64_t *launches)
         if (launches) launches[c] = (int64_t)s->events[c].size();
     }
     return SPDP_OK;
+}
+
+int spdp_check(spdp_state *s, int64_t *bad)
+{
+    if (!s) return fail(SPDP_E_ARG, "state is NULL");
+    HIP_TRY(hipSetDevice(s->device));
+    const Model &m = s->m;
+    const int64_t need = 2 * (int64_t)m.G * m.Kp + m.Kp + (m.Sp > 0 ? (int64_t)m.V * m.Kp : 0);
+    int32_t *scratch = nullptr;
+    if (hipMalloc(&scratch, (size_t)need * sizeof(int32_t)) != hipSuccess) {
+        (void)hipGetLastError();
+        return fail(SPDP_E_NOMEM, "check scratch of %lld ints", (long long)need);
+    }
+    unsigned long long c[4] = {0, 0, 0, 0};
+    hipError_t e = launch_fill_u64(s->b.ctr, 4, 0, s->st);
+    if (e == hipSuccess) e = launch_check(m, s->b, s->b.zr[s->cur], scratch, s->b.ctr, s->st);
+    if (e == hipSuccess) e = hipMemcpyAsync(c, s->b.ctr, sizeof c, hipMemcpyDeviceToHost, s->st);
+    if (e == hipSuccess) e = hipStreamSynchronize(s->st);
+    (void)hipFree(scratch);
+    HIP_TRY(e);
+    if (bad) *bad = (int64_t)(c[0] + c[1]);
+    if (c[0] || c[1])
+        return fail(SPDP_E_STATE,
+                    "count state inconsistent: %llu count cells or token states differ from a "
+                    "recount of (z, r) or are invalid; %llu totals or shadow-base cells differ",
+                    c[0], c[1]);
+    return SPDP_OK;
+}
+
+int spdp_debug_poke(spdp_state *s, int32_t g, int32_t w, int32_t k, int32_t dn, int32_t dt)
+{
+    if (!s) return fail(SPDP_E_ARG, "state is NULL");
+    const Model &m = s->m;
+    if (g < 0 || g >= m.G || w < 0 || w >= m.V || k < 0 || k >= m.K)
+        return fail(SPDP_E_ARG, "cell (%d, %d, %d) out of range", g, w, k);
+    HIP_TRY(hipSetDevice(s->device));
+    int32_t *cell = s->b.nt + ((int64_t)g * m.V + w) * m.Kp + k;
+    int32_t x = 0;
+    HIP_TRY(hipMemcpyAsync(&x, cell, sizeof x, hipMemcpyDeviceToHost, s->st));
+    int rc = sync(s);
+    if (rc != SPDP_OK) return rc;
+    const int32_t n = (x & kCountMax) + dn, t = (x >> kCountBits) + dt;
+    if (n < 0 || n > kCountMax || t < 0 || t > kCountMax)
+        return fail(SPDP_E_ARG, "poked counts (%d, %d) out of [0, %d]", n, t, kCountMax);
+    x = n | (t << kCountBits);
+    HIP_TRY(hipMemcpyAsync(cell, &x, sizeof x, hipMemcpyHostToDevice, s->st));
+    return sync(s);
 }
 
 int spdp_info(const spdp_state *s, int64_t *out8)

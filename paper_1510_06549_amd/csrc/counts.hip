@@ -6,12 +6,15 @@
 // bounded by the largest per-(group, word) token count, checked < 2^16 at
 // creation).
 //
-//   row index   tokens sorted by count row q = g V + w (stable, so each row's
-//               token list is in increasing token index), built once
+//   row index   tokens grouped by count row q = g V + w (row offsets by an
+//               exclusive scan of the per-row token counts, then a scatter
+//               with one atomic cursor per row; the order inside a row is
+//               free, since nothing below depends on it), built once
 //   k_rows      per row: LDS histogram of its tokens' (z, r) -> the row's
 //               packed cells; then every cell left with customers but no
 //               table promotes the smallest-index token of that cell to table
 //               head (the repair of the parallel pass), and the row is written
+//               (a narrow row also as its 16-bit copy, which the sampler reads)
 //   k_base      shadow-base table counts B[w][k] = sum_g t[g][w][k], and the
 //               16-bit copy the sampler reads (with a flag raised when a count
 //               does not fit, in which case the sampler reads B itself)
@@ -19,9 +22,7 @@
 //               the same with word associations: shadow-base counts keyed by
 //               each head's source word, and a promoted head takes its row's
 //               most probable source
-//   k_unpack    export of n and t as separate int32 arrays
-#include <hipcub/hipcub.hpp>
-
+//   k_unpack    export of n and t as separate int32 arrays, [k][w] per group
 #include <climits>
 
 #include "spdp_internal.hpp"
@@ -38,15 +39,9 @@ inline int64_t blocks_for(int64_t n, int per_block)
     return b < 1 ? 1 : b;
 }
 
-__global__ void k_iota(int32_t *__restrict__ x, int64_t n)
-{
-    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (i < n) x[i] = (int32_t)i;
-}
-
 // The row's tokens' states, four per lane in flight: lane l takes row list
-// entries rs + l, rs + l + 64, ... and hands each (list index j, state v) to
-// f in any order.
+// entries rs + l, rs + l + 64, ... and hands each (token index, state v) to f
+// in any order.
 template <typename F>
 __device__ __forceinline__ void for_row_states(int32_t rs, int32_t re, int32_t lane,
                                                const int32_t *__restrict__ perm,
@@ -60,19 +55,23 @@ __device__ __forceinline__ void for_row_states(int32_t rs, int32_t re, int32_t l
 #pragma unroll
         for (int u = 0; u < 4; ++u) v[u] = zr[t[u]];
 #pragma unroll
-        for (int u = 0; u < 4; ++u) f(j + 64 * u, v[u]);
+        for (int u = 0; u < 4; ++u) f(t[u], v[u]);
     }
-    for (; j < re; j += 64) f(j, zr[perm[j]]);
+    for (; j < re; j += 64) {
+        const int32_t t = perm[j];
+        f(t, zr[t]);
+    }
 }
 
-// One 64-lane block per count row; the row's histogram and the first list
+// One 64-lane block per count row; the row's histogram and the smallest token
 // index of each topic in LDS (2 Kp ints of dynamic shared memory).  Every
 // token's state is read once: a cell left with customers but no table holds
-// only r = 0 tokens, and its first token in the row list (the smallest token
-// index, the list being a stable sort) becomes its head.
+// only r = 0 tokens, and its smallest-index token becomes its head.
 __global__ void __launch_bounds__(64) k_rows(int32_t Kp, const int32_t *__restrict__ row_off,
                                              const int32_t *__restrict__ perm,
+                                             const uint8_t *__restrict__ row_narrow,
                                              int32_t *__restrict__ zr, int32_t *__restrict__ nt,
+                                             uint16_t *__restrict__ nt16,
                                              uint32_t *__restrict__ rep_part)
 {
     extern __shared__ int32_t rows_lds[];
@@ -87,21 +86,24 @@ __global__ void __launch_bounds__(64) k_rows(int32_t Kp, const int32_t *__restri
             first[k] = INT_MAX;
         }
         __syncthreads();
-        for_row_states(rs, re, lane, perm, zr, [&](int32_t j, int32_t v) {
+        for_row_states(rs, re, lane, perm, zr, [&](int32_t tok, int32_t v) {
             atomicAdd(&h[v >> 1], 1 + ((v & 1) << 16));
-            atomicMin(&first[v >> 1], j);
+            atomicMin(&first[v >> 1], tok);
         });
         __syncthreads();
         int32_t *__restrict__ row = nt + q * Kp;
+        uint16_t *__restrict__ row16 = nt16 + q * Kp;
+        const bool nar = row_narrow[q] != 0;
         for (int32_t k = lane; k < Kp; k += 64) {
             int32_t x = h[k];
             if (x != 0 && (x >> 16) == 0) {
-                const int32_t tok = perm[first[k]];
+                const int32_t tok = first[k];
                 zr[tok] = zr[tok] | 1;
                 x += 1 << 16;
                 ++rep;
             }
             row[k] = x;
+            if (nar) row16[k] = narrow_of(x);
         }
     }
     for (int o = 32; o > 0; o >>= 1) rep += __shfl_xor(rep, o);
@@ -117,8 +119,10 @@ __global__ void __launch_bounds__(64) k_rows_assoc(int32_t Kp, int32_t Sp,
                                                    const int32_t *__restrict__ perm,
                                                    const int32_t *__restrict__ srcrec,
                                                    const uint8_t *__restrict__ head_slot,
+                                                   const uint8_t *__restrict__ row_narrow,
                                                    int32_t *__restrict__ zr,
                                                    int32_t *__restrict__ nt,
+                                                   uint16_t *__restrict__ nt16,
                                                    int32_t *__restrict__ B,
                                                    uint32_t *__restrict__ rep_part)
 {
@@ -135,25 +139,28 @@ __global__ void __launch_bounds__(64) k_rows_assoc(int32_t Kp, int32_t Sp,
             first[k] = INT_MAX;
         }
         __syncthreads();
-        for_row_states(rs, re, lane, perm, zr, [&](int32_t j, int32_t v) {
+        for_row_states(rs, re, lane, perm, zr, [&](int32_t tok, int32_t v) {
             const int32_t k = zr_topic(v);
             atomicAdd(&h[k], 1 + ((v & 1) << 16));
-            atomicMin(&first[k], j);
+            atomicMin(&first[k], tok);
             if (v & 1) atomicAdd(&B[(int64_t)src[zr_slot(v)] * Kp + k], 1);
         });
         __syncthreads();
         const int32_t hs = head_slot[q];
         int32_t *__restrict__ row = nt + q * Kp;
+        uint16_t *__restrict__ row16 = nt16 + q * Kp;
+        const bool nar = row_narrow[q] != 0;
         for (int32_t k = lane; k < Kp; k += 64) {
             int32_t x = h[k];
             if (x != 0 && (x >> 16) == 0) {
-                const int32_t tok = perm[first[k]];
+                const int32_t tok = first[k];
                 zr[tok] = zr_pack(k, 1, hs);
                 x += 1 << 16;
                 atomicAdd(&B[(int64_t)src[hs] * Kp + k], 1);
                 ++rep;
             }
             row[k] = x;
+            if (nar) row16[k] = narrow_of(x);
         }
     }
     for (int o = 32; o > 0; o >>= 1) rep += __shfl_xor(rep, o);
@@ -192,15 +199,30 @@ __global__ void k_base(int32_t G, int32_t V, int32_t Kp, const int32_t *__restri
     if (__any(over) && (threadIdx.x & 63) == 0) atomicOr(wide, 1);
 }
 
-__global__ void k_unpack(int32_t V, int32_t K, int32_t Kp, const int32_t *__restrict__ nt_g,
-                         int32_t *__restrict__ n_out, int32_t *__restrict__ t_out)
+// Export of one group's counts as [k][w] (topic-major, the thesis's logical
+// order): a 64 x 64 tile of cells is read along topics (rows are contiguous
+// in k) and written along words through LDS, so both sides are coalesced.
+__global__ void __launch_bounds__(256) k_unpack(int32_t V, int32_t K, int32_t Kp,
+                                                const int32_t *__restrict__ nt_g,
+                                                int32_t *__restrict__ n_out,
+                                                int32_t *__restrict__ t_out)
 {
-    const int64_t j = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (j >= (int64_t)V * K) return;
-    const int64_t w = j / K, k = j % K;
-    const int32_t x = nt_g[w * Kp + k];
-    if (n_out) n_out[j] = x & 0xFFFF;
-    if (t_out) t_out[j] = x >> 16;
+    __shared__ int32_t tile[64][65];
+    const int32_t tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
+    const int32_t w0 = blockIdx.x * 64, k0 = blockIdx.y * 64;
+    for (int32_t i = ty; i < 64; i += 4) {
+        const int32_t w = w0 + i, k = k0 + tx;
+        tile[i][tx] = (w < V && k < K) ? nt_g[(int64_t)w * Kp + k] : 0;
+    }
+    __syncthreads();
+    for (int32_t i = ty; i < 64; i += 4) {
+        const int32_t k = k0 + i, w = w0 + tx;
+        if (k >= K || w >= V) continue;
+        const int32_t x = tile[tx][i];
+        const int64_t j = (int64_t)k * V + w;
+        if (n_out) n_out[j] = x & 0xFFFF;
+        if (t_out) t_out[j] = x >> 16;
+    }
 }
 
 // Sum of x[0..n) into *out (fixed-order two-level reduction).
@@ -257,98 +279,289 @@ __global__ void __launch_bounds__(kBlock) k_sum_u64(const unsigned long long *__
 
 constexpr int kReduceBlocks = 1024;
 
+// ------------------------------------------------------- exclusive scan
+// Three passes over tiles of kScanTile ints: tile sums, a one-block scan of
+// the tile sums (in place, exclusive), and the tiles' own scans offset by
+// their tile's prefix.  Totals must fit in int32.
+constexpr int kScanThreads = 256;
+constexpr int kScanItems = 16;
+constexpr int kScanTile = kScanThreads * kScanItems;
+
+// Block-wide exclusive scan of one int per thread; the block's total is
+// returned to every thread.
+__device__ int32_t block_exclusive_scan(int32_t x, int32_t *total)
+{
+    __shared__ int32_t warp_sums[kScanThreads / 64];
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    int32_t incl = x;
+    for (int o = 1; o < 64; o <<= 1) {
+        const int32_t y = __shfl_up(incl, o);
+        if (lane >= o) incl += y;
+    }
+    __syncthreads();
+    if (lane == 63) warp_sums[w] = incl;
+    __syncthreads();
+    int32_t before = 0, all = 0;
+    for (int i = 0; i < kScanThreads / 64; ++i) {
+        const int32_t v = warp_sums[i];
+        if (i < w) before += v;
+        all += v;
+    }
+    *total = all;
+    return before + incl - x;
+}
+
+__global__ void __launch_bounds__(kScanThreads) k_tile_sums(const int32_t *__restrict__ in,
+                                                            int64_t n, int32_t *__restrict__ sums)
+{
+    const int64_t t0 = (int64_t)blockIdx.x * kScanTile + (int64_t)threadIdx.x * kScanItems;
+    int32_t s = 0;
+    for (int i = 0; i < kScanItems; ++i)
+        if (t0 + i < n) s += in[t0 + i];
+    int32_t total = 0;
+    (void)block_exclusive_scan(s, &total);
+    if (threadIdx.x == 0) sums[blockIdx.x] = total;
+}
+
+__global__ void __launch_bounds__(kScanThreads) k_scan_sums(int32_t *__restrict__ sums, int64_t nb)
+{
+    int32_t carry = 0;
+    for (int64_t b0 = 0; b0 < nb; b0 += kScanThreads) {
+        const int64_t j = b0 + threadIdx.x;
+        const int32_t x = j < nb ? sums[j] : 0;
+        int32_t total = 0;
+        const int32_t ex = block_exclusive_scan(x, &total);
+        if (j < nb) sums[j] = carry + ex;
+        carry += total;
+    }
+}
+
+__global__ void __launch_bounds__(kScanThreads) k_tile_scan(const int32_t *__restrict__ in,
+                                                            int64_t n,
+                                                            const int32_t *__restrict__ sums,
+                                                            int32_t *__restrict__ out)
+{
+    const int64_t t0 = (int64_t)blockIdx.x * kScanTile + (int64_t)threadIdx.x * kScanItems;
+    int32_t v[kScanItems], s = 0;
+    for (int i = 0; i < kScanItems; ++i) {
+        v[i] = t0 + i < n ? in[t0 + i] : 0;
+        s += v[i];
+    }
+    int32_t total = 0;
+    int32_t run = sums[blockIdx.x] + block_exclusive_scan(s, &total);
+    for (int i = 0; i < kScanItems; ++i) {
+        if (t0 + i < n) out[t0 + i] = run;
+        run += v[i];
+    }
+}
+
+// token i goes to the next free slot of its row
+__global__ void k_scatter_rows(int64_t N, const int32_t *__restrict__ gw,
+                               int32_t *__restrict__ cursor, int32_t *__restrict__ perm)
+{
+    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i < N) perm[atomicAdd(&cursor[gw[i]], 1)] = (int32_t)i;
+}
+
+// ------------------------------------------------------- visiting order
+constexpr int kOrderThreads = 1024;
+constexpr int kOrderChunk = 4096;  // documents per chunk (4 per thread)
+constexpr int kOrderItems = kOrderChunk / kOrderThreads;
+
+// Block-wide exclusive scan for the order kernels (1024 threads).
+__device__ int32_t order_exclusive_scan(int32_t x, int32_t *total)
+{
+    __shared__ int32_t wsum[kOrderThreads / 64];
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    int32_t incl = x;
+    for (int o = 1; o < 64; o <<= 1) {
+        const int32_t y = __shfl_up(incl, o);
+        if (lane >= o) incl += y;
+    }
+    __syncthreads();
+    if (lane == 63) wsum[w] = incl;
+    __syncthreads();
+    int32_t before = 0, all = 0;
+    for (int i = 0; i < kOrderThreads / 64; ++i) {
+        const int32_t v = wsum[i];
+        if (i < w) before += v;
+        all += v;
+    }
+    *total = all;
+    return before + incl - x;
+}
+
+// lengths of this thread's documents of chunk blockIdx.x (0 past the end)
+__device__ __forceinline__ void chunk_lengths(int32_t D, const int64_t *__restrict__ doc_off,
+                                              int32_t (&len)[kOrderItems], int32_t &longest)
+{
+    const int64_t d0 = (int64_t)blockIdx.x * kOrderChunk + (int64_t)threadIdx.x * kOrderItems;
+    int32_t mx = 0;
+    for (int i = 0; i < kOrderItems; ++i) {
+        const int64_t d = d0 + i;
+        len[i] = d < D ? (int32_t)(doc_off[d + 1] - doc_off[d]) : 0;
+        mx = max(mx, len[i]);
+    }
+    __shared__ int32_t lmax;
+    if (threadIdx.x == 0) lmax = 0;
+    __syncthreads();
+    atomicMax(&lmax, mx);
+    __syncthreads();
+    longest = lmax;
+}
+
+// cnt[c][p] = documents of chunk c longer than p (p < L)
+__global__ void __launch_bounds__(kOrderThreads) k_order_counts(int32_t D, int32_t L,
+                                                                const int64_t *__restrict__ doc_off,
+                                                                int32_t *__restrict__ cnt)
+{
+    int32_t len[kOrderItems], longest = 0;
+    chunk_lengths(D, doc_off, len, longest);
+    int32_t *row = cnt + (int64_t)blockIdx.x * L;
+    for (int32_t p = 0; p < L; ++p) {
+        if (p >= longest) {  // (uniform: no document of the chunk reaches p)
+            for (int32_t q = p + threadIdx.x; q < L; q += kOrderThreads) row[q] = 0;
+            break;
+        }
+        int32_t x = 0;
+        for (int i = 0; i < kOrderItems; ++i) x += len[i] > p ? 1 : 0;
+        int32_t total = 0;
+        (void)order_exclusive_scan(x, &total);
+        if (threadIdx.x == 0) row[p] = total;
+    }
+}
+
+// cnt[c][p] -> first slot of chunk c's documents at position p (position p
+// starts after every token of positions < p; chunks in order within it);
+// base[p] = that start
+__global__ void __launch_bounds__(kOrderThreads) k_order_offsets(int32_t chunks, int32_t L,
+                                                                 int32_t *__restrict__ cnt,
+                                                                 int32_t *__restrict__ base)
+{
+    // per position: exclusive scan over chunks (one thread per position)
+    for (int32_t p = threadIdx.x; p < L; p += kOrderThreads) {
+        int32_t run = 0;
+        for (int32_t c = 0; c < chunks; ++c) {
+            const int32_t x = cnt[(int64_t)c * L + p];
+            cnt[(int64_t)c * L + p] = run;
+            run += x;
+        }
+        base[p] = run;  // tokens at position p
+    }
+    __syncthreads();
+    // positions' starts: exclusive scan of the per-position token counts
+    int32_t carry = 0;
+    for (int32_t p0 = 0; p0 < L; p0 += kOrderThreads) {
+        const int32_t p = p0 + threadIdx.x;
+        const int32_t x = p < L ? base[p] : 0;
+        int32_t total = 0;
+        const int32_t ex = order_exclusive_scan(x, &total);
+        __syncthreads();
+        if (p < L) base[p] = carry + ex;
+        carry += total;
+        __syncthreads();
+    }
+}
+
+__global__ void __launch_bounds__(kOrderThreads) k_order_place(int32_t D, int32_t L,
+                                                               const int64_t *__restrict__ doc_off,
+                                                               const int32_t *__restrict__ cnt,
+                                                               const int32_t *__restrict__ base,
+                                                               int32_t *__restrict__ order)
+{
+    int32_t len[kOrderItems], longest = 0;
+    chunk_lengths(D, doc_off, len, longest);
+    const int64_t d0 = (int64_t)blockIdx.x * kOrderChunk + (int64_t)threadIdx.x * kOrderItems;
+    const int32_t *row = cnt + (int64_t)blockIdx.x * L;
+    for (int32_t p = 0; p < longest; ++p) {
+        int32_t x = 0;
+        for (int i = 0; i < kOrderItems; ++i) x += len[i] > p ? 1 : 0;
+        int32_t total = 0;
+        int32_t slot = base[p] + row[p] + order_exclusive_scan(x, &total);
+        for (int i = 0; i < kOrderItems; ++i)
+            if (len[i] > p) order[slot++] = (int32_t)(doc_off[d0 + i] + p);
+    }
+}
+
 }  // namespace
+
+hipError_t exclusive_scan(const int32_t *in, int32_t *out, int64_t n, hipStream_t st)
+{
+    if (n <= 0) return hipSuccess;
+    const int64_t nb = (n + kScanTile - 1) / kScanTile;
+    int32_t *sums = nullptr;
+    hipError_t e = hipMalloc(&sums, (size_t)nb * sizeof(int32_t));
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(k_tile_sums, dim3((unsigned)nb), dim3(kScanThreads), 0, st, in, n, sums);
+    hipLaunchKernelGGL(k_scan_sums, dim3(1), dim3(kScanThreads), 0, st, sums, nb);
+    hipLaunchKernelGGL(k_tile_scan, dim3((unsigned)nb), dim3(kScanThreads), 0, st, in, n, sums,
+                       out);
+    e = hipGetLastError();
+    hipError_t e2 = hipStreamSynchronize(st);
+    (void)hipFree(sums);
+    return e != hipSuccess ? e : e2;
+}
 
 hipError_t build_row_index(const Model &m, DeviceBuffers &b, const int32_t *gw_count,
                            hipStream_t st)
 {
     const int64_t rows = (int64_t)m.G * m.V;
-    hipError_t e;
-    // row offsets: exclusive sum of the per-row token counts (rows + 1 entries,
-    // the last count being zero)
-    size_t scan_bytes = 0;
-    e = hipcub::DeviceScan::ExclusiveSum(nullptr, scan_bytes, gw_count, b.row_off, rows + 1, st);
-    if (e != hipSuccess) return e;
-    // stable radix sort of (row, token) pairs
-    int end_bit = 1;
-    while ((1ll << end_bit) < rows) ++end_bit;
-    int32_t *keys_out = nullptr, *vals_in = nullptr;
-    size_t sort_bytes = 0;
-    e = hipcub::DeviceRadixSort::SortPairs(nullptr, sort_bytes, b.gw, keys_out, vals_in, b.perm,
-                                           (int)m.N, 0, end_bit, st);
-    if (e != hipSuccess) return e;
-    void *temp = nullptr;
-    const size_t temp_bytes = scan_bytes > sort_bytes ? scan_bytes : sort_bytes;
-    if ((e = hipMalloc(&temp, temp_bytes > 0 ? temp_bytes : 1)) != hipSuccess) return e;
-    if ((e = hipMalloc(&keys_out, (size_t)(m.N > 0 ? m.N : 1) * 4)) != hipSuccess) {
-        (void)hipFree(temp);
-        return e;
-    }
-    if ((e = hipMalloc(&vals_in, (size_t)(m.N > 0 ? m.N : 1) * 4)) != hipSuccess) {
-        (void)hipFree(temp);
-        (void)hipFree(keys_out);
-        return e;
-    }
-    size_t tb = temp_bytes;
-    e = hipcub::DeviceScan::ExclusiveSum(temp, tb, gw_count, b.row_off, rows + 1, st);
-    if (e == hipSuccess && m.N > 0) {
-        hipLaunchKernelGGL(k_iota, dim3((unsigned)blocks_for(m.N, kBlock)), dim3(kBlock), 0, st,
-                           vals_in, m.N);
+    // row offsets: exclusive sum of the per-row token counts (rows + 1
+    // entries, the last count being zero)
+    hipError_t e = exclusive_scan(gw_count, b.row_off, rows + 1, st);
+    if (e != hipSuccess || m.N <= 0) return e;
+    int32_t *cursor = nullptr;
+    if ((e = hipMalloc(&cursor, (size_t)rows * sizeof(int32_t))) != hipSuccess) return e;
+    e = hipMemcpyAsync(cursor, b.row_off, (size_t)rows * sizeof(int32_t),
+                       hipMemcpyDeviceToDevice, st);
+    if (e == hipSuccess) {
+        hipLaunchKernelGGL(k_scatter_rows, dim3((unsigned)blocks_for(m.N, kBlock)), dim3(kBlock),
+                           0, st, m.N, b.gw, cursor, b.perm);
         e = hipGetLastError();
-        if (e == hipSuccess) {
-            tb = temp_bytes;
-            e = hipcub::DeviceRadixSort::SortPairs(temp, tb, b.gw, keys_out, vals_in, b.perm,
-                                                   (int)m.N, 0, end_bit, st);
-        }
     }
     hipError_t e2 = hipStreamSynchronize(st);
-    (void)hipFree(temp);
-    (void)hipFree(keys_out);
-    (void)hipFree(vals_in);
+    (void)hipFree(cursor);
     return e != hipSuccess ? e : e2;
 }
 
-// Visiting order of the asynchronous sweep: tokens stably sorted by their
-// position inside the document, so at each position the documents come in
-// index order (the word order rearrangement).  Fills b.order and b.tok_doc.
+// Visiting order of the asynchronous sweep: tokens by their position inside
+// the document, documents in index order at each position (the word order
+// rearrangement).  Documents are taken in chunks of kOrderChunk; for every
+// position p, chunk c counts its documents longer than p, a scan over chunks
+// and over positions gives each (chunk, position) its first slot, and the
+// chunk's block ranks its documents longer than p by a block-wide scan.
+// Fills b.order and b.tok_doc.
 hipError_t build_visit_order(const Model &m, DeviceBuffers &b, hipStream_t st)
 {
     if (m.N <= 0) return hipSuccess;
-    int32_t *pos = nullptr, *keys_out = nullptr, *vals_in = nullptr;
-    void *temp = nullptr;
+    int32_t *pos = nullptr, *mx = nullptr, *cnt = nullptr, *base = nullptr;
     hipError_t e = hipMalloc(&pos, (size_t)m.N * 4);
-    if (e == hipSuccess) e = hipMalloc(&keys_out, (size_t)m.N * 4);
-    if (e == hipSuccess) e = hipMalloc(&vals_in, (size_t)m.N * 4);
-    if (e == hipSuccess) e = launch_tok_doc(m, b.doc_off, b.tok_doc, pos, st);
-    if (e == hipSuccess) {
-        hipLaunchKernelGGL(k_iota, dim3((unsigned)blocks_for(m.N, kBlock)), dim3(kBlock), 0, st,
-                           vals_in, m.N);
-        e = hipGetLastError();
-    }
-    // the longest document bounds the keys
-    int32_t *mx = nullptr;
-    int32_t longest = 0;
     if (e == hipSuccess) e = hipMalloc(&mx, 4);
+    if (e == hipSuccess) e = launch_tok_doc(m, b.doc_off, b.tok_doc, pos, st);
+    // the longest document bounds the positions
+    int32_t longest = 0;
     if (e == hipSuccess) e = launch_fill_i32(mx, 1, 0, st);
     if (e == hipSuccess) e = launch_max_i32(pos, m.N, mx, st);
     if (e == hipSuccess) e = hipMemcpyAsync(&longest, mx, 4, hipMemcpyDeviceToHost, st);
     if (e == hipSuccess) e = hipStreamSynchronize(st);
-    int end_bit = 1;
-    while ((1ll << end_bit) <= longest) ++end_bit;
-    size_t bytes = 0;
-    if (e == hipSuccess)
-        e = hipcub::DeviceRadixSort::SortPairs(nullptr, bytes, pos, keys_out, vals_in, b.order,
-                                               (int)m.N, 0, end_bit, st);
-    if (e == hipSuccess) e = hipMalloc(&temp, bytes > 0 ? bytes : 1);
-    if (e == hipSuccess)
-        e = hipcub::DeviceRadixSort::SortPairs(temp, bytes, pos, keys_out, vals_in, b.order,
-                                               (int)m.N, 0, end_bit, st);
+    const int32_t L = longest + 1;  // positions 0 .. longest
+    const int64_t chunks = (m.D + kOrderChunk - 1) / kOrderChunk;
+    if (e == hipSuccess) e = hipMalloc(&cnt, (size_t)(chunks * L) * sizeof(int32_t));
+    if (e == hipSuccess) e = hipMalloc(&base, (size_t)L * sizeof(int32_t));
+    if (e == hipSuccess) {
+        hipLaunchKernelGGL(k_order_counts, dim3((unsigned)chunks), dim3(kOrderThreads), 0, st,
+                           m.D, L, b.doc_off, cnt);
+        hipLaunchKernelGGL(k_order_offsets, dim3(1), dim3(kOrderThreads), 0, st, (int32_t)chunks,
+                           L, cnt, base);
+        hipLaunchKernelGGL(k_order_place, dim3((unsigned)chunks), dim3(kOrderThreads), 0, st,
+                           m.D, L, b.doc_off, cnt, base, b.order);
+        e = hipGetLastError();
+    }
     hipError_t e2 = hipStreamSynchronize(st);
     (void)hipFree(pos);
-    (void)hipFree(keys_out);
-    (void)hipFree(vals_in);
     (void)hipFree(mx);
-    (void)hipFree(temp);
+    (void)hipFree(cnt);
+    (void)hipFree(base);
     return e != hipSuccess ? e : e2;
 }
 
@@ -356,8 +569,8 @@ hipError_t launch_rows(const Model &m, const DeviceBuffers &b, int32_t *zr, hipS
 {
     const int64_t rows = (int64_t)m.G * m.V;
     const size_t lds = 2 * (size_t)m.Kp * sizeof(int32_t);
-    hipLaunchKernelGGL(k_rows, dim3((unsigned)rows), dim3(64), lds, st, m.Kp, b.row_off, b.perm, zr,
-                       b.nt, b.rep_part);
+    hipLaunchKernelGGL(k_rows, dim3((unsigned)rows), dim3(64), lds, st, m.Kp, b.row_off, b.perm,
+                       b.row_narrow, zr, b.nt, b.nt16, b.rep_part);
     return hipGetLastError();
 }
 
@@ -378,7 +591,8 @@ hipError_t launch_rows_assoc(const Model &m, const DeviceBuffers &b, int32_t *zr
     if (e != hipSuccess) return e;
     const size_t lds = 2 * (size_t)m.Kp * sizeof(int32_t);
     hipLaunchKernelGGL(k_rows_assoc, dim3((unsigned)rows), dim3(64), lds, st, m.Kp, m.Sp,
-                       b.row_off, b.perm, b.srcrec, b.head_slot, zr, b.nt, b.B, b.rep_part);
+                       b.row_off, b.perm, b.srcrec, b.head_slot, b.row_narrow, zr, b.nt, b.nt16,
+                       b.B, b.rep_part);
     return hipGetLastError();
 }
 
@@ -395,9 +609,9 @@ hipError_t launch_base16(const Model &m, const DeviceBuffers &b, hipStream_t st)
 hipError_t launch_unpack_counts(const Model &m, const DeviceBuffers &b, int32_t g,
                                 int32_t *n_out, int32_t *t_out, hipStream_t st)
 {
-    const int64_t cells = (int64_t)m.V * m.K;
-    hipLaunchKernelGGL(k_unpack, dim3((unsigned)blocks_for(cells, kBlock)), dim3(kBlock), 0, st,
-                       m.V, m.K, m.Kp, b.nt + (int64_t)g * m.V * m.Kp, n_out, t_out);
+    const dim3 grid((unsigned)((m.V + 63) / 64), (unsigned)((m.K + 63) / 64));
+    hipLaunchKernelGGL(k_unpack, grid, dim3(256), 0, st, m.V, m.K, m.Kp,
+                       b.nt + (int64_t)g * m.V * m.Kp, n_out, t_out);
     return hipGetLastError();
 }
 

@@ -28,6 +28,41 @@
 
 namespace spdp {
 
+// fp64 wave scans of the fold-in (the sampler's DPP scan, applied to both
+// 32-bit halves of each value).
+// Both 32-bit halves move with the same DPP control (a disabled source gives
+// 0 in both halves, i.e. +0.0).
+template <int CTRL, int ROW_MASK, bool BOUND>
+__device__ __forceinline__ double dpp_src64(double x)
+{
+    const int lo = __builtin_amdgcn_update_dpp(0, __double2loint(x), CTRL, ROW_MASK, 0xF, BOUND);
+    const int hi = __builtin_amdgcn_update_dpp(0, __double2hiint(x), CTRL, ROW_MASK, 0xF, BOUND);
+    return __hiloint2double(hi, lo);
+}
+
+__device__ __forceinline__ double wave_inclusive_sum64(double x)
+{
+    x += dpp_src64<0x111, 0xF, true>(x);
+    x += dpp_src64<0x112, 0xF, true>(x);
+    x += dpp_src64<0x114, 0xF, true>(x);
+    x += dpp_src64<0x118, 0xF, true>(x);
+    x += dpp_src64<0x142, 0xA, false>(x);
+    x += dpp_src64<0x143, 0xC, false>(x);
+    return x;
+}
+
+__device__ __forceinline__ double wave_shift_right64(double x)
+{
+    return dpp_src64<0x138, 0xF, true>(x);
+}
+
+__device__ __forceinline__ double readlane64(double x, int32_t l)
+{
+    return __hiloint2double(__builtin_amdgcn_readlane(__double2hiint(x), l),
+                            __builtin_amdgcn_readlane(__double2loint(x), l));
+}
+
+
 namespace {
 
 constexpr int kBlock = 256;

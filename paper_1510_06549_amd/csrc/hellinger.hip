@@ -15,7 +15,7 @@
 // slices' partial sums are added in slice order (deterministic) and
 // H = sqrt(max(0, 1 - BC)).
 //
-// "Re-ordered to align" is read as the one-to-one matching of topics with the
+// Reordering the topics to line up is read as the one-to-one matching of topics with the
 // least total distance.  That linear assignment problem is solved on the host
 // (shortest augmenting paths with row and column potentials, the Hungarian
 // method of Kuhn and Munkres in O(kp^2 kq)): each augmentation is a chain of

@@ -6,8 +6,10 @@
 // documents are independent and the result does not depend on scheduling.
 //
 // Lane l owns the KPL contiguous topics [l KPL, l KPL + KPL).  For each token
-// the wave loads its packed count row (n | t << 16)[g][w][.] and its
-// shadow-base row B[w][.] with coalesced 16-byte loads, two tokens ahead of
+// the wave loads its packed count row (n | t << 16)[g][w][.] -- or, for a
+// (group, word) pair with at most 255 tokens, the row's 16-bit copy
+// (n | t << 8), half the bytes -- and its
+// shadow-base row B[w][.] with coalesced vector loads, two tokens ahead of
 // use (three register sets rotate, so no copy ever waits on a load in
 // flight), and gathers the folded Stirling ratios (Q0, Q1) of every cell.  The
 // 2K unnormalised weights of the thesis's conditionals (Eq.
@@ -35,6 +37,8 @@ struct SampleArgs {
     const int32_t *zr_old;
     int32_t *zr_new;
     const int32_t *nt;
+    const uint16_t *nt16;
+    const uint8_t *tok_narrow;
     const int32_t *B;
     const uint16_t *B16;
     const int32_t *wide;
@@ -130,9 +134,10 @@ struct DocWave {
     int64_t gK, cb, end;
     int32_t *c_lds;
     float *f0_lds, *f1_lds, *a0_lds, *a1_lds;
-    // token stream: lane l holds the row index, packed state and uniform of
-    // token cb + l (lanes past the document's end repeat its last token)
-    int32_t gw_c, zr_c, out_c;
+    // token stream: lane l holds the row index, packed state, narrow-row flag
+    // and uniform of token cb + l (lanes past the document's end repeat its
+    // last token)
+    int32_t gw_c, zr_c, nar_c, out_c;
     float u_c;
 };
 
@@ -142,7 +147,8 @@ __device__ __forceinline__ void load_rows(const SampleArgs &A, const DocWave<KPL
 {
     const int32_t q = readlane(W.gw_c, x);
     const int64_t wrow = (int64_t)(q - W.gV) * A.Kp;
-    load_row<KPL>(R.n, A.nt + (int64_t)q * A.Kp, W.kbase, A.Kp);
+    // a narrow row as its 16-bit copy (half the bytes), widened at use
+    load_count_row<KPL>(R.n, A.nt, A.nt16, q, W.kbase, A.Kp, readlane(W.nar_c, x) != 0);
     if constexpr (WIDE)
         load_row<KPL>(reinterpret_cast<int32_t(&)[KPL]>(R.bw), A.B + wrow, W.kbase, A.Kp);
     else
@@ -160,20 +166,22 @@ __device__ __forceinline__ void load_stream(const SampleArgs &A, DocWave<KPL> &W
     const int64_t t = min(W.cb + W.lane, last);
     W.gw_c = A.gw[t];
     W.zr_c = A.zr_old[t];
+    W.nar_c = A.tok_narrow[t];
     const uint32_t xr = philox_x0(A.seed, (uint64_t)(W.cb + W.lane), A.sweep, kPurposeSample);
     W.u_c = (float)(xr >> 8) * (1.0f / 16777216.0f);
-    asm volatile("" ::"v"(W.gw_c), "v"(W.zr_c));
+    asm volatile("" ::"v"(W.gw_c), "v"(W.zr_c), "v"(W.nar_c));
 }
 
 // Token cb + x: sample it with the rows in `cur` and request the rows of the
 // token two places ahead into `fill`.
 template <int KPL, bool TRACE, bool WIDE>
 __device__ __forceinline__ void sample_token(const SampleArgs &A, DocWave<KPL> &W, int32_t x,
-                                             const Rows<KPL, WIDE> &cur, Rows<KPL, WIDE> &fill)
+                                             Rows<KPL, WIDE> &cur, Rows<KPL, WIDE> &fill)
 {
     constexpr int NO = 2 * KPL;  // outcomes per lane
     const int32_t lane = W.lane, kbase = W.kbase;
     const int64_t i = W.cb + x;
+    if (readlane(W.nar_c, x)) widen_cells<KPL>(cur.n, kbase);
 
     const int32_t zr0 = readlane(W.zr_c, x);
     const int32_t k0 = zr0 >> 1, r0 = zr0 & 1;
@@ -485,6 +493,8 @@ hipError_t launch_sample(const Model &m, const DeviceBuffers &b, const int32_t *
     A.zr_old = zr_old;
     A.zr_new = zr_new;
     A.nt = b.nt;
+    A.nt16 = b.nt16;
+    A.tok_narrow = b.tok_narrow;
     A.B = b.B;
     A.B16 = b.B16;
     A.wide = b.wide;

@@ -47,6 +47,8 @@ struct AssocArgs {
     const int32_t *zr_old;
     int32_t *zr_new;
     const int32_t *nt;
+    const uint16_t *nt16;
+    const uint8_t *tok_narrow;
     const int32_t *B;
     const uint16_t *B16;
     const int32_t *wide;
@@ -98,9 +100,9 @@ struct AWave {
     int32_t *c_lds;
     float *f0_lds, *f1_lds, *a0_lds, *a1_lds;
     // token stream: lane l holds token cb + l (lanes past the document's end
-    // repeat its last token): row index, packed state, uniform, and the
-    // source record of its row
-    int32_t gw_c, zr_c, out_c;
+    // repeat its last token): row index, packed state, narrow-row flag,
+    // uniform, and the source record of its row
+    int32_t gw_c, zr_c, nar_c, out_c;
     float u_c;
     int32_t src_c[SP];
     float p_c[SP];
@@ -150,7 +152,8 @@ __device__ __forceinline__ void load_arows(const AssocArgs &A, const AWave<KPL, 
                                            ARows<KPL, SP, WIDE> &R)
 {
     const int32_t q = readlane(W.gw_c, x);
-    load_row<KPL>(R.n, A.nt + (int64_t)q * A.Kp, W.kbase, A.Kp);
+    // a narrow row as its 16-bit copy (half the bytes), widened at use
+    load_count_row<KPL>(R.n, A.nt, A.nt16, q, W.kbase, A.Kp, readlane(W.nar_c, x) != 0);
 #pragma unroll
     for (int s = 0; s < SP; ++s) {
         const int64_t vrow = (int64_t)readlane(W.src_c[s], x) * A.Kp;
@@ -167,6 +170,7 @@ __device__ __forceinline__ void load_astream(const AssocArgs &A, AWave<KPL, SP> 
     const int64_t t = min(W.cb + W.lane, last);
     W.gw_c = A.gw[t];
     W.zr_c = A.zr_old[t];
+    W.nar_c = A.tok_narrow[t];
     const int32_t *rec = A.srcrec + (int64_t)W.gw_c * (2 * SP);
     if constexpr (SP == 1) {
         const int2 x = *reinterpret_cast<const int2 *>(rec);
@@ -192,7 +196,7 @@ __device__ __forceinline__ void load_astream(const AssocArgs &A, AWave<KPL, SP> 
     W.u_c = (float)(xr >> 8) * (1.0f / 16777216.0f);
 #pragma unroll
     for (int s = 0; s < SP; ++s) asm volatile("" ::"v"(W.src_c[s]), "v"(W.p_c[s]));
-    asm volatile("" ::"v"(W.gw_c), "v"(W.zr_c));
+    asm volatile("" ::"v"(W.gw_c), "v"(W.zr_c), "v"(W.nar_c));
 }
 
 // fp64 weights of topic k's SP + 1 outcomes from the integer counts (the
@@ -235,11 +239,12 @@ __device__ void exact_topic(const ExactCtx &X, int32_t k, int32_t k0, int32_t r0
 // next token into `fill`.
 template <int KPL, int SP, bool WIDE>
 __device__ __forceinline__ void sample_token_assoc(const AssocArgs &A, AWave<KPL, SP> &W,
-                                                   int32_t x, const ARows<KPL, SP, WIDE> &cur,
+                                                   int32_t x, ARows<KPL, SP, WIDE> &cur,
                                                    ARows<KPL, SP, WIDE> &fill)
 {
     const int32_t lane = W.lane, kbase = W.kbase;
     const int64_t i = W.cb + x;
+    if (readlane(W.nar_c, x)) widen_cells<KPL>(cur.n, kbase);
 
     const int32_t zr0 = readlane(W.zr_c, x);
     const int32_t k0 = zr_topic(zr0), r0 = zr0 & 1, s0 = zr_slot(zr0);
@@ -616,6 +621,8 @@ hipError_t launch_sample_assoc(const Model &m, const DeviceBuffers &b, const int
     A.zr_old = zr_old;
     A.zr_new = zr_new;
     A.nt = b.nt;
+    A.nt16 = b.nt16;
+    A.tok_narrow = b.tok_narrow;
     A.B = b.B;
     A.B16 = b.B16;
     A.wide = b.wide;

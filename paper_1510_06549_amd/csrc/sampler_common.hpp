@@ -99,6 +99,74 @@ __device__ __forceinline__ void load_half_row(uint32_t (&v)[(KPL + 1) / 2],
     }
 }
 
+// Start, relative to the lane's first topic, of the cells that chunk c of a
+// narrow row read brings (16-bit cells, 16-byte chunks hold eight of them;
+// chunks are loaded with the same instructions as a full row's, so a narrow
+// row repeats its first chunk of each pair, and with KPL = 12 the third
+// chunk holds cells 4 .. 11).
+template <int KPL>
+__device__ __forceinline__ constexpr int narrow_chunk_start(int c)
+{
+    return KPL == 12 ? (c == 2 ? 4 : 0) : 8 * (c / 2);
+}
+
+// This lane's cells of the count row of (group, word) q for the token loop:
+// the 32-bit cells (load_row), or, if `narrow` (wave-uniform), the 16-bit
+// copy, read with the same load instructions into the same registers so that
+// the loads in flight are the same on both paths; the copy's cells, two per
+// 32-bit word, are turned into 32-bit cells by widen_cells once they arrive.
+// A narrow read can run up to 8 cells past the lane's slice (into the next
+// lane's cells, the next row, or the 16-bit buffer's tail padding); chunks
+// that start past the row end read the row's first chunk, as in load_row.
+template <int KPL>
+__device__ __forceinline__ void load_count_row(int32_t (&v)[KPL], const int32_t *__restrict__ nt,
+                                               const uint16_t *__restrict__ nt16, int64_t q,
+                                               int32_t kbase, int32_t Kp, bool narrow)
+{
+    const char *row = narrow ? reinterpret_cast<const char *>(nt16 + q * Kp)
+                             : reinterpret_cast<const char *>(nt + q * Kp);
+    if constexpr (KPL % 4 == 0) {
+#pragma unroll
+        for (int c = 0; c < KPL / 4; ++c) {
+            const int32_t cw = kbase + 4 * c, cn = kbase + narrow_chunk_start<KPL>(c);
+            const int32_t off = narrow ? 2 * (cn < Kp ? cn : 0) : 4 * (cw < Kp ? cw : 0);
+            const int4 x = *reinterpret_cast<const int4 *>(row + off);
+            v[4 * c + 0] = x.x;
+            v[4 * c + 1] = x.y;
+            v[4 * c + 2] = x.z;
+            v[4 * c + 3] = x.w;
+        }
+    } else if constexpr (KPL == 2) {
+        const int32_t k = kbase < Kp ? kbase : 0;
+        const int2 x = *reinterpret_cast<const int2 *>(row + (narrow ? 2 * k : 4 * k));
+        v[0] = x.x;
+        v[1] = x.y;
+    } else {
+        static_assert(KPL == 1, "KPL must be 1, 2 or a multiple of 4");
+        const int32_t k = kbase < Kp ? kbase : 0;
+        v[0] = *reinterpret_cast<const int32_t *>(row + (narrow ? 2 * (k & ~1) : 4 * k));
+    }
+}
+
+// The cells of a narrow row read by load_count_row as packed n | t << 16
+// cells (KPL = 1 reads the aligned pair holding its cell).
+template <int KPL>
+__device__ __forceinline__ void widen_cells(int32_t (&v)[KPL], int32_t kbase)
+{
+    uint32_t w[KPL];
+#pragma unroll
+    for (int j = 0; j < KPL; ++j) w[j] = (uint32_t)v[j];
+#pragma unroll
+    for (int j = 0; j < KPL; ++j) {
+        int src;
+        if constexpr (KPL % 8 == 0) src = 8 * (j / 8) + (j % 8) / 2;
+        else if constexpr (KPL == 12) src = j < 8 ? j / 2 : 10 + (j - 8) / 2;
+        else src = j / 2;
+        const bool hi = (KPL == 1) ? (kbase & 1) != 0 : (j & 1) != 0;
+        v[j] = wide_of(hi ? (w[src] >> 16) : (w[src] & 0xFFFFu));
+    }
+}
+
 template <int KPL>
 __device__ __forceinline__ void load_slice_f(float (&s)[KPL], const float *__restrict__ row,
                                              int32_t kbase, int32_t Kp)
@@ -180,38 +248,6 @@ __device__ __forceinline__ float wave_inclusive_sum(float x)
 
 // value of lane - 1 (0 in lane 0)
 __device__ __forceinline__ float wave_shift_right(float x) { return dpp_src<0x138, 0xF, true>(x); }
-
-// The same for fp64 values: both 32-bit halves move with the same DPP control
-// (a disabled source gives 0 in both halves, i.e. +0.0).
-template <int CTRL, int ROW_MASK, bool BOUND>
-__device__ __forceinline__ double dpp_src64(double x)
-{
-    const int lo = __builtin_amdgcn_update_dpp(0, __double2loint(x), CTRL, ROW_MASK, 0xF, BOUND);
-    const int hi = __builtin_amdgcn_update_dpp(0, __double2hiint(x), CTRL, ROW_MASK, 0xF, BOUND);
-    return __hiloint2double(hi, lo);
-}
-
-__device__ __forceinline__ double wave_inclusive_sum64(double x)
-{
-    x += dpp_src64<0x111, 0xF, true>(x);
-    x += dpp_src64<0x112, 0xF, true>(x);
-    x += dpp_src64<0x114, 0xF, true>(x);
-    x += dpp_src64<0x118, 0xF, true>(x);
-    x += dpp_src64<0x142, 0xA, false>(x);
-    x += dpp_src64<0x143, 0xC, false>(x);
-    return x;
-}
-
-__device__ __forceinline__ double wave_shift_right64(double x)
-{
-    return dpp_src64<0x138, 0xF, true>(x);
-}
-
-__device__ __forceinline__ double readlane64(double x, int32_t l)
-{
-    return __hiloint2double(__builtin_amdgcn_readlane(__double2hiint(x), l),
-                            __builtin_amdgcn_readlane(__double2loint(x), l));
-}
 
 // Interleaved LDS rows: the KPL values of lane l sit in 16-byte chunks
 // (chunk c of lane l at (c * 64 + l) * 4), so a wave's vector read of one

@@ -69,6 +69,27 @@ __global__ void k_make_gw(int32_t D, int32_t V, int32_t G, const int32_t *__rest
     }
 }
 
+// ------------------------------------------------------------ narrow rows
+// A row is narrow if its (group, word) pair occurs at most kNarrowMax times:
+// no count of the row can then exceed kNarrowMax.
+__global__ void k_row_narrow(int64_t rows, const int32_t *__restrict__ gw_count,
+                             uint8_t *__restrict__ row_narrow, unsigned long long *__restrict__ n)
+{
+    const int64_t q = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    const bool nar = q < rows && gw_count[q] <= kNarrowMax;
+    if (q < rows) row_narrow[q] = nar ? 1 : 0;
+    const unsigned long long c = __popcll(__ballot(nar));
+    if ((threadIdx.x & 63) == 0 && c) atomicAdd(n, c);
+}
+
+__global__ void k_tok_narrow(int64_t N, const int32_t *__restrict__ gw,
+                             const uint8_t *__restrict__ row_narrow,
+                             uint8_t *__restrict__ tok_narrow)
+{
+    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i < N) tok_narrow[i] = row_narrow[gw[i]];
+}
+
 // --------------------------------------------------------------- max int32
 __global__ void k_max_i32(const int32_t *__restrict__ x, int64_t n, int32_t *__restrict__ out)
 {
@@ -403,10 +424,16 @@ hipError_t launch_unpack_zr(const Model &m, const int32_t *zr, int32_t *z, uint8
 
 hipError_t launch_totals(const Model &m, const DeviceBuffers &b, const int32_t *zr, hipStream_t st)
 {
+    return launch_totals_into(m, b, zr, b.Ngk, b.Tgk, b.Bk, st);
+}
+
+hipError_t launch_totals_into(const Model &m, const DeviceBuffers &b, const int32_t *zr,
+                              int32_t *Ngk, int32_t *Tgk, int32_t *Bk, hipStream_t st)
+{
     hipError_t e;
     const int64_t bins = (int64_t)m.G * m.Kp;
-    if ((e = fill(b.Ngk, bins, 0, st)) != hipSuccess) return e;
-    if ((e = fill(b.Tgk, bins, 0, st)) != hipSuccess) return e;
+    if ((e = fill(Ngk, bins, 0, st)) != hipSuccess) return e;
+    if ((e = fill(Tgk, bins, 0, st)) != hipSuccess) return e;
     if (m.N > 0) {
         // (if the queries fail, lds_max stays 0 and the global-atomic histogram runs)
         int dev = 0, lds_max = 0;
@@ -416,15 +443,28 @@ hipError_t launch_totals(const Model &m, const DeviceBuffers &b, const int32_t *
         if (lds <= lds_max && lds <= 96 * 1024) {
             const unsigned nb = (unsigned)blocks_for(m.N, kTotalsChunk);
             hipLaunchKernelGGL(k_totals_lds, dim3(nb), dim3(1024), (size_t)lds, st, m.N, m.Kp,
-                               (int32_t)bins, m.divV, b.gw, zr, b.Ngk, b.Tgk);
+                               (int32_t)bins, m.divV, b.gw, zr, Ngk, Tgk);
         } else {
             hipLaunchKernelGGL(k_totals_global, dim3((unsigned)blocks_for(m.N, kBlock)), dim3(kBlock),
-                               0, st, m.N, m.Kp, m.divV, b.gw, zr, b.Ngk, b.Tgk);
+                               0, st, m.N, m.Kp, m.divV, b.gw, zr, Ngk, Tgk);
         }
         if ((e = hipGetLastError()) != hipSuccess) return e;
     }
     hipLaunchKernelGGL(k_topic_tables, dim3((unsigned)blocks_for(m.Kp, kBlock)), dim3(kBlock), 0, st,
-                       m.G, m.Kp, b.Tgk, b.Bk);
+                       m.G, m.Kp, Tgk, Bk);
+    return hipGetLastError();
+}
+
+hipError_t launch_narrow_flags(const Model &m, const int32_t *gw, const int32_t *gw_count,
+                               uint8_t *row_narrow, uint8_t *tok_narrow,
+                               unsigned long long *n_narrow, hipStream_t st)
+{
+    const int64_t rows = (int64_t)m.G * m.V;
+    hipLaunchKernelGGL(k_row_narrow, dim3((unsigned)blocks_for(rows, kBlock)), dim3(kBlock), 0, st,
+                       rows, gw_count, row_narrow, n_narrow);
+    if (m.N > 0)
+        hipLaunchKernelGGL(k_tok_narrow, dim3((unsigned)blocks_for(m.N, kBlock)), dim3(kBlock), 0,
+                           st, m.N, gw, row_narrow, tok_narrow);
     return hipGetLastError();
 }
 

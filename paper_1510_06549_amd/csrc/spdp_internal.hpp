@@ -87,6 +87,22 @@ __host__ __device__ __forceinline__ int64_t tri_index(int64_t n, int64_t t)
 // ---------------------------------------------------------------------------
 constexpr int32_t kCountBits = 16;
 constexpr int32_t kCountMax = (1 << kCountBits) - 1;  // largest n a packed cell holds
+
+// Narrow rows.  A (group, word) pair with at most kNarrowMax tokens in the
+// corpus can never have a count above kNarrowMax in any state (n[g][k][w] <=
+// c[g][w]), so its row also exists as 16-bit cells n | t << 8, half the
+// bytes, which the sampler reads instead.  Which rows are narrow is fixed at
+// creation; the rebuild writes both copies of a narrow row.
+constexpr int32_t kNarrowMax = 255;
+__host__ __device__ __forceinline__ uint16_t narrow_of(int32_t packed)
+{
+    return (uint16_t)((packed & 0xFF) | ((packed >> kCountBits) << 8));
+}
+__host__ __device__ __forceinline__ int32_t wide_of(uint32_t cell16)
+{
+    return (int32_t)((cell16 & 0xFFu) | ((cell16 & 0xFF00u) << 8));
+}
+
 struct Model {
     int64_t N;
     int32_t D, V, G, K, Kp;
@@ -119,6 +135,9 @@ struct DeviceBuffers {
     int32_t *doc_group = nullptr; // [D]
     int32_t *zr[2] = {nullptr, nullptr}; // [N] current / next packed state
     int32_t *nt = nullptr;        // [G V][Kp] packed n | t << 16
+    uint16_t *nt16 = nullptr;     // [G V][Kp] narrow rows as n | t << 8 (other rows unused)
+    uint8_t *row_narrow = nullptr; // [G V] 1 if row q is narrow (c[g][w] <= kNarrowMax)
+    uint8_t *tok_narrow = nullptr; // [N] row_narrow of each token's row (the sampler's stream)
     int32_t *B = nullptr;         // [V][Kp]   shadow-base table counts
     uint16_t *B16 = nullptr;      // [V][Kp]   min(B, 65535): the sampler's copy
     int32_t *wide = nullptr;      // [1] 1 if some B exceeds 65535 (the sampler then reads B)
@@ -172,6 +191,11 @@ hipError_t launch_make_gw(const Model &m, const int32_t *words, const int64_t *d
                           const int32_t *doc_group, int32_t *gw, int32_t *gw_count,
                           int32_t *bad, hipStream_t st);
 hipError_t launch_max_i32(const int32_t *x, int64_t n, int32_t *out, hipStream_t st);
+// narrow-row flags from the per-row token counts: per row and per token; the
+// number of narrow rows is added to *n_narrow
+hipError_t launch_narrow_flags(const Model &m, const int32_t *gw, const int32_t *gw_count,
+                               uint8_t *row_narrow, uint8_t *tok_narrow,
+                               unsigned long long *n_narrow, hipStream_t st);
 hipError_t launch_stirling(const Model &m, double *logS, float2 *Q, double2 *Q64, double *lfact,
                            hipStream_t st);
 hipError_t launch_init_z(const Model &m, uint64_t seed, int32_t *zr, hipStream_t st);
@@ -194,11 +218,19 @@ hipError_t launch_pack_zrs(const Model &m, const DeviceBuffers &b, const int32_t
 hipError_t launch_unpack_slot(const Model &m, const int32_t *zr, uint8_t *s, hipStream_t st);
 hipError_t launch_unpack_counts(const Model &m, const DeviceBuffers &b, int32_t g,
                                 int32_t *n_out, int32_t *t_out, hipStream_t st);
+// invariant check of the count state (count rows against a recount of the
+// tokens' states, both copies of narrow rows, the shadow base, the totals):
+// the number of failing cells or totals is added to *bad
+hipError_t launch_check(const Model &m, const DeviceBuffers &b, const int32_t *zr,
+                        int32_t *scratch_totals, unsigned long long *bad, hipStream_t st);
 hipError_t launch_stat_sums(const Model &m, const DeviceBuffers &b, const int32_t *zr_now,
                             const int32_t *zr_before, hipStream_t st);
 int64_t stat_partials_needed();
 hipError_t launch_totals(const Model &m, const DeviceBuffers &b, const int32_t *zr,
                          hipStream_t st);
+// the same into other arrays (N, T: [G][Kp], Bk: [Kp])
+hipError_t launch_totals_into(const Model &m, const DeviceBuffers &b, const int32_t *zr,
+                              int32_t *Ngk, int32_t *Tgk, int32_t *Bk, hipStream_t st);
 hipError_t launch_factors(const Model &m, const DeviceBuffers &b, hipStream_t st);
 hipError_t launch_sample(const Model &m, const DeviceBuffers &b, const int32_t *zr_old,
                          int32_t *zr_new, uint32_t sweep, uint64_t seed, float *tr_w,

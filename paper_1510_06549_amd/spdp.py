@@ -33,7 +33,7 @@ EXPORTS = (
     "spdp_kernel_timing", "spdp_kernel_times", "spdp_info", "spdp_last_error",
     "spdp_estimates", "spdp_heldout", "spdp_hellinger", "spdp_align_topics",
     "spdp_create_assoc", "spdp_get_slots", "spdp_set_assignments_assoc", "spdp_max_sources",
-    "spdp_sweep_async", "spdp_read_probe",
+    "spdp_sweep_async", "spdp_read_probe", "spdp_check", "spdp_debug_poke",
 )
 
 
@@ -124,6 +124,10 @@ def load_library() -> C.CDLL:
     L.spdp_max_sources.restype = cint
     L.spdp_sweep_async.argtypes = [vp, u32, u64, i32, i32]
     L.spdp_sweep_async.restype = cint
+    L.spdp_check.argtypes = [vp, C.POINTER(i64)]
+    L.spdp_check.restype = cint
+    L.spdp_debug_poke.argtypes = [vp, i32, i32, i32, i32, i32]
+    L.spdp_debug_poke.restype = cint
     return L
 
 
@@ -305,6 +309,21 @@ def spdp_read_probe(buf_ptr: int, nbytes: int, row_bytes: int = 0, rows: int = 0
     return ms.value
 
 
+def spdp_check(h):
+    """Number of failing cells, tokens and totals; raises SpdpError
+    (SPDP_E_STATE) if there is any."""
+    bad = C.c_int64(0)
+    rc = lib().spdp_check(h, C.byref(bad))
+    if rc == SPDP_E_STATE:
+        raise SpdpError(rc, spdp_last_error())
+    _check(rc)
+    return int(bad.value)
+
+
+def spdp_debug_poke(h, g, w, k, dn, dt):
+    _check(lib().spdp_debug_poke(h, int(g), int(w), int(k), int(dn), int(dt)))
+
+
 def spdp_info(h) -> dict:
     out = np.zeros(8, dtype=np.int64)
     _check(lib().spdp_info(h, out.ctypes.data))
@@ -416,9 +435,9 @@ class Sampler:
         return s
 
     def counts(self, g_begin=0, g_end=None):
-        """n, t as [g][w][k] int32 arrays."""
+        """n, t as [g][k][w] int32 arrays."""
         g_end = self.G if g_end is None else g_end
-        n = np.empty((g_end - g_begin, self.V, self.K), dtype=np.int32)
+        n = np.empty((g_end - g_begin, self.K, self.V), dtype=np.int32)
         t = np.empty_like(n)
         spdp_counts(self.h, g_begin, g_end, n, t)
         return n, t
@@ -433,6 +452,12 @@ class Sampler:
 
     def loglik(self):
         return spdp_loglik(self.h)
+
+    def check(self):
+        return spdp_check(self.h)
+
+    def poke(self, g, w, k, dn, dt):
+        spdp_debug_poke(self.h, g, w, k, dn, dt)
 
     def conditionals(self, sweep, seed, tok_begin, tok_end):
         T = tok_end - tok_begin

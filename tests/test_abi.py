@@ -69,6 +69,8 @@ def test_null_state_is_an_argument_error():
     L = sp.lib()
     assert L.spdp_sweep(None, 0, 0) == sp.SPDP_E_ARG
     assert L.spdp_stats(None, None, None) == sp.SPDP_E_ARG
+    assert L.spdp_check(None, None) == sp.SPDP_E_ARG
+    assert L.spdp_debug_poke(None, 0, 0, 0, 1, 0) == sp.SPDP_E_ARG
     L.spdp_destroy(None)  # NULL is ignored
 
 

@@ -51,8 +51,8 @@ def test_largest_workload_with_associations():
     assert np.array_equal(B, c.Bkw.T) and np.array_equal(Bk, c.Bk)
     for g in (0, cp.n_groups - 1):
         n_g, t_g = s.counts(g, g + 1)
-        assert np.array_equal(n_g[0], c.n[g].T), f"n of group {g}"
-        assert np.array_equal(t_g[0], c.t[g].T), f"t of group {g}"
+        assert np.array_equal(n_g[0], c.n[g]), f"n of group {g}"
+        assert np.array_equal(t_g[0], c.t[g]), f"t of group {g}"
     del n_g, t_g
 
     sweep = 1

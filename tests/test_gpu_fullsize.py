@@ -26,18 +26,24 @@ def say(*a):
     print(*a, flush=True)
 
 
-def test_largest_workload_sampled_parity():
+@pytest.mark.parametrize("warm", [1, 25])
+def test_largest_workload_sampled_parity(warm):
+    """warm = 1: the sweep after one warm-up sweep; warm = 25: the sweep after
+    the benchmark's 5 warm-up and 20 timed sweeps (same seed and sweep
+    numbers), the state the benchmark measures; there the joint is checked
+    too (Eq. SPDP-Blocked-Gibbs-Joint-Prob, P = I)."""
     import torch
 
     wl = synth.workload("g20-d50000-k500")
-    say(f"full-size parity, workload {wl.name}: generating corpus")
+    say(f"full-size parity, workload {wl.name}, after {warm} sweep(s): generating corpus")
     cp = synth.generate(wl, 0)
     s = parity.sp.Sampler(cp.words, cp.doc_off, cp.doc_group, cp.n_groups, wl.vocab, wl.K,
                           wl.alpha, wl.a, wl.b, wl.gamma, init_seed=0,
                           hip_stream=torch.cuda.current_stream().cuda_stream)
     seed = 1000
-    say("  warm-up sweep")
-    s.sweep(0, seed)
+    say(f"  {warm} warm-up sweep(s)")
+    for sw in range(warm):
+        s.sweep(sw, seed)
     z, r = s.assignments()
     say("  oracle model and dense rebuild")
     m = oracle.Model(cp.words, cp.doc_off, cp.doc_group, cp.n_groups, wl.K, wl.vocab, wl.alpha,
@@ -52,12 +58,18 @@ def test_largest_workload_sampled_parity():
     assert np.array_equal(B, c.Bkw.T) and np.array_equal(Bk, c.Bk)
     for g in (0, cp.n_groups - 1):
         n_g, t_g = s.counts(g, g + 1)
-        assert np.array_equal(n_g[0], c.n[g].T), f"n of group {g}"
-        assert np.array_equal(t_g[0], c.t[g].T), f"t of group {g}"
+        assert np.array_equal(n_g[0], c.n[g]), f"n of group {g}"
+        assert np.array_equal(t_g[0], c.t[g]), f"t of group {g}"
     del n_g, t_g
+    if warm > 1:
+        say("  joint of the library's state against the oracle's")
+        ll_g = s.loglik()
+        ll_o = m.loglik(z, r, c)
+        say(f"    library {ll_g!r} oracle {ll_o!r} rel {abs(ll_g - ll_o) / abs(ll_o):.3e}")
+        assert abs(ll_g - ll_o) <= parity.LL_RTOL * abs(ll_o)
 
     # sampled documents, one by one against the oracle
-    sweep = 1
+    sweep = warm
     zo, ro = z.copy(), r.copy()
     for d0 in (0, m.D // 2 + 7, m.D - 150):
         d1 = d0 + 150

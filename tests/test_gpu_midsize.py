@@ -24,18 +24,23 @@ def say(*a):
     print(*a, flush=True)
 
 
-def test_midsize_workload_every_draw():
+@pytest.mark.parametrize("warm,seed", [(1, 4321), (25, 1000)])
+def test_midsize_workload_every_draw(warm, seed):
+    """warm = 1: the sweep after one warm-up sweep; warm = 25: the sweep after
+    the benchmark's schedule of 5 warm-up and 20 timed sweeps (its seed).
+    The joint (Eq. SPDP-Blocked-Gibbs-Joint-Prob, P = I) is compared before
+    and after the compared sweep."""
     import torch
 
     wl = synth.workload("g10-d20000-k200")
-    say(f"mid-size parity, workload {wl.name}: generating corpus")
+    say(f"mid-size parity, workload {wl.name}, after {warm} sweep(s): generating corpus")
     cp = synth.generate(wl, 0)
     s = parity.sp.Sampler(cp.words, cp.doc_off, cp.doc_group, cp.n_groups, wl.vocab, wl.K,
                           wl.alpha, wl.a, wl.b, wl.gamma, init_seed=0,
                           hip_stream=torch.cuda.current_stream().cuda_stream)
-    seed = 4321
-    say("  warm-up sweep")
-    s.sweep(0, seed)
+    say(f"  {warm} warm-up sweep(s)")
+    for sw in range(warm):
+        s.sweep(sw, seed)
     z, r = s.assignments()
     say("  oracle model and dense rebuild")
     m = oracle.Model(cp.words, cp.doc_off, cp.doc_group, cp.n_groups, wl.K, wl.vocab, wl.alpha,
@@ -49,11 +54,14 @@ def test_midsize_workload_every_draw():
     assert np.array_equal(B, c.Bkw.T) and np.array_equal(Bk, c.Bk)
     for g in (0, cp.n_groups - 1):
         n_g, t_g = s.counts(g, g + 1)
-        assert np.array_equal(n_g[0], c.n[g].T), f"n of group {g}"
-        assert np.array_equal(t_g[0], c.t[g].T), f"t of group {g}"
+        assert np.array_equal(n_g[0], c.n[g]), f"n of group {g}"
+        assert np.array_equal(t_g[0], c.t[g]), f"t of group {g}"
     del n_g, t_g
+    ll_g, ll_o = s.loglik(), m.loglik(z, r, c)
+    say(f"  joint: library {ll_g!r} oracle {ll_o!r}")
+    assert abs(ll_g - ll_o) <= parity.LL_RTOL * abs(ll_o)
 
-    sweep = 1
+    sweep = warm
     say("  every token: library draws vs the oracle's sampling step")
     zr_pre = s.sampled(sweep, seed)
     zg, rg = (zr_pre >> 1).astype(np.int32), (zr_pre & 1).astype(np.uint8)
@@ -95,4 +103,7 @@ def test_midsize_workload_every_draw():
     N, T, B, Bk = s.totals()
     assert np.array_equal(N, c2.Ngk) and np.array_equal(T, c2.Tgk)
     assert np.array_equal(B, c2.Bkw.T) and np.array_equal(Bk, c2.Bk)
+    ll_g, ll_o = s.loglik(), m.loglik(zs, rs, c2)
+    say(f"  joint after the sweep: library {ll_g!r} oracle {ll_o!r}")
+    assert abs(ll_g - ll_o) <= parity.LL_RTOL * abs(ll_o)
     s.close()

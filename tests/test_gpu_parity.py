@@ -48,7 +48,31 @@ def test_sweeps_parity(corpora, idx, sweeps):
     s.close()
 
 
-@pytest.mark.parametrize("idx", [0, 1])
+def test_late_sweeps_parity_g4(corpora):
+    """The per-sweep protocol on the 3M-token workload at sweeps 0, 1, 50 and
+    99 of a 100-sweep run (the sweeps between run on the library only), with
+    the joint compared before each of them and at the end."""
+    wl = synth.workload(2)
+    cp = corpora[2]
+    s, m = parity.make_pair(cp, wl, init_seed=1)
+    seed = 2026
+    for sw in range(100):
+        if sw in (0, 1, 50, 99):
+            z, r = s.assignments()
+            ll_g, ll_o = s.loglik(), m.loglik(z, r, m.rebuild(z, r))
+            say(f"sweep parity, workload {wl.name}, sweep {sw}: joint {ll_g!r} / {ll_o!r}")
+            assert abs(ll_g - ll_o) <= parity.LL_RTOL * abs(ll_o)
+            rep, changed, repaired = parity.one_step(s, m, sw, seed)
+            say(f"  {rep} changed={changed} repaired={repaired}")
+        else:
+            s.sweep(sw, seed)
+    z, r = s.assignments()
+    ll_g, ll_o = s.loglik(), m.loglik(z, r, m.rebuild(z, r))
+    assert abs(ll_g - ll_o) <= parity.LL_RTOL * abs(ll_o)
+    s.close()
+
+
+@pytest.mark.parametrize("idx", [0, 1, 2])
 def test_loglik_parity(corpora, idx):
     wl = synth.workload(idx)
     say(f"loglik parity, workload {wl.name}")
@@ -60,7 +84,7 @@ def test_loglik_parity(corpora, idx):
         ll_o = m.loglik(z, r, c)
         ll_g = s.loglik()
         say(f"  sweep {sw}: gpu {ll_g!r} oracle {ll_o!r}")
-        assert abs(ll_g - ll_o) <= 1e-6 * abs(ll_o)
+        assert abs(ll_g - ll_o) <= parity.LL_RTOL * abs(ll_o)
         s.sweep(sw, 77)
     # generator truth through set_assignments
     s.set_assignments(cp.z_true, cp.r_true)
