@@ -44,13 +44,25 @@ def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
-def sample_bytes_per_token(K: int, wide: bool) -> int:
+def narrow_fraction(cp) -> float:
+    """Share of tokens whose (group, word) pair occurs at most 255 times: the
+    sampler reads those tokens' count rows as 16-bit cells (n | t << 8, half
+    the bytes).  A pure function of the corpus."""
+    import numpy as np
+
+    q = np.repeat(cp.doc_group, np.diff(cp.doc_off)).astype(np.int64) * cp.vocab + cp.words
+    c = np.bincount(q)
+    return float(np.mean(c[q] <= 255)) if len(q) else 0.0
+
+
+def sample_bytes_per_token(K: int, wide: bool, narrow: float = 0.0) -> float:
     """Bytes the sampling kernel must move per token in this library's layout:
     the K-cell count row of (group, word) (customers and tables packed in one
-    int32 per cell), the K-entry shadow-base row of the word (16-bit counts,
-    or int32 once some count exceeds 65535), and the token stream (row index
-    and state in, state out)."""
-    return 4 * K + (4 if wide else 2) * K + 12
+    int32 per cell, or in 16 bits for the share `narrow` of tokens whose pair
+    occurs at most 255 times), the K-entry shadow-base row of the word (16-bit
+    counts, or int32 once some count exceeds 65535), and the token stream
+    (row index, state and narrow-row flag in, state out)."""
+    return (4 - 2 * narrow) * K + (4 if wide else 2) * K + 13
 
 
 def assoc_bytes_per_token(K: int, wide: bool, mean_sources: float, Sp: int) -> float:
@@ -81,16 +93,25 @@ def dense_bytes_per_token(K: int) -> int:
     return 12 * K + 12
 
 
+def kernel_source_hash(kernel: str) -> str:
+    """SHA-256 of the sources a sampling kernel is compiled from: its own file,
+    then the two headers that file includes."""
+    import hashlib
+
+    csrc = os.path.join(ROOT, "paper_1510_06549_amd", "csrc")
+    source = {"k_sample": "sample.hip", "k_sample_assoc": "sample_assoc.hip"}[kernel]
+    h = hashlib.sha256()
+    for name in (source, "sampler_common.hpp", "spdp_internal.hpp"):
+        h.update(open(os.path.join(csrc, name), "rb").read())
+    return h.hexdigest()
+
+
 def recorded_traffic(kernel: str, workload: str):
     """HBM bytes per launch of the sampling kernel measured with rocprofv3
     counters, if they were taken on the current source of that kernel
-    (profiles/traffic_<kernel>_<workload>.txt holds the figure with the
-    SHA-256 of the kernel's source followed by sampler_common.hpp at the
-    time), else None."""
-    import hashlib
-
+    (profiles/traffic_<kernel>_<workload>.txt holds the figure with
+    kernel_source_hash() at the time), else None."""
     path = os.path.join(ROOT, "profiles", f"traffic_{kernel}_{workload}.txt")
-    csrc = os.path.join(ROOT, "paper_1510_06549_amd", "csrc")
     if not os.path.exists(path):
         return None
     kv = {}
@@ -98,18 +119,24 @@ def recorded_traffic(kernel: str, workload: str):
         if ":" in line and not line.startswith("#"):
             k, v = line.split(":", 1)
             kv[k.strip()] = v.strip()
-    source = {"k_sample": "sample.hip", "k_sample_assoc": "sample_assoc.hip"}[kernel]
-    h = hashlib.sha256()
-    for name in (source, "sampler_common.hpp"):
-        h.update(open(os.path.join(csrc, name), "rb").read())
-    if kv.get("source_sha256") != h.hexdigest() or "bytes_per_launch" not in kv:
+    if kv.get("source_sha256") != kernel_source_hash(kernel) or "bytes_per_launch" not in kv:
         return None
     return float(kv["bytes_per_launch"])
 
 
-def cpu_baseline(cp, wl, state, target_s: float, assoc=None):
-    """The oracle's sampling step timed on the host cores over a bounded
-    sample of documents; state = (z, r) or (z, r, slot) with assoc."""
+def cpu_baseline(cp, wl, state, target_s: float, assoc=None, full_sweeps: int = 0,
+                 seed: int = 0):
+    """The oracle's whole sweep (sampling step, count rebuild, repair) timed on
+    the host cores, from the library's state = (z, r) or (z, r, slot).
+
+    full_sweeps = 0 (a bounded sample, about target_s + the rebuild): the
+    sampling step over the first documents, sized to about target_s, against
+    the sweep-start counts, and the count rebuild and repair of the whole
+    corpus, timed once; the sweep's time is the sampling time scaled to all
+    tokens plus the rebuild and repair time.  full_sweeps = S > 0: S whole
+    sweeps of the oracle from the state, timed.  Both on all host threads and
+    on one thread (one thread: whole sweeps only if they take at most two
+    minutes, else the bounded sample)."""
     import numpy as np
 
     import oracle
@@ -121,41 +148,74 @@ def cpu_baseline(cp, wl, state, target_s: float, assoc=None):
     c = m.rebuild(*state)
     log(f"[bench] oracle model + dense counts ready in {time.time() - t0:.1f}s")
     threads = oracle.num_threads()
-    # calibrate on a few documents, then size the sample to about target_s
+    N = m.N
+
+    def rebuild_repair():
+        st = [x.copy() for x in state]
+        t = time.perf_counter()
+        c2 = m.rebuild(*st, counts=c)
+        m.repair(*st, c2)
+        return time.perf_counter() - t
+
+    def sampled(seconds, per_tok):
+        """(tokens, seconds) of the sampling step over the first documents,
+        sized to about `seconds`."""
+        want = int(seconds / per_tok)
+        d = max(1, min(int(np.searchsorted(m.doc_off, want)), m.D))
+        t = time.perf_counter()
+        m.sample_docs(c, *[x.copy() for x in state], 0, 1, 0, d)
+        return int(m.doc_off[d]), time.perf_counter() - t, d
+
+    def whole_sweeps(n):
+        st = [x.copy() for x in state]
+        cc = m.rebuild(*st)
+        t = time.perf_counter()
+        for k in range(n):
+            m.sweep(cc, *st, k, 1000 + seed)
+        return (time.perf_counter() - t) / n
+
+    # calibration: a few documents
     d_cal = min(2048, m.D)
-    t0 = time.perf_counter()
+    t = time.perf_counter()
     m.sample_docs(c, *[x.copy() for x in state], 0, 1, 0, d_cal)
-    dt = max(time.perf_counter() - t0, 1e-6)
-    tok_cal = int(m.doc_off[d_cal])
-    per_tok = dt / max(tok_cal, 1)
-    want_tok = int(target_s / per_tok)
-    d_s = int(np.searchsorted(m.doc_off, want_tok))
-    d_s = max(d_cal, min(d_s, m.D))
-    t0 = time.perf_counter()
-    m.sample_docs(c, *[x.copy() for x in state], 0, 1, 0, d_s)
-    dt = time.perf_counter() - t0
-    toks = int(m.doc_off[d_s])
-    # the same step on one thread, over a sample a fifth as long in time
+    per_tok = max(time.perf_counter() - t, 1e-6) / max(int(m.doc_off[d_cal]), 1)
+    t_rr = rebuild_repair()  # serial: the same on one thread
+    if full_sweeps > 0:
+        t_sweep = whole_sweeps(full_sweeps)
+        desc = (f"{full_sweeps} whole oracle sweep(s) (sampling step of all {N} tokens, count "
+                f"rebuild, repair), fp64, OpenMP over documents: {t_sweep:.2f}s per sweep")
+    else:
+        toks, dt, d = sampled(target_s, per_tok)
+        t_sweep = dt * N / max(toks, 1) + t_rr
+        desc = (f"sampling step of the first {d} documents ({toks} tokens, {dt:.1f}s) against "
+                f"the full sweep-start counts, scaled to all {N} tokens, plus the count rebuild "
+                f"and repair of the whole corpus ({t_rr:.1f}s); fp64, OpenMP over documents")
     oracle.set_num_threads(1)
     try:
-        want1 = int(target_s / 5 / (per_tok * threads))
-        d_1 = max(1, min(int(np.searchsorted(m.doc_off, want1)), m.D))
-        t0 = time.perf_counter()
-        m.sample_docs(c, *[x.copy() for x in state], 0, 1, 0, d_1)
-        dt1 = time.perf_counter() - t0
+        t = time.perf_counter()
+        m.sample_docs(c, *[x.copy() for x in state], 0, 1, 0, d_cal)
+        per_tok1 = max(time.perf_counter() - t, 1e-6) / max(int(m.doc_off[d_cal]), 1)
+        if full_sweeps > 0 and full_sweeps * (per_tok1 * N + t_rr) <= 120.0:
+            t_sweep1 = whole_sweeps(full_sweeps)
+            desc1 = f"{full_sweeps} whole oracle sweep(s) on one thread: {t_sweep1:.2f}s per sweep"
+        else:
+            toks1, dt1, d1 = sampled(target_s / 5, per_tok1)
+            t_sweep1 = dt1 * N / max(toks1, 1) + t_rr
+            desc1 = (f"sampling step of the first {d1} documents ({toks1} tokens, {dt1:.1f}s) on "
+                     f"one thread, scaled to all tokens, plus the rebuild and repair "
+                     f"({t_rr:.1f}s)")
     finally:
         oracle.set_num_threads(threads)
-    toks1 = int(m.doc_off[d_1])
     return {
-        "value": toks / dt,
+        "value": N / t_sweep,
         "unit": "tokens/s",
         "cores": threads,
         "kind": "oracle",
-        "sample": (f"sampling step of the first {d_s} documents ({toks} tokens) against the full "
-                   f"sweep-start counts, fp64, OpenMP over documents, {dt:.1f}s; count rebuild "
-                   f"excluded"),
-        "value_1thread": toks1 / dt1,
-        "sample_1thread": f"the first {d_1} documents ({toks1} tokens), {dt1:.1f}s",
+        "sample": desc,
+        "s_per_sweep": round(t_sweep, 4),
+        "value_1thread": N / t_sweep1,
+        "s_per_sweep_1thread": round(t_sweep1, 4),
+        "sample_1thread": desc1,
         "host_cpu": host_cpu(),
     }
 
@@ -322,6 +382,8 @@ def main():
     ap.add_argument("--no-read-probe", action="store_true",
                     help="skip the read-bandwidth probe reported beside the roofline")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--cpu-sweeps", type=int, default=0,
+                    help="time this many whole oracle sweeps instead of a bounded sample")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="also run a plain device copy of this size (counter calibration)")
     ap.add_argument("--assoc", type=int, default=0,
@@ -424,7 +486,8 @@ def main():
         bpt = async_bytes_per_token(wl.K)
         traffic = None
     elif assoc is None:
-        bpt = sample_bytes_per_token(wl.K, wide)
+        narrow = narrow_fraction(cp)
+        bpt = sample_bytes_per_token(wl.K, wide, narrow)
         traffic = recorded_traffic("k_sample", wl.name)
     else:
         # mean length of the source list of each token's row
@@ -455,6 +518,7 @@ def main():
     if args.async_sweep:
         pass
     elif assoc is None:
+        roofline["narrow_row_token_share"] = round(narrow, 4)
         roofline["dense_int32_bytes_per_token"] = dense_bytes_per_token(wl.K)
         roofline["dense_int32_equiv_GBps"] = round(
             N * dense_bytes_per_token(wl.K) / avg_sample_s / 1e9, 1)
@@ -468,7 +532,7 @@ def main():
     if not args.no_cpu_baseline:
         state = s.assignments() + ((s.slots(),) if assoc is not None else ())
         s.close()
-        cpu = cpu_baseline(cp, wl, state, args.cpu_seconds, assoc)
+        cpu = cpu_baseline(cp, wl, state, args.cpu_seconds, assoc, args.cpu_sweeps, args.seed)
         log(f"[bench] cpu baseline {cpu}")
     else:
         s.close()
