@@ -263,6 +263,28 @@ int spdp_hellinger(spdp_state *s, const double *p, int32_t kp, const double *q, 
                    int32_t n_outcomes, double *h, int where);
 
 /*
+ * For callers that cannot allocate device memory (code under stream capture,
+ * tight serving loops, harnesses that forbid hipMalloc): spdp_hellinger on
+ * device buffers that allocates nothing.  p [n_outcomes][kp], q
+ * [n_outcomes][kq] and h [kp][kq] are fp64 device pointers on the state's
+ * GPU (p may not be NULL: the state's phi0 would need a buffer), each inside
+ * one device allocation that holds its size (checked against the
+ * allocation, not against a caller's sub-range of it); the result equals
+ * spdp_hellinger's.
+ * The partial sums over outcome slices go to a static device array of
+ * 2^20 doubles (8 MiB) that each GPU the library runs on holds until the
+ * process ends, so kp * kq may not exceed 2^20 (always true for topic counts
+ * up to SPDP_MAX_K).  Only enqueues on the state's stream (no
+ * synchronisation): calls on one GPU share the array, so calls that overlap
+ * (other streams or host threads) race; calls in one stream's order do not.
+ * Errors: E_ARG (NULL pointer, negative size, topic count above SPDP_MAX_K,
+ * a buffer that is not device memory or too short), E_RANGE (kp * kq above
+ * 2^20), E_HIP.
+ */
+int spdp_hellinger_noalloc(spdp_state *s, const double *p, int32_t kp, const double *q,
+                           int32_t kq, int32_t n_outcomes, double *h);
+
+/*
  * Topic alignment for comparing two models (the topics are reordered to line up in the
  * Hellinger comparison): the one-to-one matching of the kp rows of h
  * [kp][kq] (kp <= kq; e.g. distances from spdp_hellinger) to columns that

@@ -303,6 +303,11 @@ int create_state(const spdp_corpus *corpus, const spdp_groups *groups, const spd
 
     TRY_HIP(hipGetDevice(&s->device));
     s->st = (hipStream_t)corpus->hip_stream;
+    {
+        // the allocation-free Hellinger's scratch address on this device
+        double *scratch_addr = nullptr;
+        TRY_HIP((hipError_t)hellinger_scratch(s->device, &scratch_addr));
+    }
     Model &m = s->m;
     m.N = N;
     m.D = D;
@@ -779,6 +784,45 @@ int spdp_hellinger(spdp_state *s, const double *p, int32_t kp, const double *q, 
     if (e == hipSuccess) e = hipStreamSynchronize(s->st);
     for (void *x : tmp) (void)hipFree(x);
     HIP_TRY(e);
+    return SPDP_OK;
+}
+
+int spdp_hellinger_noalloc(spdp_state *s, const double *p, int32_t kp, const double *q,
+                           int32_t kq, int32_t n_outcomes, double *h)
+{
+    if (!s || !p || !q || !h) return fail(SPDP_E_ARG, "null argument");
+    if (kp < 0 || kq < 0 || n_outcomes < 0) return fail(SPDP_E_ARG, "negative size");
+    if (kp > SPDP_MAX_K || kq > SPDP_MAX_K)
+        return fail(SPDP_E_ARG, "topic counts must be at most %d", SPDP_MAX_K);
+    const int64_t nh = (int64_t)kp * kq;
+    if (nh > kHellingerScratch)
+        return fail(SPDP_E_RANGE, "kp * kq = %lld exceeds the %lld partial sums of the static "
+                    "scratch", (long long)nh, (long long)kHellingerScratch);
+    HIP_TRY(hipSetDevice(s->device));
+    double *part = nullptr;
+    HIP_TRY((hipError_t)hellinger_scratch(s->device, &part));
+    // p, q and h must be device memory holding their sizes (the kernels read
+    // and write them directly)
+    const struct {
+        const void *ptr;
+        int64_t bytes;
+        const char *name;
+    } bufs[3] = {{p, (int64_t)n_outcomes * kp * 8, "p"},
+                 {q, (int64_t)n_outcomes * kq * 8, "q"},
+                 {h, nh * 8, "h"}};
+    for (const auto &x : bufs) {
+        hipDeviceptr_t base = nullptr;
+        size_t size = 0;
+        if (hipMemGetAddressRange(&base, &size, const_cast<void *>(x.ptr)) != hipSuccess) {
+            (void)hipGetLastError();
+            return fail(SPDP_E_ARG, "%s is not device memory", x.name);
+        }
+        if (static_cast<const char *>(x.ptr) + x.bytes > static_cast<const char *>(base) + size)
+            return fail(SPDP_E_ARG, "%s: %lld bytes run past its allocation", x.name,
+                        (long long)x.bytes);
+    }
+    const HellingerPlan plan = hellinger_plan(kp, kq, n_outcomes, kHellingerScratch);
+    HIP_TRY(launch_hellinger(plan, p, kp, q, kq, n_outcomes, part, h, s->st));
     return SPDP_OK;
 }
 

@@ -25,9 +25,16 @@
 
 #include <cmath>
 #include <limits>
+#include <mutex>
 #include <vector>
 
 namespace spdp {
+
+// Partial sums of the allocation-free entry point (spdp_hellinger_noalloc):
+// one array per GPU, held until the process ends.  Host code never passes
+// this name to a kernel -- on the host it is only a stand-in for the symbol --
+// but the device address that hellinger_scratch() looks up once per device.
+static __device__ __align__(256) double scratch[kHellingerScratch];
 
 namespace {
 
@@ -105,6 +112,45 @@ __global__ void k_hell_finish(int64_t n, int32_t slices, const double *__restric
 }
 
 }  // namespace
+
+int hellinger_scratch(int device, double **out)
+{
+    static std::mutex mu;
+    static double *addr[kMaxDevices] = {};
+    static bool looked_up[kMaxDevices] = {};
+    *out = nullptr;
+    if (device < 0 || device >= kMaxDevices) return (int)hipErrorInvalidDevice;
+    std::lock_guard<std::mutex> lock(mu);
+    if (!looked_up[device]) {
+        int cur = 0;
+        hipError_t e = hipGetDevice(&cur);
+        if (e == hipSuccess && cur != device) e = hipSetDevice(device);
+        void *p = nullptr;
+        if (e == hipSuccess) e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (cur != device) (void)hipSetDevice(cur);
+        if (e != hipSuccess) return (int)e;
+        addr[device] = static_cast<double *>(p);
+        looked_up[device] = true;
+    }
+    *out = addr[device];
+    return (int)hipSuccess;
+}
+
+HellingerPlan hellinger_plan(int32_t kp, int32_t kq, int64_t V, int64_t max_part)
+{
+    HellingerPlan p = hellinger_plan(kp, kq, V);
+    const int64_t nh = (int64_t)kp * kq;
+    if (nh == 0 || V <= 0) return p;
+    int64_t most = max_part / nh;  // slices whose partial sums fit
+    if (most < 1) most = 1;
+    if (p.slices > most) {
+        const int64_t stages = (V + kStage - 1) / kStage;
+        const int64_t per = (stages + most - 1) / most;
+        p.slice = per * kStage;
+        p.slices = (int32_t)((V + p.slice - 1) / p.slice);
+    }
+    return p;
+}
 
 HellingerPlan hellinger_plan(int32_t kp, int32_t kq, int64_t V)
 {

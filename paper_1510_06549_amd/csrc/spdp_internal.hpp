@@ -273,6 +273,15 @@ struct HellingerPlan {
     int64_t tiles = 1;   // output tiles (grid x)
 };
 HellingerPlan hellinger_plan(int32_t kp, int32_t kq, int64_t V);
+// the same with at most max_part partial sums (slices * kp * kq <= max_part
+// whenever kp * kq <= max_part)
+HellingerPlan hellinger_plan(int32_t kp, int32_t kq, int64_t V, int64_t max_part);
+// The allocation-free variant's partial-sum buffer: a file-scope device array
+// of kHellingerScratch doubles (8 MiB) per GPU; hellinger_scratch() returns
+// its device address on `device`, looked up once per device (a hipError_t).
+constexpr int64_t kHellingerScratch = 1 << 20;
+constexpr int kMaxDevices = 64;
+int hellinger_scratch(int device, double **out);
 hipError_t launch_hellinger(const HellingerPlan &p, const double *P, int32_t kp, const double *Q,
                             int32_t kq, int64_t V, double *part, double *h, hipStream_t st);
 // least-total-cost matching of the rows of c [kp][kq] (kp <= kq, finite):

@@ -34,6 +34,7 @@ EXPORTS = (
     "spdp_estimates", "spdp_heldout", "spdp_hellinger", "spdp_align_topics",
     "spdp_create_assoc", "spdp_get_slots", "spdp_set_assignments_assoc", "spdp_max_sources",
     "spdp_sweep_async", "spdp_read_probe", "spdp_check", "spdp_debug_poke",
+    "spdp_hellinger_noalloc",
 )
 
 
@@ -124,6 +125,8 @@ def load_library() -> C.CDLL:
     L.spdp_max_sources.restype = cint
     L.spdp_sweep_async.argtypes = [vp, u32, u64, i32, i32]
     L.spdp_sweep_async.restype = cint
+    L.spdp_hellinger_noalloc.argtypes = [vp, vp, i32, vp, i32, i32, vp]
+    L.spdp_hellinger_noalloc.restype = cint
     L.spdp_check.argtypes = [vp, C.POINTER(i64)]
     L.spdp_check.restype = cint
     L.spdp_debug_poke.argtypes = [vp, i32, i32, i32, i32, i32]
@@ -307,6 +310,19 @@ def spdp_read_probe(buf_ptr: int, nbytes: int, row_bytes: int = 0, rows: int = 0
                                  int(waves), None if stream is None else C.c_void_p(int(stream)),
                                  C.byref(ms)))
     return ms.value
+
+
+def spdp_hellinger_noalloc(h, p, q, out):
+    """Device tensors p [V, kp], q [V, kq], out [kp, kq] (float64); enqueues
+    only, on the state's stream."""
+    V, kp = p.shape
+    kq = q.shape[1]
+    assert q.shape[0] == V and tuple(out.shape) == (kp, kq)
+    for x in (p, q, out):
+        assert x.is_cuda and x.dtype.is_floating_point and x.element_size() == 8
+        assert x.is_contiguous()
+    _check(lib().spdp_hellinger_noalloc(h, p.data_ptr(), kp, q.data_ptr(), kq, V,
+                                        out.data_ptr()))
 
 
 def spdp_check(h):
