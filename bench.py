@@ -65,12 +65,14 @@ def sample_bytes_per_token(K: int, wide: bool, narrow: float = 0.0) -> float:
     return (4 - 2 * narrow) * K + (4 if wide else 2) * K + 13
 
 
-def assoc_bytes_per_token(K: int, wide: bool, mean_sources: float, Sp: int) -> float:
+def assoc_bytes_per_token(K: int, wide: bool, mean_sources: float, Sp: int,
+                          narrow: float = 0.0) -> float:
     """Bytes the association sampler must move per token: the packed count
-    row, one shadow-base row per source of the token's row (mean_sources on
-    average), the token stream (row index and state in, state out) and the
-    row's source record (Sp source words and Sp fp32 p)."""
-    return 4 * K + (4 if wide else 2) * K * mean_sources + 12 + 8 * Sp
+    row (16-bit cells for the share `narrow` of tokens, as in the plain
+    sampler), one shadow-base row per source of the token's row (mean_sources
+    on average), the token stream (row index, state and narrow-row flag in,
+    state out) and the row's source record (Sp source words and Sp fp32 p)."""
+    return (4 - 2 * narrow) * K + (4 if wide else 2) * K * mean_sources + 13 + 8 * Sp
 
 
 def foldin_bytes_per_token(K: int) -> int:
@@ -167,11 +169,19 @@ def cpu_baseline(cp, wl, state, target_s: float, assoc=None, full_sweeps: int = 
         return int(m.doc_off[d]), time.perf_counter() - t, d
 
     def whole_sweeps(n):
+        """Mean time of n whole sweeps: the sampling step of every document
+        (in eight runs of documents, each logged), then rebuild and repair."""
         st = [x.copy() for x in state]
         cc = m.rebuild(*st)
+        bounds = np.linspace(0, m.D, 9).astype(int)
         t = time.perf_counter()
         for k in range(n):
-            m.sweep(cc, *st, k, 1000 + seed)
+            for j in range(8):
+                m.sample_docs(cc, *st, k, 1000 + seed, int(bounds[j]), int(bounds[j + 1]))
+                if N > 10_000_000:
+                    log(f"[bench] oracle sweep {k}: documents up to {bounds[j + 1]} sampled")
+            cc = m.rebuild(*st, counts=cc)
+            m.repair(*st, cc)
         return (time.perf_counter() - t) / n
 
     # calibration: a few documents
@@ -495,7 +505,8 @@ def main():
         q = np.repeat(cp.doc_group, np.diff(cp.doc_off)).astype(np.int64) * cp.vocab + cp.words
         mean_sources = float(lens[q].mean())
         Sp = 1 if s.S <= 1 else (2 if s.S <= 2 else (4 if s.S <= 4 else 8))
-        bpt = assoc_bytes_per_token(wl.K, wide, mean_sources, Sp)
+        narrow = narrow_fraction(cp)
+        bpt = assoc_bytes_per_token(wl.K, wide, mean_sources, Sp, narrow)
         traffic = (recorded_traffic("k_sample_assoc", f"{wl.name}-assoc{args.assoc}")
                    if args.assoc_eps == 0.3 else None)
     alg = N * bpt
@@ -523,6 +534,7 @@ def main():
         roofline["dense_int32_equiv_GBps"] = round(
             N * dense_bytes_per_token(wl.K) / avg_sample_s / 1e9, 1)
     else:
+        roofline["narrow_row_token_share"] = round(narrow, 4)
         roofline["mean_sources_per_token"] = round(mean_sources, 4)
 
     if not args.no_read_probe:
