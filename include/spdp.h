@@ -349,7 +349,8 @@ int spdp_stats(const spdp_state *s, int64_t *changed, int64_t *repaired);
  * Per-kernel timing with HIP events on the state's stream.  enable = 1 starts
  * recording (and clears the accumulators), 0 stops.  spdp_kernel_times writes
  * the accumulated milliseconds and launch counts of the SPDP_NKERNELS kernel
- * classes, in this order: sampling; count rebuild with repair; shadow base;
+ * classes, in this order: sampling; count rebuild with repair (which also
+ * sums the shadow-base counts); the 16-bit copy of the shadow base;
  * per-restaurant totals and per-sweep constants.  Synchronises.
  */
 #define SPDP_NKERNELS 4

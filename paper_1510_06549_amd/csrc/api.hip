@@ -50,6 +50,9 @@ struct spdp_state {
     int cur = 0;
     int64_t bytes = 0;
     int64_t n_narrow_rows = 0;
+    // true while the 32-bit rows of the narrow rows equal their 16-bit copies
+    // (the rebuild writes a narrow row only as its copy)
+    mutable bool rows32 = false;
     bool timing = false;
     std::vector<EventPair> events[SPDP_NKERNELS];
     std::vector<void *> allocs;
@@ -126,18 +129,26 @@ int rebuild_state(spdp_state *s)
     const Model &m = s->m;
     DeviceBuffers &b = s->b;
     int32_t *zr = b.zr[s->cur];
-    if (m.Sp > 0) {
-        HIP_TRY(launch_rows_assoc(m, b, zr, s->st));
-        HIP_TRY(launch_base16(m, b, s->st));
-    } else {
-        HIP_TRY(launch_rows(m, b, zr, s->st));
-        HIP_TRY(launch_base(m, b, s->st));
-    }
+    if (m.Sp > 0) HIP_TRY(launch_rows_assoc(m, b, zr, s->st));
+    else HIP_TRY(launch_rows(m, b, zr, s->st));
+    HIP_TRY(launch_base16(m, b, s->st));
+    s->rows32 = false;
     HIP_TRY(launch_totals(m, b, zr, s->st));
     if (m.N > 0)
         HIP_TRY(hipMemcpyAsync(b.zr[1 - s->cur], zr, (size_t)m.N * sizeof(int32_t),
                                hipMemcpyDeviceToDevice, s->st));
     return SPDP_OK;
+}
+
+// The 32-bit rows of the narrow rows, rewritten from their 16-bit copies once
+// after each rebuild, for the entry points that read 32-bit rows (export,
+// estimates, likelihood, fold-in, the asynchronous sweep).
+hipError_t widen_rows(const spdp_state *s)
+{
+    if (s->rows32) return hipSuccess;
+    hipError_t e = launch_widen(s->m, s->b, s->st);
+    if (e == hipSuccess) s->rows32 = true;
+    return e;
 }
 
 int check_device_flags(spdp_state *s, int32_t *host_err)
@@ -509,8 +520,9 @@ int spdp_sweep(spdp_state *s, uint32_t sweep, uint64_t seed)
             return rc;
         if ((rc = timed(s, 1, [&] { return launch_rows(m, b, zr_new, s->st); })) != SPDP_OK)
             return rc;
-        if ((rc = timed(s, 2, [&] { return launch_base(m, b, s->st); })) != SPDP_OK) return rc;
+        if ((rc = timed(s, 2, [&] { return launch_base16(m, b, s->st); })) != SPDP_OK) return rc;
     }
+    s->rows32 = false;
     if ((rc = timed(s, 3, [&] { return launch_totals(m, b, zr_new, s->st); })) != SPDP_OK) return rc;
     s->cur = 1 - s->cur;
     return SPDP_OK;
@@ -544,6 +556,8 @@ int spdp_sweep_async(spdp_state *s, uint32_t sweep, uint64_t seed, int32_t waves
     if (m.N > 0)
         HIP_TRY(hipMemcpyAsync(zr_new, zr_old, (size_t)m.N * sizeof(int32_t),
                                hipMemcpyDeviceToDevice, s->st));
+    // the pass reads and updates the 32-bit rows of every row
+    HIP_TRY(widen_rows(s));
     if ((rc = timed(s, 3, [&] { return launch_doc_counts(m, b, zr_new, b.cdk, s->st); })) != SPDP_OK)
         return rc;
     if ((rc = timed(s, 0, [&] {
@@ -552,7 +566,8 @@ int spdp_sweep_async(spdp_state *s, uint32_t sweep, uint64_t seed, int32_t waves
          })) != SPDP_OK)
         return rc;
     if ((rc = timed(s, 1, [&] { return launch_rows(m, b, zr_new, s->st); })) != SPDP_OK) return rc;
-    if ((rc = timed(s, 2, [&] { return launch_base(m, b, s->st); })) != SPDP_OK) return rc;
+    if ((rc = timed(s, 2, [&] { return launch_base16(m, b, s->st); })) != SPDP_OK) return rc;
+    s->rows32 = false;
     if ((rc = timed(s, 3, [&] { return launch_totals(m, b, zr_new, s->st); })) != SPDP_OK) return rc;
     s->cur = 1 - s->cur;
     return SPDP_OK;
@@ -567,6 +582,7 @@ int spdp_counts(const spdp_state *s, int32_t g_begin, int32_t g_end, int32_t *n_
     if (where != 0 && where != 1) return fail(SPDP_E_ARG, "where must be 0 or 1");
     HIP_TRY(hipSetDevice(s->device));
     if (!n_gkw && !t_gkw) return SPDP_OK;
+    HIP_TRY(widen_rows(s));
     const int64_t cells = (int64_t)m.V * m.K;
     int32_t *stage_n = nullptr, *stage_t = nullptr;
     if (where == 0) {
@@ -619,6 +635,7 @@ int spdp_loglik(spdp_state *s, double *out)
 {
     if (!s || !out) return fail(SPDP_E_ARG, "null argument");
     HIP_TRY(hipSetDevice(s->device));
+    HIP_TRY(widen_rows(s));
     HIP_TRY(launch_fill_i32(s->b.err, 2, 0, s->st));
     HIP_TRY(launch_loglik(s->m, s->b, s->b.zr[s->cur], s->st));
     double v = 0.0;
@@ -640,6 +657,7 @@ int spdp_estimates(spdp_state *s, int32_t g_begin, int32_t g_end, double *theta,
     if (phi && (g_begin < 0 || g_end > m.G || g_begin > g_end))
         return fail(SPDP_E_ARG, "bad group range");
     HIP_TRY(hipSetDevice(s->device));
+    if (phi) HIP_TRY(widen_rows(s));
     const int64_t vk = (int64_t)m.V * m.K, dk = (int64_t)m.D * m.K;
     // device destinations (the caller's buffers, or one staging buffer reused)
     double *stage = nullptr;
@@ -697,6 +715,7 @@ int spdp_heldout(spdp_state *s, const spdp_corpus *test, const spdp_groups *test
         }
     }
     HIP_TRY(hipSetDevice(s->device));
+    HIP_TRY(widen_rows(s));
     int32_t *gw_d = nullptr, *grp_d = nullptr, *z_d = nullptr;
     int64_t *off_d = nullptr;
     double *ll_d = nullptr;
@@ -1148,16 +1167,34 @@ int spdp_debug_poke(spdp_state *s, int32_t g, int32_t w, int32_t k, int32_t dn, 
     if (g < 0 || g >= m.G || w < 0 || w >= m.V || k < 0 || k >= m.K)
         return fail(SPDP_E_ARG, "cell (%d, %d, %d) out of range", g, w, k);
     HIP_TRY(hipSetDevice(s->device));
-    int32_t *cell = s->b.nt + ((int64_t)g * m.V + w) * m.Kp + k;
-    int32_t x = 0;
-    HIP_TRY(hipMemcpyAsync(&x, cell, sizeof x, hipMemcpyDeviceToHost, s->st));
+    // the copy the samplers read: the 16-bit one of a narrow row
+    const int64_t q = (int64_t)g * m.V + w;
+    uint8_t nar = 0;
+    HIP_TRY(hipMemcpyAsync(&nar, s->b.row_narrow + q, 1, hipMemcpyDeviceToHost, s->st));
     int rc = sync(s);
     if (rc != SPDP_OK) return rc;
+    const int32_t cap = nar ? kNarrowMax : kCountMax;
+    int32_t x = 0;
+    if (nar) {
+        uint16_t y = 0;
+        HIP_TRY(hipMemcpyAsync(&y, s->b.nt16 + q * m.Kp + k, sizeof y, hipMemcpyDeviceToHost, s->st));
+        if ((rc = sync(s)) != SPDP_OK) return rc;
+        x = wide_of(y);
+    } else {
+        HIP_TRY(hipMemcpyAsync(&x, s->b.nt + q * m.Kp + k, sizeof x, hipMemcpyDeviceToHost, s->st));
+        if ((rc = sync(s)) != SPDP_OK) return rc;
+    }
     const int32_t n = (x & kCountMax) + dn, t = (x >> kCountBits) + dt;
-    if (n < 0 || n > kCountMax || t < 0 || t > kCountMax)
-        return fail(SPDP_E_ARG, "poked counts (%d, %d) out of [0, %d]", n, t, kCountMax);
+    if (n < 0 || n > cap || t < 0 || t > cap)
+        return fail(SPDP_E_ARG, "poked counts (%d, %d) out of [0, %d]", n, t, cap);
     x = n | (t << kCountBits);
-    HIP_TRY(hipMemcpyAsync(cell, &x, sizeof x, hipMemcpyHostToDevice, s->st));
+    if (nar) {
+        const uint16_t y = narrow_of(x);
+        HIP_TRY(hipMemcpyAsync(s->b.nt16 + q * m.Kp + k, &y, sizeof y, hipMemcpyHostToDevice, s->st));
+        s->rows32 = false;
+    } else {
+        HIP_TRY(hipMemcpyAsync(s->b.nt + q * m.Kp + k, &x, sizeof x, hipMemcpyHostToDevice, s->st));
+    }
     return sync(s);
 }
 

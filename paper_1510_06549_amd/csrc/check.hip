@@ -9,11 +9,12 @@
 // without changing anything.
 //
 //   k_check_rows   per count row: LDS recount of its tokens' states against
-//                  the stored packed cells (and the 16-bit copy of a narrow
-//                  row); invalid cells; tokens with a topic out of range or
-//                  (word associations) a head whose slot names no source
-//   k_check_base   plain model: B[w][k] = sum_g t[g][w][k], B16 = min(B,
-//                  65535), and the width flag
+//                  the stored packed cells (of a narrow row, its 16-bit copy,
+//                  the one the rebuild writes and the samplers read); invalid
+//                  cells; tokens with a topic out of range or (word
+//                  associations) a head whose slot names no source
+//   k_check_base   plain model: B[w][k] = sum_g t[g][w][k] over the same
+//                  copies, B16 = min(B, 65535), and the width flag
 //   k_base_heads / k_cmp_base
 //                  word associations: B recounted from the heads' sources
 //   k_cmp_i32      recomputed totals against the stored ones
@@ -76,16 +77,14 @@ __global__ void __launch_bounds__(64) k_check_rows(int32_t K, int32_t Kp, int32_
         add_bad(bad, wrong);
     }
     __syncthreads();
-    const int32_t *__restrict__ row = nt + q * Kp;
-    const bool nar = row_narrow[q] != 0 && rs < re;
+    const bool nar = row_narrow[q] != 0;
     for (int32_t k0 = 0; k0 < Kp; k0 += 64) {
         const int32_t k = k0 + lane;
         bool wrong = false;
         if (k < Kp) {
-            const int32_t x = row[k];
+            const int32_t x = nar ? wide_of(nt16[q * Kp + k]) : nt[q * Kp + k];
             const int32_t n = x & kCountMax, t = x >> kCountBits;
             wrong = x != h[k] || t > n || (t == 0) != (n == 0);
-            if (nar) wrong = wrong || nt16[q * Kp + k] != narrow_of(x);
         }
         add_bad(bad, wrong);
     }
@@ -94,6 +93,8 @@ __global__ void __launch_bounds__(64) k_check_rows(int32_t K, int32_t Kp, int32_
 // B[w][k] against sum_g t[g][w][k] of the stored rows, B16 against min(B,
 // 65535); over counts the cells with B > 65535.
 __global__ void k_check_base(int32_t G, int32_t V, int32_t Kp, const int32_t *__restrict__ nt,
+                             const uint16_t *__restrict__ nt16,
+                             const uint8_t *__restrict__ row_narrow,
                              const int32_t *__restrict__ B, const uint16_t *__restrict__ B16,
                              unsigned long long *__restrict__ bad,
                              unsigned long long *__restrict__ over)
@@ -103,7 +104,11 @@ __global__ void k_check_base(int32_t G, int32_t V, int32_t Kp, const int32_t *__
     bool wrong = false, big = false;
     if (j < cells) {
         int32_t s = 0;
-        for (int32_t g = 0; g < G; ++g) s += nt[(int64_t)g * cells + j] >> kCountBits;
+        const int64_t w = j / Kp;
+        for (int32_t g = 0; g < G; ++g) {
+            const int64_t c = (int64_t)g * cells + j;
+            s += row_narrow[(int64_t)g * V + w] ? (int32_t)(nt16[c] >> 8) : (nt[c] >> kCountBits);
+        }
         const int32_t b = B[j];
         big = b > 0xFFFF;
         wrong = b != s || B16[j] != (uint16_t)(big ? 0xFFFF : b);
@@ -195,7 +200,8 @@ hipError_t launch_check(const Model &m, const DeviceBuffers &b, const int32_t *z
                            vk, b.B, Bre, b.B16, bad + 1, bad + 2);
     } else {
         hipLaunchKernelGGL(k_check_base, dim3((unsigned)blocks_for(vk, kBlock)), dim3(kBlock), 0,
-                           st, m.G, m.V, m.Kp, b.nt, b.B, b.B16, bad + 1, bad + 2);
+                           st, m.G, m.V, m.Kp, b.nt, b.nt16, b.row_narrow, b.B, b.B16, bad + 1,
+                           bad + 2);
     }
     hipLaunchKernelGGL(k_check_wide, dim3(1), dim3(64), 0, st, b.wide, bad + 2, bad + 1);
     return hipGetLastError();

@@ -11,17 +11,21 @@
 //               with one atomic cursor per row; the order inside a row is
 //               free, since nothing below depends on it), built once
 //   k_rows      per row: LDS histogram of its tokens' (z, r) -> the row's
-//               packed cells; then every cell left with customers but no
-//               table promotes the smallest-index token of that cell to table
-//               head (the repair of the parallel pass), and the row is written
-//               (a narrow row also as its 16-bit copy, which the sampler reads)
-//   k_base      shadow-base table counts B[w][k] = sum_g t[g][w][k], and the
-//               16-bit copy the sampler reads (with a flag raised when a count
-//               does not fit, in which case the sampler reads B itself)
-//   k_rows_assoc / k_base16
+//               packed cells; then every cell left with customers but no table
+//               promotes the smallest-index token of that cell to table head
+//               (the repair of the parallel pass); the row is written (a
+//               narrow row only as its 16-bit copy, which the samplers read;
+//               its 32-bit row is rewritten from it by k_widen when an entry
+//               point reads it), and its table counts are added to the shadow
+//               base B[w][k] = sum_g t[g][w][k] (integer atomics, zeroed
+//               before, so the sum does not depend on their order)
+//   k_rows_assoc
 //               the same with word associations: shadow-base counts keyed by
 //               each head's source word, and a promoted head takes its row's
 //               most probable source
+//   k_base16    the 16-bit copy of B the samplers read, min(B, 65535), with a
+//               flag raised when a count does not fit (the samplers then read
+//               B itself)
 //   k_unpack    export of n and t as separate int32 arrays, [k][w] per group
 #include <climits>
 
@@ -66,12 +70,15 @@ __device__ __forceinline__ void for_row_states(int32_t rs, int32_t re, int32_t l
 // One 64-lane block per count row; the row's histogram and the smallest token
 // index of each topic in LDS (2 Kp ints of dynamic shared memory).  Every
 // token's state is read once: a cell left with customers but no table holds
-// only r = 0 tokens, and its smallest-index token becomes its head.
-__global__ void __launch_bounds__(64) k_rows(int32_t Kp, const int32_t *__restrict__ row_off,
+// only r = 0 tokens, and its smallest-index token becomes its head.  Blocks
+// run in row order, so that the rows in flight together belong to one group,
+// whose states then stay in the last-level cache while they are gathered.
+__global__ void __launch_bounds__(64) k_rows(int32_t V, int32_t Kp,
+                                             const int32_t *__restrict__ row_off,
                                              const int32_t *__restrict__ perm,
                                              const uint8_t *__restrict__ row_narrow,
                                              int32_t *__restrict__ zr, int32_t *__restrict__ nt,
-                                             uint16_t *__restrict__ nt16,
+                                             uint16_t *__restrict__ nt16, int32_t *__restrict__ B,
                                              uint32_t *__restrict__ rep_part)
 {
     extern __shared__ int32_t rows_lds[];
@@ -93,6 +100,7 @@ __global__ void __launch_bounds__(64) k_rows(int32_t Kp, const int32_t *__restri
         __syncthreads();
         int32_t *__restrict__ row = nt + q * Kp;
         uint16_t *__restrict__ row16 = nt16 + q * Kp;
+        int32_t *__restrict__ base = B + (q % V) * Kp;
         const bool nar = row_narrow[q] != 0;
         for (int32_t k = lane; k < Kp; k += 64) {
             int32_t x = h[k];
@@ -102,8 +110,9 @@ __global__ void __launch_bounds__(64) k_rows(int32_t Kp, const int32_t *__restri
                 x += 1 << 16;
                 ++rep;
             }
-            row[k] = x;
             if (nar) row16[k] = narrow_of(x);
+            else row[k] = x;
+            if (x >> 16) atomicAdd(&base[k], x >> 16);
         }
     }
     for (int o = 32; o > 0; o >>= 1) rep += __shfl_xor(rep, o);
@@ -159,8 +168,8 @@ __global__ void __launch_bounds__(64) k_rows_assoc(int32_t Kp, int32_t Sp,
                 atomicAdd(&B[(int64_t)src[hs] * Kp + k], 1);
                 ++rep;
             }
-            row[k] = x;
             if (nar) row16[k] = narrow_of(x);
+            else row[k] = x;
         }
     }
     for (int o = 32; o > 0; o >>= 1) rep += __shfl_xor(rep, o);
@@ -181,22 +190,15 @@ __global__ void k_base16(int64_t cells, const int32_t *__restrict__ B,
     if (__any(over) && (threadIdx.x & 63) == 0) atomicOr(wide, 1);
 }
 
-// B[w][k] = sum_g t[g][w][k];  B16 = min(B, 65535), *wide = 1 if any B > 65535
-__global__ void k_base(int32_t G, int32_t V, int32_t Kp, const int32_t *__restrict__ nt,
-                       int32_t *__restrict__ B, uint16_t *__restrict__ B16,
-                       int32_t *__restrict__ wide)
+// The 32-bit rows of the narrow rows, rewritten from their 16-bit copies (one
+// block per row; rows that are not narrow are skipped).
+__global__ void k_widen(int32_t Kp, const uint8_t *__restrict__ row_narrow,
+                        const uint16_t *__restrict__ nt16, int32_t *__restrict__ nt)
 {
-    const int64_t j = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    const int64_t cells = (int64_t)V * Kp;
-    bool over = false;
-    if (j < cells) {
-        int32_t s = 0;
-        for (int32_t g = 0; g < G; ++g) s += nt[(int64_t)g * cells + j] >> 16;
-        B[j] = s;
-        over = s > 0xFFFF;
-        B16[j] = (uint16_t)(over ? 0xFFFF : s);
-    }
-    if (__any(over) && (threadIdx.x & 63) == 0) atomicOr(wide, 1);
+    const int64_t q = blockIdx.x;
+    if (!row_narrow[q]) return;
+    for (int32_t k = threadIdx.x; k < Kp; k += blockDim.x)
+        nt[q * Kp + k] = wide_of(nt16[q * Kp + k]);
 }
 
 // Export of one group's counts as [k][w] (topic-major, the thesis's logical
@@ -568,19 +570,19 @@ hipError_t build_visit_order(const Model &m, DeviceBuffers &b, hipStream_t st)
 hipError_t launch_rows(const Model &m, const DeviceBuffers &b, int32_t *zr, hipStream_t st)
 {
     const int64_t rows = (int64_t)m.G * m.V;
+    hipError_t e = launch_fill_i32(b.B, (int64_t)m.V * m.Kp, 0, st);
+    if (e != hipSuccess) return e;
     const size_t lds = 2 * (size_t)m.Kp * sizeof(int32_t);
-    hipLaunchKernelGGL(k_rows, dim3((unsigned)rows), dim3(64), lds, st, m.Kp, b.row_off, b.perm,
-                       b.row_narrow, zr, b.nt, b.nt16, b.rep_part);
+    hipLaunchKernelGGL(k_rows, dim3((unsigned)rows), dim3(64), lds, st, m.V, m.Kp, b.row_off,
+                       b.perm, b.row_narrow, zr, b.nt, b.nt16, b.B, b.rep_part);
     return hipGetLastError();
 }
 
-hipError_t launch_base(const Model &m, const DeviceBuffers &b, hipStream_t st)
+hipError_t launch_widen(const Model &m, const DeviceBuffers &b, hipStream_t st)
 {
-    const int64_t cells = (int64_t)m.V * m.Kp;
-    hipError_t e = launch_fill_i32(b.wide, 1, 0, st);
-    if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(k_base, dim3((unsigned)blocks_for(cells, kBlock)), dim3(kBlock), 0, st, m.G,
-                       m.V, m.Kp, b.nt, b.B, b.B16, b.wide);
+    const int64_t rows = (int64_t)m.G * m.V;
+    hipLaunchKernelGGL(k_widen, dim3((unsigned)rows), dim3(m.Kp < 256 ? (unsigned)m.Kp : 256u), 0,
+                       st, m.Kp, b.row_narrow, b.nt16, b.nt);
     return hipGetLastError();
 }
 

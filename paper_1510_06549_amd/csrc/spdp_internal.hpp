@@ -91,8 +91,9 @@ constexpr int32_t kCountMax = (1 << kCountBits) - 1;  // largest n a packed cell
 // Narrow rows.  A (group, word) pair with at most kNarrowMax tokens in the
 // corpus can never have a count above kNarrowMax in any state (n[g][k][w] <=
 // c[g][w]), so its row also exists as 16-bit cells n | t << 8, half the
-// bytes, which the sampler reads instead.  Which rows are narrow is fixed at
-// creation; the rebuild writes both copies of a narrow row.
+// bytes, which the samplers read instead.  Which rows are narrow is fixed at
+// creation; the rebuild writes only the 16-bit copy of a narrow row, and its
+// 32-bit row is rewritten from that copy when an entry point reads it.
 constexpr int32_t kNarrowMax = 255;
 __host__ __device__ __forceinline__ uint16_t narrow_of(int32_t packed)
 {
@@ -135,13 +136,14 @@ struct DeviceBuffers {
     int32_t *doc_group = nullptr; // [D]
     int32_t *zr[2] = {nullptr, nullptr}; // [N] current / next packed state
     int32_t *nt = nullptr;        // [G V][Kp] packed n | t << 16
-    uint16_t *nt16 = nullptr;     // [G V][Kp] narrow rows as n | t << 8 (other rows unused)
+    uint16_t *nt16 = nullptr;     // [G V][Kp] narrow rows as n | t << 8 (other rows unused);
+                                  // the rebuild writes a narrow row only here
     uint8_t *row_narrow = nullptr; // [G V] 1 if row q is narrow (c[g][w] <= kNarrowMax)
     uint8_t *tok_narrow = nullptr; // [N] row_narrow of each token's row (the sampler's stream)
     int32_t *B = nullptr;         // [V][Kp]   shadow-base table counts
     uint16_t *B16 = nullptr;      // [V][Kp]   min(B, 65535): the sampler's copy
     int32_t *wide = nullptr;      // [1] 1 if some B exceeds 65535 (the sampler then reads B)
-    int32_t *perm = nullptr;      // [N] tokens sorted by row (stable)
+    int32_t *perm = nullptr;      // [N] tokens grouped by row (any order inside a row)
     int32_t *row_off = nullptr;   // [G V + 1] offsets of each row's tokens in perm
     int32_t *Ngk = nullptr;       // [G][Kp]
     int32_t *Tgk = nullptr;       // [G][Kp]
@@ -205,12 +207,17 @@ hipError_t launch_unpack_zr(const Model &m, const int32_t *zr, int32_t *z, uint8
                             hipStream_t st);
 hipError_t build_row_index(const Model &m, DeviceBuffers &b, const int32_t *gw_count,
                            hipStream_t st);
+// count rows with the repair, and the shadow-base counts B (zeroed, then each
+// row's table counts added) of the plain model, from the state zr
 hipError_t launch_rows(const Model &m, const DeviceBuffers &b, int32_t *zr, hipStream_t st);
-hipError_t launch_base(const Model &m, const DeviceBuffers &b, hipStream_t st);
+// the 32-bit rows of the narrow rows from their 16-bit copies (the rebuild
+// writes a narrow row only as its copy; entry points that read 32-bit rows
+// call this first)
+hipError_t launch_widen(const Model &m, const DeviceBuffers &b, hipStream_t st);
 // word associations: count rows with the repair, and the shadow-base counts
-// keyed by source (B zeroed, then one increment per head), then B16 and the
-// width flag from B
+// keyed by source (B zeroed, then one increment per head)
 hipError_t launch_rows_assoc(const Model &m, const DeviceBuffers &b, int32_t *zr, hipStream_t st);
+// B16 and the width flag from B (after either rebuild)
 hipError_t launch_base16(const Model &m, const DeviceBuffers &b, hipStream_t st);
 hipError_t launch_pack_zrs(const Model &m, const DeviceBuffers &b, const int32_t *z,
                            const uint8_t *r, const uint8_t *s, int32_t *zr, int32_t *bad,

@@ -156,3 +156,36 @@ def test_read_probe_on_a_device_buffer():
         sp.spdp_read_probe(host.ctypes.data, host.nbytes, 0, 0, 64, st)
     assert e.value.code == sp.SPDP_E_ARG
     assert torch.all(buf == 1)
+
+
+@pytest.mark.parametrize("K", [1, 2, 64, 65, 129, 257, 513, 769, 1024])
+def test_narrow_and_wide_rows_at_every_lane_layout(K):
+    """Rows of both widths in one corpus: words repeated more than 255 times in
+    a group (32-bit rows) beside rare words (16-bit narrow copies), including
+    a pair with exactly 255 tokens (the last narrow count) and one with 256,
+    at every per-lane topic count of the sampler."""
+    say(f"narrow and wide count rows, K = {K}")
+    rng = np.random.default_rng(K)
+    V = 40
+    docs = []
+    for d in range(60):
+        g = d % 2
+        L = int(rng.integers(20, 90))
+        # word 0: ~15 per document (wide in both groups); word 1: a tail word
+        ws = [0] * 15 + list(rng.integers(2, V, size=L))
+        docs.append((g, ws))
+    # exactly 255 tokens of word 1 in group 0 and 256 in group 1
+    docs.append((0, [1] * 255))
+    docs.append((1, [1] * 200))
+    docs.append((1, [1] * 56))
+    cp = corpus_from_docs(docs, vocab=V)
+    q = np.repeat(cp.doc_group, np.diff(cp.doc_off)).astype(np.int64) * V + cp.words
+    c = np.bincount(q, minlength=2 * V)
+    assert c[1] == 255 and c[V + 1] == 256 and c[0] > 255 and c[V] > 255
+    wl = W(K=K)
+    s, m = parity.make_pair(cp, wl, init_seed=K)
+    for sw in range(3):
+        rep, ch, rp = parity.one_step(s, m, sw, 17)
+        say(f"  {rep}")
+    assert s.check() == 0
+    s.close()
