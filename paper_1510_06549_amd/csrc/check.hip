@@ -107,7 +107,7 @@ __global__ void k_check_base(int32_t G, int32_t V, int32_t Kp, const int32_t *__
         const int64_t w = j / Kp;
         for (int32_t g = 0; g < G; ++g) {
             const int64_t c = (int64_t)g * cells + j;
-            s += row_narrow[(int64_t)g * V + w] ? (int32_t)(nt16[c] >> 8) : (nt[c] >> kCountBits);
+            s += (row_narrow[(int64_t)g * V + w] ? wide_of(nt16[c]) : nt[c]) >> kCountBits;
         }
         const int32_t b = B[j];
         big = b > 0xFFFF;
