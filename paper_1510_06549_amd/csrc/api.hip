@@ -399,6 +399,11 @@ int create_state(const spdp_corpus *corpus, const spdp_groups *groups, const spd
     unsigned long long n_narrow = 0;
     {
         int rc2 = dev_alloc(s, &B.perm, N, "row-sorted tokens");
+        if (!assoc) {  // the plain model's rebuild gathers from routed states
+            if (rc2 == SPDP_OK) rc2 = dev_alloc(s, &B.tok_slot, N, "state route of tokens");
+            if (rc2 == SPDP_OK) rc2 = dev_alloc(s, &B.row_slot, N, "state route of row entries");
+            if (rc2 == SPDP_OK) rc2 = dev_alloc(s, &B.zr_b, N, "routed states");
+        }
         if (rc2 == SPDP_OK) rc2 = dev_alloc(s, &B.row_off, rows + 1, "row offsets");
         if (rc2 == SPDP_OK) rc2 = dev_alloc(s, &B.row_narrow, rows, "narrow-row flags");
         if (rc2 == SPDP_OK) rc2 = dev_alloc(s, &B.tok_narrow, N, "narrow-row flags of tokens");

@@ -10,6 +10,9 @@
 //               exclusive scan of the per-row token counts, then a scatter
 //               with one atomic cursor per row; the order inside a row is
 //               free, since nothing below depends on it), built once
+//   k_route     the sampled states copied into row buckets (see below), so
+//               that the rebuild's per-token gathers stay within a region of
+//               the cache's size (the plain model)
 //   k_rows      per row: LDS histogram of its tokens' (z, r) -> the row's
 //               packed cells; then every cell left with customers but no table
 //               promotes the smallest-index token of that cell to table head
@@ -45,11 +48,38 @@ inline int64_t blocks_for(int64_t n, int per_block)
 
 // The row's tokens' states, four per lane in flight: lane l takes row list
 // entries rs + l, rs + l + 64, ... and hands each (token index, state v) to f
-// in any order.
+// in any order.  The states are read from their routed copy zr_b, where the
+// states of the rows of one bucket sit together (row_slot: the copy's slot of
+// each row list entry).
 template <typename F>
 __device__ __forceinline__ void for_row_states(int32_t rs, int32_t re, int32_t lane,
                                                const int32_t *__restrict__ perm,
-                                               const int32_t *__restrict__ zr, F &&f)
+                                               const int32_t *__restrict__ row_slot,
+                                               const int32_t *__restrict__ zr_b, F &&f)
+{
+    int32_t j = rs + lane;
+    for (; j + 192 < re; j += 256) {
+        int32_t t[4], s[4], v[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            t[u] = perm[j + 64 * u];
+            s[u] = row_slot[j + 64 * u];
+        }
+#pragma unroll
+        for (int u = 0; u < 4; ++u) v[u] = zr_b[s[u]];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) f(t[u], v[u]);
+    }
+    for (; j < re; j += 64) f(perm[j], zr_b[row_slot[j]]);
+}
+
+// The same, gathering each state from token order (the word-association
+// rebuild, whose time is set by its atomics into B rather than by these
+// gathers, so that routing the states first does not pay there).
+template <typename F>
+__device__ __forceinline__ void for_row_states_direct(int32_t rs, int32_t re, int32_t lane,
+                                                      const int32_t *__restrict__ perm,
+                                                      const int32_t *__restrict__ zr, F &&f)
 {
     int32_t j = rs + lane;
     for (; j + 192 < re; j += 256) {
@@ -67,6 +97,81 @@ __device__ __forceinline__ void for_row_states(int32_t rs, int32_t re, int32_t l
     }
 }
 
+// ------------------------------------------------------- state route
+// The rebuild reads each row's states in row order, while the sampler writes
+// them in token order.  Gathering them one 4-byte state at a time from token
+// order fetches a whole line per state; instead the plain model's rebuild
+// first copies the states (k_route, coalesced reads, writes in runs) into
+// zr_b, where the states of each bucket of rows (the rows starting in one
+// window of 2^kRouteShift row positions, about 4 MB of states) occupy that
+// bucket's range of row positions, so that the rows' gathers stay within a
+// region that fits the cache.  The route is static: fixed with the row index.
+constexpr int kRouteShift = 20;
+constexpr int kRouteThreads = 1024;
+
+// start of each bucket's range: the smallest start of its non-empty rows
+__global__ void k_bucket_start(int64_t rows, const int32_t *__restrict__ row_off,
+                               int32_t *__restrict__ start)
+{
+    const int64_t q = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (q < rows && row_off[q] < row_off[q + 1])
+        atomicMin(&start[row_off[q] >> kRouteShift], row_off[q]);
+}
+
+// tok_slot[i]: token i's slot in its bucket's range.  Each block counts its
+// tokens per bucket in LDS (nb ints), reserves one run per bucket with a
+// global cursor (initialised to the bucket starts), and places its tokens in
+// those runs.
+__global__ void __launch_bounds__(kRouteThreads) k_route_build(int64_t N, int32_t nb,
+                                                               const int32_t *__restrict__ gw,
+                                                               const int32_t *__restrict__ row_off,
+                                                               int32_t *__restrict__ cursor,
+                                                               int32_t *__restrict__ tok_slot)
+{
+    extern __shared__ int32_t run[];
+    for (int32_t k = threadIdx.x; k < nb; k += kRouteThreads) run[k] = 0;
+    __syncthreads();
+    const int64_t i = (int64_t)blockIdx.x * kRouteThreads + threadIdx.x;
+    int32_t bk = 0, local = 0;
+    if (i < N) {
+        bk = row_off[gw[i]] >> kRouteShift;
+        local = atomicAdd(&run[bk], 1);
+    }
+    __syncthreads();
+    for (int32_t k = threadIdx.x; k < nb; k += kRouteThreads) {
+        const int32_t c = run[k];
+        run[k] = c ? atomicAdd(&cursor[k], c) : 0;
+    }
+    __syncthreads();
+    if (i < N) tok_slot[i] = run[bk] + local;
+}
+
+// row_slot[j] = tok_slot[perm[j]]
+__global__ void k_compose(int64_t N, const int32_t *__restrict__ perm,
+                          const int32_t *__restrict__ tok_slot, int32_t *__restrict__ row_slot)
+{
+    const int64_t j = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (j < N) row_slot[j] = tok_slot[perm[j]];
+}
+
+// zr_b[tok_slot[i]] = zr[i], four tokens per thread
+__global__ void __launch_bounds__(kBlock) k_route(int64_t N, const int32_t *__restrict__ tok_slot,
+                                                  const int32_t *__restrict__ zr,
+                                                  int32_t *__restrict__ zr_b)
+{
+    const int64_t i0 = (int64_t)blockIdx.x * (4 * kBlock) + threadIdx.x;
+    int32_t d[4], v[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+        const int64_t i = i0 + (int64_t)u * kBlock;
+        d[u] = i < N ? tok_slot[i] : -1;
+        v[u] = i < N ? zr[i] : 0;
+    }
+#pragma unroll
+    for (int u = 0; u < 4; ++u)
+        if (d[u] >= 0) zr_b[d[u]] = v[u];
+}
+
 // One 64-lane block per count row; the row's histogram and the smallest token
 // index of each topic in LDS (2 Kp ints of dynamic shared memory).  Every
 // token's state is read once: a cell left with customers but no table holds
@@ -76,6 +181,8 @@ __device__ __forceinline__ void for_row_states(int32_t rs, int32_t re, int32_t l
 __global__ void __launch_bounds__(64) k_rows(int32_t V, int32_t Kp,
                                              const int32_t *__restrict__ row_off,
                                              const int32_t *__restrict__ perm,
+                                             const int32_t *__restrict__ row_slot,
+                                             const int32_t *__restrict__ zr_b,
                                              const uint8_t *__restrict__ row_narrow,
                                              int32_t *__restrict__ zr, int32_t *__restrict__ nt,
                                              uint16_t *__restrict__ nt16, int32_t *__restrict__ B,
@@ -93,7 +200,7 @@ __global__ void __launch_bounds__(64) k_rows(int32_t V, int32_t Kp,
             first[k] = INT_MAX;
         }
         __syncthreads();
-        for_row_states(rs, re, lane, perm, zr, [&](int32_t tok, int32_t v) {
+        for_row_states(rs, re, lane, perm, row_slot, zr_b, [&](int32_t tok, int32_t v) {
             atomicAdd(&h[v >> 1], 1 + ((v & 1) << 16));
             atomicMin(&first[v >> 1], tok);
         });
@@ -148,7 +255,7 @@ __global__ void __launch_bounds__(64) k_rows_assoc(int32_t Kp, int32_t Sp,
             first[k] = INT_MAX;
         }
         __syncthreads();
-        for_row_states(rs, re, lane, perm, zr, [&](int32_t tok, int32_t v) {
+        for_row_states_direct(rs, re, lane, perm, zr, [&](int32_t tok, int32_t v) {
             const int32_t k = zr_topic(v);
             atomicAdd(&h[k], 1 + ((v & 1) << 16));
             atomicMin(&first[k], tok);
@@ -523,6 +630,27 @@ hipError_t build_row_index(const Model &m, DeviceBuffers &b, const int32_t *gw_c
     }
     hipError_t e2 = hipStreamSynchronize(st);
     (void)hipFree(cursor);
+    if (e != hipSuccess || e2 != hipSuccess) return e != hipSuccess ? e : e2;
+    if (!b.tok_slot) return hipSuccess;  // no route (word associations)
+
+    // the state route (bucket starts are row starts, so every bucket's tokens
+    // fill exactly its range of row positions)
+    const int32_t nb = (int32_t)((m.N - 1) >> kRouteShift) + 1;
+    int32_t *start = nullptr;
+    if ((e = hipMalloc(&start, (size_t)nb * sizeof(int32_t))) != hipSuccess) return e;
+    e = launch_fill_i32(start, nb, INT_MAX, st);
+    if (e == hipSuccess) {
+        hipLaunchKernelGGL(k_bucket_start, dim3((unsigned)blocks_for(rows, kBlock)), dim3(kBlock),
+                           0, st, rows, b.row_off, start);
+        hipLaunchKernelGGL(k_route_build, dim3((unsigned)blocks_for(m.N, kRouteThreads)),
+                           dim3(kRouteThreads), (size_t)nb * sizeof(int32_t), st, m.N, nb, b.gw,
+                           b.row_off, start, b.tok_slot);
+        hipLaunchKernelGGL(k_compose, dim3((unsigned)blocks_for(m.N, kBlock)), dim3(kBlock), 0, st,
+                           m.N, b.perm, b.tok_slot, b.row_slot);
+        e = hipGetLastError();
+    }
+    e2 = hipStreamSynchronize(st);
+    (void)hipFree(start);
     return e != hipSuccess ? e : e2;
 }
 
@@ -572,9 +700,13 @@ hipError_t launch_rows(const Model &m, const DeviceBuffers &b, int32_t *zr, hipS
     const int64_t rows = (int64_t)m.G * m.V;
     hipError_t e = launch_fill_i32(b.B, (int64_t)m.V * m.Kp, 0, st);
     if (e != hipSuccess) return e;
+    if (m.N > 0)
+        hipLaunchKernelGGL(k_route, dim3((unsigned)blocks_for(m.N, 4 * kBlock)), dim3(kBlock), 0, st,
+                           m.N, b.tok_slot, zr, b.zr_b);
     const size_t lds = 2 * (size_t)m.Kp * sizeof(int32_t);
     hipLaunchKernelGGL(k_rows, dim3((unsigned)rows), dim3(64), lds, st, m.V, m.Kp, b.row_off,
-                       b.perm, b.row_narrow, zr, b.nt, b.nt16, b.B, b.rep_part);
+                       b.perm, b.row_slot, b.zr_b, b.row_narrow, zr, b.nt, b.nt16, b.B,
+                       b.rep_part);
     return hipGetLastError();
 }
 
