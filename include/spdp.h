@@ -103,8 +103,10 @@ typedef struct {
  *   a      Pitman-Yor discount, 0 <= a < 1
  *   b      Pitman-Yor concentration, > 0
  *   gamma  symmetric Dirichlet prior of the shadow base phi0_k, > 0
- * Errors: E_ARG, E_NOMEM, E_HIP, E_RANGE (Stirling cache beyond 8 GiB, or a
- * (group, word) pair occurring 65536 times or more: counts are held in 16 bits).
+ * Errors: E_ARG, E_NOMEM, E_HIP, E_RANGE (a (group, word) pair occurring more
+ * than 32767 times: the samplers address the cached Stirling ratio pairs,
+ * tri(n) of them for n customers, with 32-bit byte offsets; the cache then
+ * takes 17.2 GB of device memory).
  * On success *out holds the new state; on error *out is NULL.
  */
 int spdp_create(const spdp_corpus *corpus, const spdp_groups *groups, int32_t K, double alpha,

@@ -34,7 +34,11 @@ int fail(int code, const char *fmt, ...)
             return fail(SPDP_E_HIP, "%s failed: %s", #expr, hipGetErrorString(e_));        \
     } while (0)
 
-constexpr int64_t kStirlingBudget = 8ll << 30;  // bytes for log S + fp32 and fp64 ratio pairs
+constexpr int64_t kStirlingBudget = 20ll << 30;  // bytes for log S + fp32 and fp64 ratio pairs
+// The samplers address the fp32 ratio pairs with 32-bit byte offsets, so the
+// pair table holds at most 2^29 pairs: tri(ncap) <= 2^29, i.e. ncap <= 32767
+// (17.2 GB of tables at that size).
+constexpr int32_t kMaxNcap = 32767;
 
 struct EventPair {
     hipEvent_t a, b;
@@ -427,8 +431,10 @@ int create_state(const spdp_corpus *corpus, const spdp_groups *groups, const spd
     // Stirling cache
     const int64_t n_logS = tri_index(m.ncap + 1, 0);  // rows 0..ncap
     const int64_t n_Q = tri_index(m.ncap, 0);         // rows 0..ncap-1
-    if (n_logS * 8 + n_Q * 24 > kStirlingBudget || m.ncap >= 65535)
-        TRY(fail(SPDP_E_RANGE, "Stirling cache for %d customers exceeds its budget", m.ncap));
+    if (m.ncap > kMaxNcap || n_logS * 8 + n_Q * 24 > kStirlingBudget)
+        TRY(fail(SPDP_E_RANGE,
+                 "a (group, word) pair occurs %d times; the Stirling cache covers at most %d",
+                 m.ncap, kMaxNcap));
     TRY(dev_alloc(s, &B.logS, n_logS, "log Stirling table"));
     TRY(dev_alloc(s, &B.Q, n_Q, "Stirling ratio pairs"));
     TRY(dev_alloc(s, &B.Q64, n_Q, "fp64 Stirling ratio pairs"));

@@ -189,3 +189,35 @@ def test_narrow_and_wide_rows_at_every_lane_layout(K):
         say(f"  {rep}")
     assert s.check() == 0
     s.close()
+
+
+def test_stirling_cache_above_23k_customers():
+    """A (group, word) pair with 24 000 tokens, above the 23 170 at which the
+    fp32 ratio pairs pass 2^31 bytes: the sampler's 32-bit byte offsets into
+    them reach 2.3 GB.  Weights, draws and the rebuild match the oracle over
+    two sweeps; a pair with 32 768 tokens is refused with E_RANGE (the
+    offsets would pass 4 GiB)."""
+    from paper_1510_06549_amd import spdp as sp
+
+    say("Stirling cache for 24000 customers")
+    rng = np.random.default_rng(11)
+    docs = []
+    for _ in range(3):
+        d = [0] * 8000 + list(rng.integers(1, 5, size=30))
+        rng.shuffle(d)
+        docs.append((0, d))
+    cp = corpus_from_docs(docs, vocab=5)
+    wl = W(K=3, alpha=0.5, a=0.5, b=20.0, gamma=0.1)
+    s, m = parity.make_pair(cp, wl)
+    assert s.info["ncap"] == 24000
+    for sw in range(2):
+        rep, _, _ = parity.one_step(s, m, sw, 29)
+        say(f"  sweep {sw}: {rep}")
+    assert s.check() == 0
+    s.close()
+    say("a pair with 32768 tokens is refused")
+    words = np.zeros(32768, np.int32)
+    with pytest.raises(sp.SpdpError) as e:
+        sp.spdp_create(words, np.array([0, 32768], np.int64), np.array([0], np.int32), 1, 2, 3,
+                       0.1, 0.5, 1.0, 0.1)
+    assert e.value.code == sp.SPDP_E_RANGE
