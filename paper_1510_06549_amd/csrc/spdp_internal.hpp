@@ -230,9 +230,9 @@ hipError_t launch_pack_zrs(const Model &m, const DeviceBuffers &b, const int32_t
 hipError_t launch_unpack_slot(const Model &m, const int32_t *zr, uint8_t *s, hipStream_t st);
 hipError_t launch_unpack_counts(const Model &m, const DeviceBuffers &b, int32_t g,
                                 int32_t *n_out, int32_t *t_out, hipStream_t st);
-// invariant check of the count state (count rows against a recount of the
-// tokens' states, both copies of narrow rows, the shadow base, the totals):
-// the number of failing cells or totals is added to *bad
+// invariant check of the count state (count rows, in the copy the rebuild
+// writes, against a recount of the tokens' states; the shadow base; the
+// totals): the number of failing cells or totals is added to *bad
 hipError_t launch_check(const Model &m, const DeviceBuffers &b, const int32_t *zr,
                         int32_t *scratch_totals, unsigned long long *bad, hipStream_t st);
 hipError_t launch_stat_sums(const Model &m, const DeviceBuffers &b, const int32_t *zr_now,
