@@ -104,9 +104,9 @@ typedef struct {
  *   b      Pitman-Yor concentration, > 0
  *   gamma  symmetric Dirichlet prior of the shadow base phi0_k, > 0
  * Errors: E_ARG, E_NOMEM, E_HIP, E_RANGE (a (group, word) pair occurring more
- * than 32767 times: the samplers address the cached Stirling ratio pairs,
- * tri(n) of them for n customers, with 32-bit byte offsets; the cache then
- * takes 17.2 GB of device memory).
+ * than 65535 times: counts are held in 16 bits).  The Stirling cache takes
+ * about 16 (ncap + 1)^2 bytes of device memory for ncap customers of the most
+ * frequent pair: 17.2 GB at 32767, 68.7 GB at 65535.
  * On success *out holds the new state; on error *out is NULL.
  */
 int spdp_create(const spdp_corpus *corpus, const spdp_groups *groups, int32_t K, double alpha,

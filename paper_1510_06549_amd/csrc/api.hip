@@ -34,11 +34,11 @@ int fail(int code, const char *fmt, ...)
             return fail(SPDP_E_HIP, "%s failed: %s", #expr, hipGetErrorString(e_));        \
     } while (0)
 
-constexpr int64_t kStirlingBudget = 20ll << 30;  // bytes for log S + fp32 and fp64 ratio pairs
-// The samplers address the fp32 ratio pairs with 32-bit byte offsets, so the
-// pair table holds at most 2^29 pairs: tri(ncap) <= 2^29, i.e. ncap <= 32767
-// (17.2 GB of tables at that size).
-constexpr int32_t kMaxNcap = 32767;
+constexpr int64_t kStirlingBudget = 72ll << 30;  // bytes for log S + fp32 and fp64 ratio pairs
+// The cache covers every n the packed counts can hold (68.7 GB of tables at
+// ncap = 65535); past 2^29 fp32 ratio pairs (ncap > 32767) the samplers
+// address them with 64-bit instead of 32-bit offsets.
+constexpr int32_t kMaxNcap = kCountMax;
 
 struct EventPair {
     hipEvent_t a, b;

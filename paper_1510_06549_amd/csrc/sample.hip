@@ -174,7 +174,7 @@ __device__ __forceinline__ void load_stream(const SampleArgs &A, DocWave<KPL> &W
 
 // Token cb + x: sample it with the rows in `cur` and request the rows of the
 // token two places ahead into `fill`.
-template <int KPL, bool TRACE, bool WIDE>
+template <int KPL, bool TRACE, bool WIDE, bool BIGQ>
 __device__ __forceinline__ void sample_token(const SampleArgs &A, DocWave<KPL> &W, int32_t x,
                                              Rows<KPL, WIDE> &cur, Rows<KPL, WIDE> &fill)
 {
@@ -200,8 +200,13 @@ __device__ __forceinline__ void sample_token(const SampleArgs &A, DocWave<KPL> &
         const uint32_t cn = v & kCountMax, ct = v >> kCountBits;
         uint32_t ix = ((cn * (cn + 1)) >> 1) + ct;
         ix = ix < q_last ? ix : q_last;
-        // (byte offsets fit in 32 bits: the ratio table is below 4 GiB)
-        qv[j] = *reinterpret_cast<const float2 *>(reinterpret_cast<const char *>(A.Q) + (ix << 3));
+        // 32-bit byte offsets while the ratio table is below 4 GiB (2^29 pairs),
+        // else 64-bit addresses
+        if constexpr (BIGQ)
+            qv[j] = A.Q[ix];
+        else
+            qv[j] = *reinterpret_cast<const float2 *>(reinterpret_cast<const char *>(A.Q) +
+                                                      (ix << 3));
     }
     // removed-customer constants of the own topic (a small table that stays
     // in cache; requested with the gathers)
@@ -370,7 +375,7 @@ __device__ __forceinline__ void sample_token(const SampleArgs &A, DocWave<KPL> &
 
 // Launched twice per sweep, once per width of the shadow-base rows; the
 // launch that does not match the flag set by the count rebuild returns.
-template <int KPL, bool TRACE, bool WIDE>
+template <int KPL, bool TRACE, bool WIDE, bool BIGQ>
 __global__ void __launch_bounds__(64, (KPL <= 8 ? 4 : 2)) k_sample(SampleArgs A)
 {
     // live document row c[k], the group's per-topic constants f0, f1 and the
@@ -444,25 +449,32 @@ __global__ void __launch_bounds__(64, (KPL <= 8 ? 4 : 2)) k_sample(SampleArgs A)
             x = 0;
             load_stream<KPL>(A, W, last);
         }
-        sample_token<KPL, TRACE, WIDE>(A, W, x, ra, rc);
-        if (i + 1 < end) sample_token<KPL, TRACE, WIDE>(A, W, x + 1, rb, ra);
-        if (i + 2 < end) sample_token<KPL, TRACE, WIDE>(A, W, x + 2, rc, rb);
+        sample_token<KPL, TRACE, WIDE, BIGQ>(A, W, x, ra, rc);
+        if (i + 1 < end) sample_token<KPL, TRACE, WIDE, BIGQ>(A, W, x + 1, rb, ra);
+        if (i + 2 < end) sample_token<KPL, TRACE, WIDE, BIGQ>(A, W, x + 2, rc, rb);
     }
     if (lane < end - W.cb) A.zr_new[W.cb + lane] = W.out_c;
+}
+
+template <int KPL, bool BIGQ>
+hipError_t launch_kpl_q(const SampleArgs &A, bool trace, hipStream_t st)
+{
+    const unsigned grid = (unsigned)(8 * A.docs_per_xcd);
+    if (trace) {
+        hipLaunchKernelGGL((k_sample<KPL, true, false, BIGQ>), dim3(grid), dim3(64), 0, st, A);
+        hipLaunchKernelGGL((k_sample<KPL, true, true, BIGQ>), dim3(grid), dim3(64), 0, st, A);
+    } else {
+        hipLaunchKernelGGL((k_sample<KPL, false, false, BIGQ>), dim3(grid), dim3(64), 0, st, A);
+        hipLaunchKernelGGL((k_sample<KPL, false, true, BIGQ>), dim3(grid), dim3(64), 0, st, A);
+    }
+    return hipGetLastError();
 }
 
 template <int KPL>
 hipError_t launch_kpl(const SampleArgs &A, bool trace, hipStream_t st)
 {
-    const unsigned grid = (unsigned)(8 * A.docs_per_xcd);
-    if (trace) {
-        hipLaunchKernelGGL((k_sample<KPL, true, false>), dim3(grid), dim3(64), 0, st, A);
-        hipLaunchKernelGGL((k_sample<KPL, true, true>), dim3(grid), dim3(64), 0, st, A);
-    } else {
-        hipLaunchKernelGGL((k_sample<KPL, false, false>), dim3(grid), dim3(64), 0, st, A);
-        hipLaunchKernelGGL((k_sample<KPL, false, true>), dim3(grid), dim3(64), 0, st, A);
-    }
-    return hipGetLastError();
+    return A.nQ > kSmallQ ? launch_kpl_q<KPL, true>(A, trace, st)
+                          : launch_kpl_q<KPL, false>(A, trace, st);
 }
 
 }  // namespace

@@ -237,7 +237,7 @@ __device__ void exact_topic(const ExactCtx &X, int32_t k, int32_t k0, int32_t r0
 
 // Token cb + x: sample it with the rows in `cur` and request the rows of the
 // next token into `fill`.
-template <int KPL, int SP, bool WIDE>
+template <int KPL, int SP, bool WIDE, bool BIGQ>
 __device__ __forceinline__ void sample_token_assoc(const AssocArgs &A, AWave<KPL, SP> &W,
                                                    int32_t x, ARows<KPL, SP, WIDE> &cur,
                                                    ARows<KPL, SP, WIDE> &fill)
@@ -262,7 +262,11 @@ __device__ __forceinline__ void sample_token_assoc(const AssocArgs &A, AWave<KPL
         const uint32_t cn = v & kCountMax, ct = v >> kCountBits;
         uint32_t ix = ((cn * (cn + 1)) >> 1) + ct;
         ix = ix < q_last ? ix : q_last;
-        qv[j] = *reinterpret_cast<const float2 *>(reinterpret_cast<const char *>(A.Q) + (ix << 3));
+        if constexpr (BIGQ)
+            qv[j] = A.Q[ix];
+        else
+            qv[j] = *reinterpret_cast<const float2 *>(reinterpret_cast<const char *>(A.Q) +
+                                                      (ix << 3));
     }
     const float f0k = A.fk[as_vector(W.gK + k0)];
     const float f1k = A.fk[as_vector((int64_t)(1 + r0) * A.GK + W.gK + k0)];
@@ -513,7 +517,7 @@ constexpr int assoc_waves()
 
 // Launched twice per sweep, once per width of the shadow-base rows; the
 // launch that does not match the flag set by the rebuild returns.
-template <int KPL, int SP, bool WIDE>
+template <int KPL, int SP, bool WIDE, bool BIGQ>
 __global__ void __launch_bounds__(64, (assoc_waves<KPL, SP, WIDE>())) k_sample_assoc(AssocArgs A)
 {
     __shared__ int32_t c_lds[64 * KPL];
@@ -579,8 +583,8 @@ __global__ void __launch_bounds__(64, (assoc_waves<KPL, SP, WIDE>())) k_sample_a
             x = 0;
             load_astream<KPL, SP>(A, W, last);
         }
-        sample_token_assoc<KPL, SP, WIDE>(A, W, x, ra, rb);
-        if (i + 1 < end) sample_token_assoc<KPL, SP, WIDE>(A, W, x + 1, rb, ra);
+        sample_token_assoc<KPL, SP, WIDE, BIGQ>(A, W, x, ra, rb);
+        if (i + 1 < end) sample_token_assoc<KPL, SP, WIDE, BIGQ>(A, W, x + 1, rb, ra);
     }
     if (lane < end - W.cb) A.zr_new[W.cb + lane] = W.out_c;
 }
@@ -589,8 +593,13 @@ template <int KPL, int SP>
 hipError_t launch_assoc_kpl(const AssocArgs &A, hipStream_t st)
 {
     const unsigned grid = (unsigned)(8 * A.docs_per_xcd);
-    hipLaunchKernelGGL((k_sample_assoc<KPL, SP, false>), dim3(grid), dim3(64), 0, st, A);
-    hipLaunchKernelGGL((k_sample_assoc<KPL, SP, true>), dim3(grid), dim3(64), 0, st, A);
+    if (A.nQ > kSmallQ) {
+        hipLaunchKernelGGL((k_sample_assoc<KPL, SP, false, true>), dim3(grid), dim3(64), 0, st, A);
+        hipLaunchKernelGGL((k_sample_assoc<KPL, SP, true, true>), dim3(grid), dim3(64), 0, st, A);
+    } else {
+        hipLaunchKernelGGL((k_sample_assoc<KPL, SP, false, false>), dim3(grid), dim3(64), 0, st, A);
+        hipLaunchKernelGGL((k_sample_assoc<KPL, SP, true, false>), dim3(grid), dim3(64), 0, st, A);
+    }
     return hipGetLastError();
 }
 

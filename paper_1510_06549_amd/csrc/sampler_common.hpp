@@ -7,6 +7,10 @@
 
 namespace spdp {
 
+// Ratio pairs addressable with 32-bit byte offsets (a 4 GiB table): the
+// samplers use 64-bit addresses only for a table past this.
+constexpr int64_t kSmallQ = 1ll << 29;
+
 // KPL consecutive int32 of one row, loaded with the widest aligned vector
 // loads; chunks that start at or beyond the row length are zero.
 template <int KPL>

@@ -195,29 +195,41 @@ def test_stirling_cache_above_23k_customers():
     """A (group, word) pair with 24 000 tokens, above the 23 170 at which the
     fp32 ratio pairs pass 2^31 bytes: the sampler's 32-bit byte offsets into
     them reach 2.3 GB.  Weights, draws and the rebuild match the oracle over
-    two sweeps; a pair with 32 768 tokens is refused with E_RANGE (the
-    offsets would pass 4 GiB)."""
+    two sweeps."""
+    check_large_pair(24000, 11)
+
+
+def test_stirling_cache_past_2_29_ratio_pairs():
+    """A (group, word) pair with 33 000 tokens: 544 M ratio pairs, past the 2^29
+    that 32-bit byte offsets reach, so the samplers' 64-bit-address instance
+    runs (17.4 GB of tables).  Weights, draws and the rebuild match the oracle
+    over two sweeps; a pair with 65 536 tokens, which 16-bit counts cannot
+    hold, is refused with E_RANGE."""
     from paper_1510_06549_amd import spdp as sp
 
-    say("Stirling cache for 24000 customers")
-    rng = np.random.default_rng(11)
+    check_large_pair(33000, 13)
+    say("a pair with 65536 tokens is refused")
+    words = np.zeros(65536, np.int32)
+    with pytest.raises(sp.SpdpError) as e:
+        sp.spdp_create(words, np.array([0, 65536], np.int64), np.array([0], np.int32), 1, 2, 3,
+                       0.1, 0.5, 1.0, 0.1)
+    assert e.value.code == sp.SPDP_E_RANGE
+
+
+def check_large_pair(count, seed):
+    say(f"Stirling cache for {count} customers")
+    rng = np.random.default_rng(seed)
     docs = []
     for _ in range(3):
-        d = [0] * 8000 + list(rng.integers(1, 5, size=30))
+        d = [0] * (count // 3) + list(rng.integers(1, 5, size=30))
         rng.shuffle(d)
         docs.append((0, d))
     cp = corpus_from_docs(docs, vocab=5)
     wl = W(K=3, alpha=0.5, a=0.5, b=20.0, gamma=0.1)
     s, m = parity.make_pair(cp, wl)
-    assert s.info["ncap"] == 24000
+    assert s.info["ncap"] == count
     for sw in range(2):
         rep, _, _ = parity.one_step(s, m, sw, 29)
         say(f"  sweep {sw}: {rep}")
     assert s.check() == 0
     s.close()
-    say("a pair with 32768 tokens is refused")
-    words = np.zeros(32768, np.int32)
-    with pytest.raises(sp.SpdpError) as e:
-        sp.spdp_create(words, np.array([0, 32768], np.int64), np.array([0], np.int32), 1, 2, 3,
-                       0.1, 0.5, 1.0, 0.1)
-    assert e.value.code == sp.SPDP_E_RANGE
