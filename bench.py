@@ -532,6 +532,10 @@ def main():
         pass
     elif assoc is None:
         roofline["narrow_row_token_share"] = round(narrow, 4)
+        # context: the same launch time in the bytes of the layout without
+        # narrow rows (32-bit count rows for every token)
+        roofline["all_rows_32bit_equiv_GBps"] = round(
+            N * sample_bytes_per_token(wl.K, wide, 0.0) / avg_sample_s / 1e9, 1)
         roofline["dense_int32_bytes_per_token"] = dense_bytes_per_token(wl.K)
         roofline["dense_int32_equiv_GBps"] = round(
             N * dense_bytes_per_token(wl.K) / avg_sample_s / 1e9, 1)
