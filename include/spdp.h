@@ -378,11 +378,12 @@ int spdp_check(spdp_state *s, int64_t *bad);
 
 /*
  * Test hook: add dn customers and dt tables to the stored count cell of
- * (group g, word w, topic k) -- the 32-bit row only, nothing else -- so that
- * tests can make the state inconsistent and see spdp_check report it (any
- * later rebuild, e.g. spdp_set_assignments, restores consistent counts).
+ * (group g, word w, topic k) -- in the copy the samplers read (the 16-bit
+ * copy of a narrow row, else the 32-bit row), nothing else -- so that tests
+ * can make the state inconsistent and see spdp_check report it (any later
+ * rebuild, e.g. spdp_set_assignments, restores consistent counts).
  * Synchronises.  Errors: E_ARG (cell out of range, or a count would leave
- * [0, 65535]), E_HIP.
+ * [0, 255] in a narrow row or [0, 65535] in a wide one), E_HIP.
  */
 int spdp_debug_poke(spdp_state *s, int32_t g, int32_t w, int32_t k, int32_t dn, int32_t dt);
 

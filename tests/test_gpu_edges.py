@@ -216,8 +216,16 @@ def test_stirling_cache_past_2_29_ratio_pairs():
     assert e.value.code == sp.SPDP_E_RANGE
 
 
-def check_large_pair(count, seed):
-    say(f"Stirling cache for {count} customers")
+def test_stirling_cache_past_2_29_ratio_pairs_with_word_associations():
+    """The association sampler's 64-bit-address instance: the same 33 000-token
+    pair under P = 0.7 I + 0.3 Pi (two sources in every row: word 0 lists
+    itself and word 4), so new tables of word 0 draw either source.  Weights,
+    draws, sources and the rebuild match the oracle over two sweeps."""
+    check_large_pair(33000, 18, sources=2)
+
+
+def check_large_pair(count, seed, sources=0):
+    say(f"Stirling cache for {count} customers" + (f", {sources} sources" if sources else ""))
     rng = np.random.default_rng(seed)
     docs = []
     for _ in range(3):
@@ -226,8 +234,9 @@ def check_large_pair(count, seed):
         docs.append((0, d))
     cp = corpus_from_docs(docs, vocab=5)
     wl = W(K=3, alpha=0.5, a=0.5, b=20.0, gamma=0.1)
-    s, m = parity.make_pair(cp, wl)
-    assert s.info["ncap"] == count
+    assoc = synth.associations(1, 5, sources, 0.3, seed) if sources else None
+    s, m = parity.make_pair(cp, wl, assoc=assoc)
+    assert s.info["ncap"] == count and s.S == sources
     for sw in range(2):
         rep, _, _ = parity.one_step(s, m, sw, 29)
         say(f"  sweep {sw}: {rep}")
