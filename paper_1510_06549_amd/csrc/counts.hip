@@ -55,7 +55,7 @@ template <typename F>
 __device__ __forceinline__ void for_row_states(int32_t rs, int32_t re, int32_t lane,
                                                const int32_t *__restrict__ perm,
                                                const int32_t *__restrict__ row_slot,
-                                               const int32_t *__restrict__ zr_b, F &&f)
+                                               const uint16_t *__restrict__ zr_b, F &&f)
 {
     int32_t j = rs + lane;
     for (; j + 192 < re; j += 256) {
@@ -66,11 +66,11 @@ __device__ __forceinline__ void for_row_states(int32_t rs, int32_t re, int32_t l
             s[u] = row_slot[j + 64 * u];
         }
 #pragma unroll
-        for (int u = 0; u < 4; ++u) v[u] = zr_b[s[u]];
+        for (int u = 0; u < 4; ++u) v[u] = (int32_t)zr_b[s[u]];
 #pragma unroll
         for (int u = 0; u < 4; ++u) f(t[u], v[u]);
     }
-    for (; j < re; j += 64) f(perm[j], zr_b[row_slot[j]]);
+    for (; j < re; j += 64) f(perm[j], (int32_t)zr_b[row_slot[j]]);
 }
 
 // The same, gathering each state from token order (the word-association
@@ -103,10 +103,13 @@ __device__ __forceinline__ void for_row_states_direct(int32_t rs, int32_t re, in
 // order fetches a whole line per state; instead the plain model's rebuild
 // first copies the states (k_route, coalesced reads, writes in runs) into
 // zr_b, where the states of each bucket of rows (the rows starting in one
-// window of 2^kRouteShift row positions, about 4 MB of states) occupy that
-// bucket's range of row positions, so that the rows' gathers stay within a
-// region that fits the cache.  The route is static: fixed with the row index.
-constexpr int kRouteShift = 20;
+// window of 2^kRouteShift row positions) occupy that bucket's range of row
+// positions, so that the rows' gathers stay within a region that fits the
+// cache.  Without word associations a state is z << 1 | r < 2^11 (K <= 1024),
+// so the copy holds it in 16 bits: a bucket is about 4 MB, and a cache line
+// serves 64 states.  The route is static: fixed with the row index.
+constexpr int kRouteShift = 21;
+static_assert(2 * SPDP_MAX_K - 1 <= 0xFFFF, "a state without a source slot fits in 16 bits");
 constexpr int kRouteThreads = 1024;
 
 // start of each bucket's range: the smallest start of its non-empty rows
@@ -154,10 +157,10 @@ __global__ void k_compose(int64_t N, const int32_t *__restrict__ perm,
     if (j < N) row_slot[j] = tok_slot[perm[j]];
 }
 
-// zr_b[tok_slot[i]] = zr[i], four tokens per thread
+// zr_b[tok_slot[i]] = zr[i] (as 16 bits), four tokens per thread
 __global__ void __launch_bounds__(kBlock) k_route(int64_t N, const int32_t *__restrict__ tok_slot,
                                                   const int32_t *__restrict__ zr,
-                                                  int32_t *__restrict__ zr_b)
+                                                  uint16_t *__restrict__ zr_b)
 {
     const int64_t i0 = (int64_t)blockIdx.x * (4 * kBlock) + threadIdx.x;
     int32_t d[4], v[4];
@@ -169,7 +172,7 @@ __global__ void __launch_bounds__(kBlock) k_route(int64_t N, const int32_t *__re
     }
 #pragma unroll
     for (int u = 0; u < 4; ++u)
-        if (d[u] >= 0) zr_b[d[u]] = v[u];
+        if (d[u] >= 0) zr_b[d[u]] = (uint16_t)v[u];
 }
 
 // One 64-lane block per count row; the row's histogram and the smallest token
@@ -182,7 +185,7 @@ __global__ void __launch_bounds__(64) k_rows(int32_t V, int32_t Kp,
                                              const int32_t *__restrict__ row_off,
                                              const int32_t *__restrict__ perm,
                                              const int32_t *__restrict__ row_slot,
-                                             const int32_t *__restrict__ zr_b,
+                                             const uint16_t *__restrict__ zr_b,
                                              const uint8_t *__restrict__ row_narrow,
                                              int32_t *__restrict__ zr, int32_t *__restrict__ nt,
                                              uint16_t *__restrict__ nt16, int32_t *__restrict__ B,

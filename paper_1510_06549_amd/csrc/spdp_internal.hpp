@@ -147,9 +147,10 @@ struct DeviceBuffers {
     int32_t *row_off = nullptr;   // [G V + 1] offsets of each row's tokens in perm
     int32_t *tok_slot = nullptr;  // [N] each token's slot in the routed state copy zr_b
     int32_t *row_slot = nullptr;  // [N] the slot of row list entry j: tok_slot[perm[j]]
-    int32_t *zr_b = nullptr;      // [N] the states routed by row bucket, rewritten by every
-                                  // rebuild before it gathers from them (plain model only:
-                                  // null with word associations)
+    uint16_t *zr_b = nullptr;     // [N] the states routed by row bucket, as 16 bits (a state
+                                  // without a source slot is z << 1 | r < 2^11), rewritten
+                                  // by every rebuild before it gathers from them (plain
+                                  // model only: null with word associations)
     int32_t *Ngk = nullptr;       // [G][Kp]
     int32_t *Tgk = nullptr;       // [G][Kp]
     int32_t *Bk = nullptr;        // [Kp]
