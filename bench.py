@@ -95,6 +95,18 @@ def dense_bytes_per_token(K: int) -> int:
     return 12 * K + 12
 
 
+def shadow_base_wide(s) -> bool:
+    """True when some shadow-base count exceeds 65535 (the samplers then read
+    the 32-bit rows of B), from B copied on the device and reduced there."""
+    import torch
+
+    from paper_1510_06549_amd import spdp as sp
+
+    B = torch.empty((s.V, s.K), dtype=torch.int32, device="cuda")
+    sp.spdp_totals(s.h, None, None, B, None)
+    return bool(B.max().item() > 0xFFFF)
+
+
 def kernel_source_hash(kernel: str) -> str:
     """SHA-256 of the sources a sampling kernel is compiled from: its own file,
     then the two headers that file includes."""
@@ -473,7 +485,7 @@ def main():
     torch.cuda.synchronize()
     log(f"[bench] {args.warmup} warm-up sweep(s) done")
     # width of the shadow-base rows the timed sweeps read (set by each rebuild)
-    wide = bool(s.totals()[2].max() > 0xFFFF)
+    wide = shadow_base_wide(s)
 
     sp.spdp_kernel_timing(s.h, True)
     torch.cuda.synchronize()
@@ -485,7 +497,7 @@ def main():
     kt = sp.spdp_kernel_times(s.h)
     sp.spdp_kernel_timing(s.h, False)
     changed, repaired = s.stats()
-    wide = wide or bool(s.totals()[2].max() > 0xFFFF)
+    wide = wide or shadow_base_wide(s)
     log(f"[bench] {args.steps} timed sweeps in {elapsed:.3f}s; kernel ms {kt}; "
         f"last sweep changed={changed} repaired={repaired}")
 
