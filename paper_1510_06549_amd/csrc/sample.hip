@@ -181,6 +181,12 @@ __device__ __forceinline__ void sample_token(const SampleArgs &A, DocWave<KPL> &
     constexpr int NO = 2 * KPL;  // outcomes per lane
     const int32_t lane = W.lane, kbase = W.kbase;
     const int64_t i = W.cb + x;
+    // Wave priorities: the part of a token that issues its loads (the ratio
+    // gathers and the rows two tokens ahead) runs at priority 2 and the serial
+    // scan and draw at 3, above the weight loops (priority 0) of the other
+    // wavefronts on the SIMD, so that a wavefront's loads leave and its draw
+    // resolves without queueing behind their vector work.
+    __builtin_amdgcn_s_setprio(2);
     if (readlane(W.nar_c, x)) widen_cells<KPL>(cur.n, kbase);
 
     const int32_t zr0 = readlane(W.zr_c, x);
@@ -217,6 +223,7 @@ __device__ __forceinline__ void sample_token(const SampleArgs &A, DocWave<KPL> &
     // does not wait for them
     asm volatile("" ::: "memory");
     load_rows<KPL, WIDE>(A, W, x + 2, fill);
+    __builtin_amdgcn_s_setprio(0);
     // only head of a cell that keeps other customers: point mass
     const int32_t nt0 = readlane(own_nt, k0 / KPL);
     const bool sole = r0 && (nt0 >> kCountBits) == 1 && (nt0 & kCountMax) > 1;
@@ -253,6 +260,7 @@ __device__ __forceinline__ void sample_token(const SampleArgs &A, DocWave<KPL> &
             acc += w0;
             s[2 * j + 1] = acc;
         }
+        __builtin_amdgcn_s_setprio(3);
         const float incl = wave_inclusive_sum(acc);
         const float excl = wave_shift_right(incl);
         const float total = readlane_f(incl, 63);
@@ -350,6 +358,7 @@ __device__ __forceinline__ void sample_token(const SampleArgs &A, DocWave<KPL> &
                 }
             }
         }
+        __builtin_amdgcn_s_setprio(0);
         if (jstar >= 0) {
             const int32_t k1 = jstar >> 1, r1 = 1 - (jstar & 1);
             result = zr_pack(k1, r1);

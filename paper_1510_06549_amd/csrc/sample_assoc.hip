@@ -328,6 +328,10 @@ __device__ __forceinline__ void sample_token_assoc(const AssocArgs &A, AWave<KPL
             o[A.S] = sole ? 0.0f : __fmul_rn(own ? m0k0 : a0[j], qv[j].x);
         }
     }
+    // the serial scan and draw at wave priority 3, above the weight loops of
+    // the other wavefronts on the SIMD, so that the draw resolves without
+    // queueing behind their vector work
+    __builtin_amdgcn_s_setprio(3);
     const float incl = wave_inclusive_sum(acc);
     const float excl = wave_shift_right(incl);
     const float total = readlane_f(incl, 63);
@@ -483,6 +487,7 @@ __device__ __forceinline__ void sample_token_assoc(const AssocArgs &A, AWave<KPL
             s1 = s0;
         }
     }
+    __builtin_amdgcn_s_setprio(0);
     // DS operations of one wave execute in order, so the next token's reads of
     // the LDS rows see this update
     if (lane == 0 && k1 != k0) {
