@@ -203,10 +203,14 @@ __global__ void __launch_bounds__(64) k_rows(int32_t V, int32_t Kp,
             first[k] = INT_MAX;
         }
         __syncthreads();
+        // the gathers at wave priority 2, so that a row's loads leave ahead of
+        // the other wavefronts' row writes
+        __builtin_amdgcn_s_setprio(2);
         for_row_states(rs, re, lane, perm, row_slot, zr_b, [&](int32_t tok, int32_t v) {
             atomicAdd(&h[v >> 1], 1 + ((v & 1) << 16));
             atomicMin(&first[v >> 1], tok);
         });
+        __builtin_amdgcn_s_setprio(0);
         __syncthreads();
         int32_t *__restrict__ row = nt + q * Kp;
         uint16_t *__restrict__ row16 = nt16 + q * Kp;
