@@ -108,15 +108,18 @@ def shadow_base_wide(s) -> bool:
 
 
 def kernel_source_hash(kernel: str) -> str:
-    """SHA-256 of the sources a sampling kernel is compiled from: its own file,
-    then the two headers that file includes."""
+    """SHA-256 of what a sampling kernel is compiled from: its own file, the
+    two headers that file includes, then the file's compiler flags."""
     import hashlib
+
+    from paper_1510_06549_amd import build_lib
 
     csrc = os.path.join(ROOT, "paper_1510_06549_amd", "csrc")
     source = {"k_sample": "sample.hip", "k_sample_assoc": "sample_assoc.hip"}[kernel]
     h = hashlib.sha256()
     for name in (source, "sampler_common.hpp", "spdp_internal.hpp"):
         h.update(open(os.path.join(csrc, name), "rb").read())
+    h.update(" ".join(build_lib.source_flags(source)).encode())
     return h.hexdigest()
 
 
