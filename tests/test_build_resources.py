@@ -1,0 +1,56 @@
+"""Register budget of the sampling kernel, checked at compile time on the CPU.
+
+The per-sweep sampler runs at 4 wavefronts per SIMD with its three row
+buffers and token stream in registers.  A source edit (or the machine
+scheduler chosen for sample.hip in build_lib) can make the compiler spill
+into scratch memory inside the token loop, which slows the kernel by a
+large factor while every parity test still passes.  This test compiles
+sample.hip for gfx950 with the library's own flags and requires, for every
+instance the sweeps launch with 16-bit shadow-base rows and without the
+debug trace, no scratch memory and at most 128 VGPRs (4 wavefronts per
+SIMD) for up to 8 topics per lane.
+"""
+import os
+import re
+import shutil
+import subprocess
+
+import pytest
+
+from paper_1510_06549_amd import build_lib
+
+HIPCC = shutil.which("hipcc") or "/opt/rocm/bin/hipcc"
+
+
+def resource_usage(src):
+    """{kernel name: {"VGPRs": n, "ScratchSize": bytes}} from the compiler's
+    resource remarks for one source, compiled with its build flags."""
+    flags = [f for f in build_lib.source_flags(src) if f not in ("-fPIC", "-Wall")]
+    cmd = [HIPCC, *flags, "--cuda-device-only", "-c", os.path.join(build_lib.CSRC, src),
+           "-o", os.devnull, "-Rpass-analysis=kernel-resource-usage"]
+    out = subprocess.run(cmd, capture_output=True, text=True, timeout=600)
+    assert out.returncode == 0, out.stderr[-2000:]
+    usage, name = {}, None
+    for line in out.stderr.splitlines():
+        m = re.search(r"Function Name: (\S+)", line)
+        if m:
+            name = m.group(1)
+            usage[name] = {}
+            continue
+        m = re.search(r"remark:\s+(VGPRs|ScratchSize \[bytes/lane\]): (\d+)", line)
+        if m and name:
+            usage[name][m.group(1).split()[0]] = int(m.group(2))
+    return usage
+
+
+@pytest.mark.skipif(not os.path.exists(HIPCC), reason="hipcc not available")
+def test_sampler_hot_instances_do_not_spill():
+    usage = resource_usage("sample.hip")
+    # k_sample<KPL, TRACE = false, WIDE = false, BIGQ>
+    hot = {n: u for n, u in usage.items() if re.search(r"k_sampleILi\d+ELb0ELb0ELb[01]E", n)}
+    assert len(hot) == 12, sorted(usage)  # KPL in {1, 2, 4, 8, 12, 16}, both address widths
+    for name, u in hot.items():
+        assert u.get("ScratchSize", 0) == 0, (name, u)
+        kpl = int(re.search(r"k_sampleILi(\d+)E", name).group(1))
+        if kpl <= 8:
+            assert u["VGPRs"] <= 128, (name, u)
