@@ -54,3 +54,15 @@ def test_sampler_hot_instances_do_not_spill():
         kpl = int(re.search(r"k_sampleILi(\d+)E", name).group(1))
         if kpl <= 8:
             assert u["VGPRs"] <= 128, (name, u)
+
+
+@pytest.mark.skipif(not os.path.exists(HIPCC), reason="hipcc not available")
+def test_association_sampler_benchmark_instance_does_not_spill():
+    """The word-association sampler at 8 topics per lane and 4 sources per
+    word (K = 500 with four sources, the measured configuration) runs at 3
+    wavefronts per SIMD: no scratch memory and at most 170 VGPRs."""
+    usage = resource_usage("sample_assoc.hip")
+    hot = {n: u for n, u in usage.items() if re.search(r"k_sample_assocILi8ELi4ELb0ELb[01]E", n)}
+    assert len(hot) == 2, sorted(usage)
+    for name, u in hot.items():
+        assert u.get("ScratchSize", 0) == 0 and u["VGPRs"] <= 170, (name, u)
