@@ -179,9 +179,12 @@ __global__ void __launch_bounds__(kBlock) k_route(int64_t N, const int32_t *__re
 // index of each topic in LDS (2 Kp ints of dynamic shared memory).  Every
 // token's state is read once: a cell left with customers but no table holds
 // only r = 0 tokens, and its smallest-index token becomes its head.  Blocks
-// run in row order, so that the rows in flight together belong to one group,
-// whose states then stay in the last-level cache while they are gathered.
-__global__ void __launch_bounds__(64) k_rows(int32_t V, int32_t Kp,
+// are dealt to the 8 XCDs in turn; block b rebuilds row
+// (b mod 8) rows_per_xcd + b / 8, so that each XCD walks its own run of rows
+// in order and the bucket of routed states its rows gather from stays in that
+// XCD's L2 (blocks past the last row return).
+__global__ void __launch_bounds__(64) k_rows(int64_t rows, int64_t rows_per_xcd, int32_t V,
+                                             int32_t Kp,
                                              const int32_t *__restrict__ row_off,
                                              const int32_t *__restrict__ perm,
                                              const int32_t *__restrict__ row_slot,
@@ -193,7 +196,8 @@ __global__ void __launch_bounds__(64) k_rows(int32_t V, int32_t Kp,
 {
     extern __shared__ int32_t rows_lds[];
     int32_t *h = rows_lds, *first = rows_lds + Kp;
-    const int64_t q = blockIdx.x;
+    const int64_t q = (int64_t)(blockIdx.x & 7) * rows_per_xcd + (blockIdx.x >> 3);
+    if (q >= rows) return;
     const int32_t lane = threadIdx.x;
     const int32_t rs = row_off[q], re = row_off[q + 1];
     uint32_t rep = 0;
@@ -711,9 +715,10 @@ hipError_t launch_rows(const Model &m, const DeviceBuffers &b, int32_t *zr, hipS
         hipLaunchKernelGGL(k_route, dim3((unsigned)blocks_for(m.N, 4 * kBlock)), dim3(kBlock), 0, st,
                            m.N, b.tok_slot, zr, b.zr_b);
     const size_t lds = 2 * (size_t)m.Kp * sizeof(int32_t);
-    hipLaunchKernelGGL(k_rows, dim3((unsigned)rows), dim3(64), lds, st, m.V, m.Kp, b.row_off,
-                       b.perm, b.row_slot, b.zr_b, b.row_narrow, zr, b.nt, b.nt16, b.B,
-                       b.rep_part);
+    const int64_t rows_per_xcd = (rows + 7) / 8;
+    hipLaunchKernelGGL(k_rows, dim3((unsigned)(8 * rows_per_xcd)), dim3(64), lds, st, rows,
+                       rows_per_xcd, m.V, m.Kp, b.row_off, b.perm, b.row_slot, b.zr_b,
+                       b.row_narrow, zr, b.nt, b.nt16, b.B, b.rep_part);
     return hipGetLastError();
 }
 
