@@ -350,6 +350,8 @@ int create_state(const spdp_corpus *corpus, const spdp_groups *groups, const spd
     TRY(dev_alloc(s, &B.doc_group, D, "doc groups"));
     TRY(dev_alloc(s, &B.err, 2, "error flags"));
     TRY(dev_alloc(s, &B.ctr, 4, "counters"));
+    TRY(dev_alloc(s, &B.claim, 9, "document claims"));
+    TRY_HIP(launch_fill_i32(B.claim, 9, 0, s->st));
     TRY(dev_alloc(s, &B.scalar, 1, "scalar"));
     TRY_HIP(launch_fill_i32(B.err, 2, 0, s->st));
     {

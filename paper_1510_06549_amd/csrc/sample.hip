@@ -42,6 +42,8 @@ struct SampleArgs {
     const int32_t *B;
     const uint16_t *B16;
     const int32_t *wide;
+    int32_t *claim;  // [9] documents claimed per XCD by the persistent launch, and the
+                     // workgroups of that launch that have finished (zero between launches)
     const float *f0;
     const float *f1;
     const float *fk;
@@ -382,26 +384,15 @@ __device__ __forceinline__ void sample_token(const SampleArgs &A, DocWave<KPL> &
     if (lane == x) W.out_c = result;
 }
 
-// Launched twice per sweep, once per width of the shadow-base rows; the
-// launch that does not match the flag set by the count rebuild returns.
+// One document on the calling wavefront; the LDS arrays are the workgroup's
+// (the live document row c[k], the group's per-topic constants f0, f1 and the
+// products a0 = (alpha + c) f0, a1 = (alpha + c) f1, kept in step with c;
+// interleaved layout).
 template <int KPL, bool TRACE, bool WIDE, bool BIGQ>
-__global__ void __launch_bounds__(64, (KPL <= 8 ? 4 : 2)) k_sample(SampleArgs A)
+__device__ __forceinline__ void sample_doc(const SampleArgs &A, int32_t d, int32_t *c_lds,
+                                           float *f0_lds, float *f1_lds, float *a0_lds,
+                                           float *a1_lds)
 {
-    // live document row c[k], the group's per-topic constants f0, f1 and the
-    // products a0 = (alpha + c) f0, a1 = (alpha + c) f1 (kept in step with c;
-    // interleaved layout)
-    __shared__ int32_t c_lds[64 * KPL];
-    __shared__ float f0_lds[64 * KPL];
-    __shared__ float f1_lds[64 * KPL];
-    __shared__ __attribute__((aligned(16))) float a0_lds[64 * KPL];
-    __shared__ __attribute__((aligned(16))) float a1_lds[64 * KPL];
-
-    // blocks are dealt round-robin over the 8 XCDs; give each XCD a
-    // contiguous range of documents so a group's hot rows stay in its L2
-    if ((*A.wide != 0) != WIDE) return;
-    const int32_t b = blockIdx.x;
-    const int32_t d = (b & 7) * A.docs_per_xcd + (b >> 3);
-    if (d >= A.D) return;
     DocWave<KPL> W;
     const int64_t beg = A.doc_off[d];
     W.end = A.doc_off[d + 1];
@@ -465,16 +456,65 @@ __global__ void __launch_bounds__(64, (KPL <= 8 ? 4 : 2)) k_sample(SampleArgs A)
     if (lane < end - W.cb) A.zr_new[W.cb + lane] = W.out_c;
 }
 
+// Launched twice per sweep, once per width of the shadow-base rows; the
+// launch that does not match the flag set by the count rebuild returns.  The
+// 16-bit width (the common case) takes one workgroup per document; blocks are
+// dealt round-robin over the 8 XCDs, and each XCD gets a contiguous range of
+// documents so a group's hot rows stay in its L2.  The 32-bit width runs as a
+// persistent grid whose workgroups claim the documents of their XCD's range
+// one at a time, so that its launch costs almost nothing when it returns.
+template <int KPL, bool TRACE, bool WIDE, bool BIGQ>
+__global__ void __launch_bounds__(64, (KPL <= 8 ? 4 : 2)) k_sample(SampleArgs A)
+{
+    __shared__ int32_t c_lds[64 * KPL];
+    __shared__ float f0_lds[64 * KPL];
+    __shared__ float f1_lds[64 * KPL];
+    __shared__ __attribute__((aligned(16))) float a0_lds[64 * KPL];
+    __shared__ __attribute__((aligned(16))) float a1_lds[64 * KPL];
+
+    if ((*A.wide != 0) != WIDE) return;
+    if constexpr (!WIDE) {
+        const int32_t b = blockIdx.x;
+        const int32_t d = (b & 7) * A.docs_per_xcd + (b >> 3);
+        if (d >= A.D) return;
+        sample_doc<KPL, TRACE, WIDE, BIGQ>(A, d, c_lds, f0_lds, f1_lds, a0_lds, a1_lds);
+    } else {
+        const int32_t xcd = blockIdx.x & 7;
+        for (;;) {
+            int32_t i = 0;
+            if (threadIdx.x == 0) i = atomicAdd(&A.claim[xcd], 1);
+            i = __shfl(i, 0);
+            if (i >= A.docs_per_xcd) break;
+            const int32_t d = xcd * A.docs_per_xcd + i;
+            if (d >= A.D) break;
+            sample_doc<KPL, TRACE, WIDE, BIGQ>(A, d, c_lds, f0_lds, f1_lds, a0_lds, a1_lds);
+        }
+        // the last workgroup to finish clears the claims for the next launch
+        if (threadIdx.x == 0) {
+            __threadfence();
+            if (atomicAdd(&A.claim[8], 1) == (int32_t)gridDim.x - 1) {
+#pragma unroll 1
+                for (int u = 0; u < 9; ++u) A.claim[u] = 0;
+            }
+        }
+    }
+}
+
+// workgroups of the persistent launch: a wavefront slot each on 256 compute
+// units at 4 wavefronts per SIMD (fewer when the documents are fewer)
+constexpr int32_t kPersistentBlocks = 4096;
+
 template <int KPL, bool BIGQ>
 hipError_t launch_kpl_q(const SampleArgs &A, bool trace, hipStream_t st)
 {
     const unsigned grid = (unsigned)(8 * A.docs_per_xcd);
+    const unsigned pgrid = grid < (unsigned)kPersistentBlocks ? grid : (unsigned)kPersistentBlocks;
     if (trace) {
         hipLaunchKernelGGL((k_sample<KPL, true, false, BIGQ>), dim3(grid), dim3(64), 0, st, A);
-        hipLaunchKernelGGL((k_sample<KPL, true, true, BIGQ>), dim3(grid), dim3(64), 0, st, A);
+        hipLaunchKernelGGL((k_sample<KPL, true, true, BIGQ>), dim3(pgrid), dim3(64), 0, st, A);
     } else {
         hipLaunchKernelGGL((k_sample<KPL, false, false, BIGQ>), dim3(grid), dim3(64), 0, st, A);
-        hipLaunchKernelGGL((k_sample<KPL, false, true, BIGQ>), dim3(grid), dim3(64), 0, st, A);
+        hipLaunchKernelGGL((k_sample<KPL, false, true, BIGQ>), dim3(pgrid), dim3(64), 0, st, A);
     }
     return hipGetLastError();
 }
@@ -519,6 +559,7 @@ hipError_t launch_sample(const Model &m, const DeviceBuffers &b, const int32_t *
     A.B = b.B;
     A.B16 = b.B16;
     A.wide = b.wide;
+    A.claim = b.claim;
     A.f0 = b.f0;
     A.f1 = b.f1;
     A.fk = b.fk;

@@ -52,6 +52,8 @@ struct AssocArgs {
     const int32_t *B;
     const uint16_t *B16;
     const int32_t *wide;
+    int32_t *claim;  // [9] documents claimed per XCD by the persistent launch, and the
+                     // workgroups of that launch that have finished (zero between launches)
     const float *f0;
     const float *f1;
     const float *fk;
@@ -520,21 +522,13 @@ constexpr int assoc_waves()
     return w > 4 ? 4 : (w < 1 ? 1 : w);
 }
 
-// Launched twice per sweep, once per width of the shadow-base rows; the
-// launch that does not match the flag set by the rebuild returns.
+// One document on the calling wavefront, with the workgroup's LDS arrays (as
+// in the plain sampler).
 template <int KPL, int SP, bool WIDE, bool BIGQ>
-__global__ void __launch_bounds__(64, (assoc_waves<KPL, SP, WIDE>())) k_sample_assoc(AssocArgs A)
+__device__ __forceinline__ void sample_doc_assoc(const AssocArgs &A, int32_t d, int32_t *c_lds,
+                                                 float *f0_lds, float *f1_lds, float *a0_lds,
+                                                 float *a1_lds)
 {
-    __shared__ int32_t c_lds[64 * KPL];
-    __shared__ float f0_lds[64 * KPL];
-    __shared__ float f1_lds[64 * KPL];
-    __shared__ __attribute__((aligned(16))) float a0_lds[64 * KPL];
-    __shared__ __attribute__((aligned(16))) float a1_lds[64 * KPL];
-
-    if ((*A.wide != 0) != WIDE) return;
-    const int32_t bidx = blockIdx.x;
-    const int32_t d = (bidx & 7) * A.docs_per_xcd + (bidx >> 3);
-    if (d >= A.D) return;
     AWave<KPL, SP> W;
     const int64_t beg = A.doc_off[d];
     W.end = A.doc_off[d + 1];
@@ -594,16 +588,60 @@ __global__ void __launch_bounds__(64, (assoc_waves<KPL, SP, WIDE>())) k_sample_a
     if (lane < end - W.cb) A.zr_new[W.cb + lane] = W.out_c;
 }
 
+// Launched twice per sweep, once per width of the shadow-base rows; the
+// launch that does not match the flag set by the rebuild returns.  As in the
+// plain sampler, the 16-bit width takes one workgroup per document (each XCD
+// a contiguous range) and the 32-bit width runs as a persistent grid whose
+// workgroups claim their XCD's documents one at a time.
+template <int KPL, int SP, bool WIDE, bool BIGQ>
+__global__ void __launch_bounds__(64, (assoc_waves<KPL, SP, WIDE>())) k_sample_assoc(AssocArgs A)
+{
+    __shared__ int32_t c_lds[64 * KPL];
+    __shared__ float f0_lds[64 * KPL];
+    __shared__ float f1_lds[64 * KPL];
+    __shared__ __attribute__((aligned(16))) float a0_lds[64 * KPL];
+    __shared__ __attribute__((aligned(16))) float a1_lds[64 * KPL];
+
+    if ((*A.wide != 0) != WIDE) return;
+    if constexpr (!WIDE) {
+        const int32_t bidx = blockIdx.x;
+        const int32_t d = (bidx & 7) * A.docs_per_xcd + (bidx >> 3);
+        if (d >= A.D) return;
+        sample_doc_assoc<KPL, SP, WIDE, BIGQ>(A, d, c_lds, f0_lds, f1_lds, a0_lds, a1_lds);
+    } else {
+        const int32_t xcd = blockIdx.x & 7;
+        for (;;) {
+            int32_t i = 0;
+            if (threadIdx.x == 0) i = atomicAdd(&A.claim[xcd], 1);
+            i = __shfl(i, 0);
+            if (i >= A.docs_per_xcd) break;
+            const int32_t d = xcd * A.docs_per_xcd + i;
+            if (d >= A.D) break;
+            sample_doc_assoc<KPL, SP, WIDE, BIGQ>(A, d, c_lds, f0_lds, f1_lds, a0_lds, a1_lds);
+        }
+        // the last workgroup to finish clears the claims for the next launch
+        if (threadIdx.x == 0) {
+            __threadfence();
+            if (atomicAdd(&A.claim[8], 1) == (int32_t)gridDim.x - 1) {
+#pragma unroll 1
+                for (int u = 0; u < 9; ++u) A.claim[u] = 0;
+            }
+        }
+    }
+}
+
 template <int KPL, int SP>
 hipError_t launch_assoc_kpl(const AssocArgs &A, hipStream_t st)
 {
     const unsigned grid = (unsigned)(8 * A.docs_per_xcd);
+    // the persistent launch: at most one workgroup per wavefront slot
+    const unsigned pgrid = grid < 4096u ? grid : 4096u;
     if (A.nQ > kSmallQ) {
         hipLaunchKernelGGL((k_sample_assoc<KPL, SP, false, true>), dim3(grid), dim3(64), 0, st, A);
-        hipLaunchKernelGGL((k_sample_assoc<KPL, SP, true, true>), dim3(grid), dim3(64), 0, st, A);
+        hipLaunchKernelGGL((k_sample_assoc<KPL, SP, true, true>), dim3(pgrid), dim3(64), 0, st, A);
     } else {
         hipLaunchKernelGGL((k_sample_assoc<KPL, SP, false, false>), dim3(grid), dim3(64), 0, st, A);
-        hipLaunchKernelGGL((k_sample_assoc<KPL, SP, true, false>), dim3(grid), dim3(64), 0, st, A);
+        hipLaunchKernelGGL((k_sample_assoc<KPL, SP, true, false>), dim3(pgrid), dim3(64), 0, st, A);
     }
     return hipGetLastError();
 }
@@ -640,6 +678,7 @@ hipError_t launch_sample_assoc(const Model &m, const DeviceBuffers &b, const int
     A.B = b.B;
     A.B16 = b.B16;
     A.wide = b.wide;
+    A.claim = b.claim;
     A.f0 = b.f0;
     A.f1 = b.f1;
     A.fk = b.fk;

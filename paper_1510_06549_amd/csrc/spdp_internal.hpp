@@ -143,6 +143,10 @@ struct DeviceBuffers {
     int32_t *B = nullptr;         // [V][Kp]   shadow-base table counts
     uint16_t *B16 = nullptr;      // [V][Kp]   min(B, 65535): the sampler's copy
     int32_t *wide = nullptr;      // [1] 1 if some B exceeds 65535 (the sampler then reads B)
+    int32_t *claim = nullptr;     // [9] documents claimed per XCD by the samplers' persistent
+                                  // launch (32-bit shadow-base rows) and its finished
+                                  // workgroups; zero between launches (its last workgroup
+                                  // clears them)
     int32_t *perm = nullptr;      // [N] tokens grouped by row (any order inside a row)
     int32_t *row_off = nullptr;   // [G V + 1] offsets of each row's tokens in perm
     int32_t *tok_slot = nullptr;  // [N] each token's slot in the routed state copy zr_b

@@ -134,6 +134,37 @@ def test_shadow_base_counts_beyond_16_bits():
     s.close()
 
 
+def test_shadow_base_beyond_16_bits_with_many_documents():
+    """The 32-bit shadow-base launch at 8 topics per lane (K = 500) over 5 000
+    documents, more than the workgroups of that launch's persistent grid, so
+    that workgroups claim several documents each: 4 groups of 1 250 documents,
+    14 occurrences of word 0 in each, all seated at their own table of topic 0
+    (B[0][0] = 70 000), and 6 other tokens per document at random states."""
+    say("shadow-base count beyond 16 bits, K = 500, 5000 documents")
+    rng = np.random.default_rng(11)
+    V, K = 60, 500
+    docs = []
+    for g in range(4):
+        for _ in range(1250):
+            d = [0] * 14 + list(rng.integers(1, V, size=6))
+            rng.shuffle(d)
+            docs.append((g, d))
+    cp = corpus_from_docs(docs, vocab=V)
+    wl = W(K=K, alpha=0.1, a=0.4, b=20.0, gamma=0.05)
+    s, m = parity.make_pair(cp, wl)
+    z = rng.integers(0, K, size=cp.n_tokens).astype(np.int32)
+    r = np.ones(cp.n_tokens, np.uint8)
+    z[cp.words == 0] = 0
+    s.set_assignments(z, r)
+    _, _, B, _ = s.totals()
+    assert B[0, 0] == 70000
+    for sw in range(2):
+        rep, ch, rp = parity.one_step(s, m, sw, 23)
+        say(f"  sweep {sw}: {rep}")
+    assert s.check() == 0
+    s.close()
+
+
 def test_read_probe_on_a_device_buffer():
     """The read probe measures a device buffer and refuses a range past it."""
     import torch
