@@ -28,7 +28,7 @@
 //               most probable source
 //   k_base16    the 16-bit copy of B the samplers read, min(B, 65535), with a
 //               flag raised when a count does not fit (the samplers then read
-//               B itself)
+//               B itself, the plain one only where the copy saturates)
 //   k_unpack    export of n and t as separate int32 arrays, [k][w] per group
 #include <climits>
 

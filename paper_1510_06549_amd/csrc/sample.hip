@@ -110,22 +110,20 @@ __device__ Exact exact_pair(const ExactCtx &A, int32_t k, int32_t k0, int32_t r0
 }
 
 // The rows one token needs: this lane's slices of its packed count row and
-// of its shadow-base row.
-template <int KPL, bool WIDE>
+// of the 16-bit copy of its shadow-base row, min(B, 65535).
+template <int KPL>
 struct Rows {
-    static constexpr int NB = WIDE ? KPL : (KPL + 1) / 2;
+    static constexpr int NB = (KPL + 1) / 2;
     int32_t n[KPL];
-    uint32_t bw[NB];  // shadow-base counts: one per word, or two 16-bit ones
+    uint32_t bw[NB];  // shadow-base counts, two 16-bit ones per word
     __device__ __forceinline__ int32_t b(int j) const
     {
-        if constexpr (WIDE) return (int32_t)bw[j];
-        else return (int32_t)((bw[j >> 1] >> (16 * (j & 1))) & 0xFFFFu);
+        return (int32_t)((bw[j >> 1] >> (16 * (j & 1))) & 0xFFFFu);
     }
     // the same for a wave-uniform j that is not a compile-time constant
     __device__ __forceinline__ int32_t b_at(int j) const
     {
-        if constexpr (WIDE) return (int32_t)pick(bw, j);
-        else return (int32_t)((pick(bw, j >> 1) >> (16 * (j & 1))) & 0xFFFFu);
+        return (int32_t)((pick(bw, j >> 1) >> (16 * (j & 1))) & 0xFFFFu);
     }
 };
 
@@ -143,18 +141,28 @@ struct DocWave {
     float u_c;
 };
 
-template <int KPL, bool WIDE>
+template <int KPL>
 __device__ __forceinline__ void load_rows(const SampleArgs &A, const DocWave<KPL> &W, int32_t x,
-                                          Rows<KPL, WIDE> &R)
+                                          Rows<KPL> &R)
 {
     const int32_t q = readlane(W.gw_c, x);
     const int64_t wrow = (int64_t)(q - W.gV) * A.Kp;
     // a narrow row as its 16-bit copy (half the bytes), widened at use
     load_count_row<KPL>(R.n, A.nt, A.nt16, q, W.kbase, A.Kp, readlane(W.nar_c, x) != 0);
-    if constexpr (WIDE)
-        load_row<KPL>(reinterpret_cast<int32_t(&)[KPL]>(R.bw), A.B + wrow, W.kbase, A.Kp);
-    else
-        load_half_row<KPL>(R.bw, A.B16 + wrow, W.kbase, A.Kp);
+    load_half_row<KPL>(R.bw, A.B16 + wrow, W.kbase, A.Kp);
+}
+
+// Shadow-base count of this lane's slot j for the fp64 path: in the 32-bit
+// launch a saturated 16-bit cell is read from B itself.
+template <int KPL, bool WIDE>
+__device__ __forceinline__ int32_t exact_b(const SampleArgs &A, const DocWave<KPL> &W, int32_t x,
+                                           const Rows<KPL> &R, int j)
+{
+    int32_t v = R.b_at(j);
+    if constexpr (WIDE) {
+        if (v == 0xFFFF) v = A.B[(int64_t)(readlane(W.gw_c, x) - W.gV) * A.Kp + W.kbase + j];
+    }
+    return v;
 }
 
 // Stream registers of the tokens from W.cb on (lanes past the document's end
@@ -178,7 +186,7 @@ __device__ __forceinline__ void load_stream(const SampleArgs &A, DocWave<KPL> &W
 // token two places ahead into `fill`.
 template <int KPL, bool TRACE, bool WIDE, bool BIGQ>
 __device__ __forceinline__ void sample_token(const SampleArgs &A, DocWave<KPL> &W, int32_t x,
-                                             Rows<KPL, WIDE> &cur, Rows<KPL, WIDE> &fill)
+                                             Rows<KPL> &cur, Rows<KPL> &fill)
 {
     constexpr int NO = 2 * KPL;  // outcomes per lane
     const int32_t lane = W.lane, kbase = W.kbase;
@@ -224,7 +232,7 @@ __device__ __forceinline__ void sample_token(const SampleArgs &A, DocWave<KPL> &
     // unused), requested after the gathers so that waiting for the gathers
     // does not wait for them
     asm volatile("" ::: "memory");
-    load_rows<KPL, WIDE>(A, W, x + 2, fill);
+    load_rows<KPL>(A, W, x + 2, fill);
     __builtin_amdgcn_s_setprio(0);
     // only head of a cell that keeps other customers: point mass
     const int32_t nt0 = readlane(own_nt, k0 / KPL);
@@ -236,6 +244,24 @@ __device__ __forceinline__ void sample_token(const SampleArgs &A, DocWave<KPL> &
         const float doc0 = A.alpha + (float)(W.c_lds[k0] - 1);
         const float m1k0 = doc0 * f1k, m0k0 = doc0 * f0k;
 
+        // Shadow-base counts of the token's word: the 16-bit copy, whose
+        // cells are exact in the 16-bit launch.  In the 32-bit launch (some
+        // count above 65535) a token whose row saturates a cell in any lane
+        // reads the lanes' slices of B itself (a rare, wave-uniform branch
+        // whose load waits for the loads in flight).
+        int32_t bv[KPL];
+#pragma unroll
+        for (int j = 0; j < KPL; ++j) bv[j] = cur.b(j);
+        if constexpr (WIDE) {
+            bool sat = false;
+#pragma unroll
+            for (int j = 0; j < KPL; ++j) sat = sat || (bv[j] == 0xFFFF);
+            if (__ballot(sat)) {
+                const int64_t wrow = (int64_t)(readlane(W.gw_c, x) - W.gV) * A.Kp;
+                load_row<KPL>(bv, A.B + wrow, kbase, A.Kp);
+            }
+        }
+
         // weights and lane-local inclusive prefix sums
         float a0[KPL], a1[KPL];
         lds_row<KPL>(a0, W.a0_lds, lane);
@@ -245,7 +271,7 @@ __device__ __forceinline__ void sample_token(const SampleArgs &A, DocWave<KPL> &
 #pragma unroll
         for (int j = 0; j < KPL; ++j) {
             const bool own = (kbase + j == k0);
-            const float bw = A.gamma + (float)(cur.b(j) - (own ? r0 : 0));
+            const float bw = A.gamma + (float)(bv[j] - (own ? r0 : 0));
             const float m1 = own ? m1k0 : a1[j];
             const float m0 = own ? m0k0 : a0[j];
             const float w1 = m1 * bw * qv[j].y;
@@ -308,7 +334,8 @@ __device__ __forceinline__ void sample_token(const SampleArgs &A, DocWave<KPL> &
                 const int32_t k = kbase + j;
                 if (k >= A.K) break;
                 const Exact e =
-                    exact_pair(X, k, k0, r0, pick(cur.n, j), cur.b_at(j), W.c_lds[k], Ng, Tg);
+                    exact_pair(X, k, k0, r0, pick(cur.n, j),
+                                         exact_b<KPL, WIDE>(A, W, x, cur, j), W.c_lds[k], Ng, Tg);
                 acc64 += e.w1;
                 if (e.w1 > 0.0) last64 = 2 * j;
                 acc64 += e.w0;
@@ -332,7 +359,8 @@ __device__ __forceinline__ void sample_token(const SampleArgs &A, DocWave<KPL> &
                 for (int j = 0; j < KPL; ++j) {
                     const int32_t k = kbase + j;
                     if (k >= A.K) break;
-                    const Exact e = exact_pair(X, k, k0, r0, pick(cur.n, j), cur.b_at(j),
+                    const Exact e = exact_pair(X, k, k0, r0, pick(cur.n, j),
+                                               exact_b<KPL, WIDE>(A, W, x, cur, j),
                                                W.c_lds[k], Ng, Tg);
                     run += e.w1;
                     if (e.w1 > 0.0 && run > target64) {
@@ -438,9 +466,9 @@ __device__ __forceinline__ void sample_doc(const SampleArgs &A, int32_t d, int32
     load_stream<KPL>(A, W, last);
 
     // three row buffers: the current token's and the next two tokens'
-    Rows<KPL, WIDE> ra, rb, rc;
-    load_rows<KPL, WIDE>(A, W, 0, ra);
-    load_rows<KPL, WIDE>(A, W, 1, rb);
+    Rows<KPL> ra, rb, rc;
+    load_rows<KPL>(A, W, 0, ra);
+    load_rows<KPL>(A, W, 1, rb);
     int32_t x = 0;  // position of token i in the stream registers
     for (int64_t i = beg; i < end; i += 3, x += 3) {
         if (x == kChunk) {
