@@ -109,8 +109,8 @@ def test_invalid_arguments():
 
 
 def test_shadow_base_counts_beyond_16_bits():
-    """A shadow-base count above 65535 (the sampler then reads the 32-bit
-    shadow-base rows instead of their 16-bit copy): 4 groups each with 16400
+    """A shadow-base count above 65535 (the sampler's 32-bit launch then
+    reads B itself where the 16-bit copy saturates): 4 groups each with 16400
     occurrences of word 0, all seated at their own table of topic 0, give
     B[0][0] = 65600."""
     say("shadow-base count beyond 16 bits")
@@ -141,6 +141,20 @@ def test_shadow_base_beyond_16_bits_with_many_documents():
     14 occurrences of word 0 in each, all seated at their own table of topic 0
     (B[0][0] = 70 000), and 6 other tokens per document at random states."""
     say("shadow-base count beyond 16 bits, K = 500, 5000 documents")
+    wide_base_case(None)
+
+
+def test_shadow_base_beyond_16_bits_with_word_associations():
+    """The association sampler's 32-bit shadow-base launch in the instance the
+    benchmark runs (K = 500, four sources per word), over more documents than
+    its persistent grid has workgroups: the corpus of the test above, every
+    table of word 0 at topic 0 drawing its first source, which is word 0
+    itself, so the source-keyed count B[0][0] = 70 000."""
+    say("shadow-base count beyond 16 bits, word associations, K = 500")
+    wide_base_case(4)
+
+
+def wide_base_case(sources):
     rng = np.random.default_rng(11)
     V, K = 60, 500
     docs = []
@@ -151,11 +165,15 @@ def test_shadow_base_beyond_16_bits_with_many_documents():
             docs.append((g, d))
     cp = corpus_from_docs(docs, vocab=V)
     wl = W(K=K, alpha=0.1, a=0.4, b=20.0, gamma=0.05)
-    s, m = parity.make_pair(cp, wl)
+    assoc = synth.associations(4, V, sources, 0.3, 5) if sources else None
+    s, m = parity.make_pair(cp, wl, assoc=assoc)
     z = rng.integers(0, K, size=cp.n_tokens).astype(np.int32)
     r = np.ones(cp.n_tokens, np.uint8)
     z[cp.words == 0] = 0
-    s.set_assignments(z, r)
+    if sources:
+        s.set_assignments(z, r, np.zeros(cp.n_tokens, np.uint8))
+    else:
+        s.set_assignments(z, r)
     _, _, B, _ = s.totals()
     assert B[0, 0] == 70000
     for sw in range(2):
