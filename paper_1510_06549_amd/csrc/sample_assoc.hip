@@ -270,8 +270,13 @@ __device__ __forceinline__ void sample_token_assoc(const AssocArgs &A, AWave<KPL
             qv[j] = *reinterpret_cast<const float2 *>(reinterpret_cast<const char *>(A.Q) +
                                                       (ix << 3));
     }
-    const float f0k = A.fk[as_vector(W.gK + k0)];
-    const float f1k = A.fk[as_vector((int64_t)(1 + r0) * A.GK + W.gK + k0)];
+    // removed-customer constants of the own topic (a small table that stays
+    // in cache), requested with the gathers as scalar loads: their addresses
+    // are wave-uniform, so they need no vector memory instruction, and the
+    // weights' LDS reads, which share their wait counter, come late enough
+    // to find them done
+    const float f0k = A.fk[W.gK + k0];
+    const float f1k = A.fk[(int64_t)(1 + r0) * A.GK + W.gK + k0];
     asm volatile("" ::: "memory");
     load_arows<KPL, SP, WIDE>(A, W, x + 1, fill);
 
