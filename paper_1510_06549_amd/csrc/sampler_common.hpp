@@ -218,16 +218,6 @@ __device__ __forceinline__ float readlane_f(float x, int32_t lane)
     return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(x), lane));
 }
 
-// Marks a wave-uniform offset as per-lane, so that the load using it is a
-// vector load: vector loads complete in issue order on one counter, which
-// lets a load issued two tokens ahead be waited for without waiting for the
-// loads issued after it.
-__device__ __forceinline__ int64_t as_vector(int64_t x)
-{
-    asm volatile("" : "+v"(x));
-    return x;
-}
-
 // Wave64 inclusive prefix sum with DPP: Hillis-Steele inside each row of 16
 // lanes (row_shr 1, 2, 4, 8), then row 0's total into row 1 and row 2's into
 // row 3 (row_bcast:15), then lane 31's running total into rows 2 and 3
