@@ -271,10 +271,9 @@ __device__ __forceinline__ void sample_token_assoc(const AssocArgs &A, AWave<KPL
                                                       (ix << 3));
     }
     // removed-customer constants of the own topic (a small table that stays
-    // in cache), requested with the gathers as scalar loads: their addresses
-    // are wave-uniform, so they need no vector memory instruction, and the
-    // weights' LDS reads, which share their wait counter, come late enough
-    // to find them done
+    // in cache), requested with the gathers; their addresses are wave-uniform,
+    // so each is one load from a scalar base address, with no per-lane 64-bit
+    // address arithmetic
     const float f0k = A.fk[W.gK + k0];
     const float f1k = A.fk[(int64_t)(1 + r0) * A.GK + W.gK + k0];
     asm volatile("" ::: "memory");
